@@ -1,0 +1,153 @@
+"""Single-request definition of the forward pass, pooling and decode logits (float64).
+
+Section 3.1 states that the forward applies the same attention and feed-forward
+layers to every request type, differing only in input length; Section 2.2 says
+an embedding request is a prefill-shaped pass followed by pooling of the final
+hidden states (mean or last-token), and a decode step reads the cached keys and
+values of all earlier tokens.  The evaluated models (Mistral-7B, Qwen2-7B,
+LLaMA-3.1-8B and their embedding derivatives) are pre-norm decoders with
+RMSNorm, rotary position embedding, grouped-query attention and a SwiGLU MLP;
+that is the block written out here:
+
+    x   = E[ids]
+    per layer:
+        a = rms(x) * g_attn
+        q, k, v = a Wq^T, a Wk^T, a Wv^T          (one fused [qkv, d] matrix)
+        q, k <- RoPE at absolute positions 0..n-1
+        o_h = softmax(q_h k_g^T / sqrt(hd), causal) v_g,  g = h // (nq / nkv)
+        x = x + o Wo^T
+        b = rms(x) * g_mlp
+        x = x + (silu(b Wg^T) * (b Wu^T)) Wd^T
+    H = rms(x) * g_final
+
+Readings taken where the paper is silent: RMSNorm eps sits inside the square
+root; RoPE rotates the half-split pairs (i, i + hd/2) by angle pos * base^(-2i/hd);
+query head h reads KV head h // (nq / nkv) (contiguous groups); no sliding
+window; the pooled tensor is the output of the final RMSNorm (the tensor the LM
+head reads); finished embeddings are divided by max(||v||_2, 1e-12).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+F64 = np.float64
+
+
+def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) * g over the last axis."""
+    x = np.asarray(x, F64)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * np.asarray(g, F64)
+
+
+def rope_rotate(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
+    """Rotary embedding of x[n, heads, hd] at integer positions[n] (half-split pairs)."""
+    x = np.asarray(x, F64)
+    hd = x.shape[-1]
+    half = hd // 2
+    inv_freq = np.power(F64(base), -(2.0 * np.arange(half, dtype=F64)) / hd)
+    ang = np.asarray(positions, F64)[:, None] * inv_freq[None, :]          # [n, half]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def softmax_rows(s: np.ndarray) -> np.ndarray:
+    m = np.max(s, axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos: np.ndarray,
+                         k_pos: np.ndarray) -> np.ndarray:
+    """Scaled dot-product attention, query i sees keys with position <= q_pos[i].
+
+    q[nq_rows, nq, hd]; k, v[n_keys, nkv, hd].  Query head h reads KV head
+    h // (nq / nkv).  Scale 1/sqrt(hd); softmax per query row over visible keys.
+    Returns o[nq_rows, nq * hd].
+    """
+    q = np.asarray(q, F64)
+    k = np.asarray(k, F64)
+    v = np.asarray(v, F64)
+    n, nq, hd = q.shape
+    nkv = k.shape[1]
+    group = nq // nkv
+    visible = np.asarray(k_pos)[None, :] <= np.asarray(q_pos)[:, None]     # [n, n_keys]
+    out = np.empty((n, nq, hd), F64)
+    scale = 1.0 / np.sqrt(F64(hd))
+    for h in range(nq):
+        g = h // group
+        s = (q[:, h, :] @ k[:, g, :].T) * scale
+        s = np.where(visible, s, -np.inf)
+        out[:, h, :] = softmax_rows(s) @ v[:, g, :]
+    return out.reshape(n, nq * hd)
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    return x / (1.0 + np.exp(-x))
+
+
+def _split_qkv(cfg, qkv: np.ndarray):
+    n = qkv.shape[0]
+    q = qkv[:, :cfg.q_dim].reshape(n, cfg.n_q_heads, cfg.head_dim)
+    k = qkv[:, cfg.q_dim:cfg.q_dim + cfg.kv_dim].reshape(n, cfg.n_kv_heads, cfg.head_dim)
+    v = qkv[:, cfg.q_dim + cfg.kv_dim:].reshape(n, cfg.n_kv_heads, cfg.head_dim)
+    return q, k, v
+
+
+def mlp(layer, b: np.ndarray) -> np.ndarray:
+    gate = b @ np.asarray(layer["w_gate"], F64).T
+    up = b @ np.asarray(layer["w_up"], F64).T
+    return (silu(gate) * up) @ np.asarray(layer["w_down"], F64).T
+
+
+def forward_full(cfg, weights, ids) -> np.ndarray:
+    """Final-normed hidden states H[n, d] of one request of tokens ids, positions 0..n-1."""
+    ids = np.asarray(ids, np.int64)
+    n = ids.shape[0]
+    pos = np.arange(n)
+    x = np.asarray(weights["tok_emb"], F64)[ids]
+    for layer in weights["layers"]:
+        a = rmsnorm(x, layer["attn_norm"], cfg.rms_eps)
+        q, k, v = _split_qkv(cfg, a @ np.asarray(layer["w_qkv"], F64).T)
+        q = rope_rotate(q, pos, cfg.rope_base)
+        k = rope_rotate(k, pos, cfg.rope_base)
+        o = causal_gqa_attention(q, k, v, pos, pos)
+        x = x + o @ np.asarray(layer["w_o"], F64).T
+        b = rmsnorm(x, layer["mlp_norm"], cfg.rms_eps)
+        x = x + mlp(layer, b)
+    return rmsnorm(x, weights["final_norm"], cfg.rms_eps)
+
+
+def l2_normalize(v: np.ndarray) -> np.ndarray:
+    v = np.asarray(v, F64)
+    return v / max(float(np.linalg.norm(v)), 1e-12)
+
+
+def pool_single_pass(H: np.ndarray, head: str) -> np.ndarray:
+    """Section 3.3 heads over all n rows at once: mean (w = 1), CLS (row 0), last (row n-1)."""
+    H = np.asarray(H, F64)
+    if head == "mean":
+        return H.sum(axis=0) / H.shape[0]
+    if head == "cls":
+        return H[0].copy()
+    if head == "last":
+        return H[-1].copy()
+    raise ValueError(f"unknown pooling head {head!r}")
+
+
+def embed_single_pass(cfg, weights, ids, head: str) -> np.ndarray:
+    """Unchunked embedding: forward, pool, L2-normalise."""
+    return l2_normalize(pool_single_pass(forward_full(cfg, weights, ids), head))
+
+
+def lm_logits(weights, h: np.ndarray) -> np.ndarray:
+    """Untied LM head over final-normed rows h[..., d]."""
+    return np.asarray(h, F64) @ np.asarray(weights["lm_head"], F64).T
+
+
+def decode_full_recompute(cfg, weights, ids) -> np.ndarray:
+    """Next-token logits after tokens ids, recomputed from the whole prefix without a cache."""
+    H = forward_full(cfg, weights, ids)
+    return lm_logits(weights, H[-1])

@@ -1,0 +1,392 @@
+"""Pins of the CPU oracle against things other than itself (no GPU).
+
+* an independent scalar-loop forward (tests/bruteforce.py) at tiny shapes;
+* a third-party implementation of the same model family (transformers' Llama);
+* closed forms and invariants of rotary embedding, softmax attention and pooling;
+* the equivalences the paper states for the method (Section 3.3 and the pooling
+  equivalence table in the appendix): chunked embedding with incremental pooling
+  equals single-pass embedding, decode through the cache equals recomputation
+  from the prefix, and a mixed batch equals each request run alone.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import OracleKV, StepError, step_oracle
+from workload import (Batch, DecodeRow, EmbChunk, ModelConfig, PagedKV, draw_tokens,
+                      make_weights, tiny_config)
+from tests import bruteforce
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def micro_config(**kw):
+    base = dict(n_layers=2, d_model=16, n_q_heads=4, n_kv_heads=2, head_dim=4, d_ff=24,
+                vocab=32, dtype="f32")
+    base.update(kw)
+    return ModelConfig(**base)
+
+
+def sharp_weights(cfg, seed):
+    # larger spread so attention is far from uniform and position errors show
+    return make_weights(cfg, seed, std=0.3, qk_std=0.6)
+
+
+# ---------------------------------------------------------------------------
+# forward pass vs independent implementations
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("nkv", [1, 2, 4])
+def test_forward_matches_scalar_loops(nkv):
+    cfg = micro_config(n_kv_heads=nkv)
+    W = sharp_weights(cfg, 5 + nkv)
+    ids = draw_tokens(3, nkv, 7, cfg.vocab)
+    H = oracle.forward_full(cfg, W, ids)
+    Hb = np.array(bruteforce.forward(cfg, W, ids.tolist()))
+    np.testing.assert_allclose(H, Hb, rtol=1e-11, atol=1e-12)
+    lg = oracle.lm_logits(W, H[-1])
+    np.testing.assert_allclose(lg, np.array(bruteforce.logits(W, Hb[-1].tolist())), rtol=1e-11,
+                               atol=1e-12)
+
+
+def _hf_llama(cfg, W):
+    torch = pytest.importorskip("torch")
+    tf = pytest.importorskip("transformers")
+    c = tf.LlamaConfig(vocab_size=cfg.vocab, hidden_size=cfg.d_model,
+                       intermediate_size=cfg.d_ff, num_hidden_layers=cfg.n_layers,
+                       num_attention_heads=cfg.n_q_heads, num_key_value_heads=cfg.n_kv_heads,
+                       head_dim=cfg.head_dim, rms_norm_eps=cfg.rms_eps, rope_theta=cfg.rope_base,
+                       tie_word_embeddings=False, attention_bias=False, mlp_bias=False,
+                       max_position_embeddings=4096)
+    c._attn_implementation = "eager"
+    m = tf.LlamaForCausalLM(c).to(torch.float64).eval()
+    t = lambda a: torch.tensor(np.asarray(a, np.float64))
+    with torch.no_grad():
+        m.model.embed_tokens.weight.copy_(t(W["tok_emb"]))
+        m.model.norm.weight.copy_(t(W["final_norm"]))
+        m.lm_head.weight.copy_(t(W["lm_head"]))
+        for l, lw in enumerate(W["layers"]):
+            L = m.model.layers[l]
+            qd, kd = cfg.q_dim, cfg.kv_dim
+            L.self_attn.q_proj.weight.copy_(t(lw["w_qkv"][:qd]))
+            L.self_attn.k_proj.weight.copy_(t(lw["w_qkv"][qd:qd + kd]))
+            L.self_attn.v_proj.weight.copy_(t(lw["w_qkv"][qd + kd:]))
+            L.self_attn.o_proj.weight.copy_(t(lw["w_o"]))
+            L.mlp.gate_proj.weight.copy_(t(lw["w_gate"]))
+            L.mlp.up_proj.weight.copy_(t(lw["w_up"]))
+            L.mlp.down_proj.weight.copy_(t(lw["w_down"]))
+            L.input_layernorm.weight.copy_(t(lw["attn_norm"]))
+            L.post_attention_layernorm.weight.copy_(t(lw["mlp_norm"]))
+    return m
+
+
+@pytest.mark.parametrize("shape", ["micro_gqa", "tiny"])
+def test_forward_matches_transformers_llama(shape):
+    torch = pytest.importorskip("torch")
+    if shape == "micro_gqa":
+        cfg = micro_config(n_kv_heads=2, head_dim=8, d_model=32, d_ff=40)
+        n = 40
+    else:
+        cfg = tiny_config()
+        n = 70
+    W = sharp_weights(cfg, 11)
+    ids = draw_tokens(4, 0, n, cfg.vocab)
+    m = _hf_llama(cfg, W)
+    with torch.no_grad():
+        out = m(torch.tensor(ids[None].astype(np.int64)), output_hidden_states=True)
+    H = oracle.forward_full(cfg, W, ids)
+    logits = oracle.lm_logits(W, H)
+    # transformers evaluates the rotary angles in float32 (about 1e-7 rad per unit of
+    # position), which sharp attention amplifies to ~2e-5 of the output scale; a wrong
+    # convention (pairing, sign, head grouping, norm placement) is off by O(1)
+    ref = out.logits[0].numpy()
+    assert np.max(np.abs(logits - ref)) <= 1e-4 * np.max(np.abs(ref))
+    Href = out.hidden_states[-1][0].numpy()
+    assert np.max(np.abs(H - Href)) <= 1e-4 * np.max(np.abs(Href))
+
+
+# ---------------------------------------------------------------------------
+# closed forms and invariants
+# ---------------------------------------------------------------------------
+def test_rope_identity_norm_and_relative_position():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((1, 3, 64))
+    np.testing.assert_array_equal(oracle.rope_rotate(x, np.array([0]), 10000.0), x)
+    for p in (1, 17, 1000, 8191):
+        y = oracle.rope_rotate(x, np.array([p]), 10000.0)
+        np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1),
+                                   rtol=1e-13)
+    q = rng.standard_normal((1, 1, 64))
+    k = rng.standard_normal((1, 1, 64))
+    dots = []
+    for m_, n_ in ((5, 2), (105, 102), (4003, 4000)):
+        qm = oracle.rope_rotate(q, np.array([m_]), 10000.0)
+        kn = oracle.rope_rotate(k, np.array([n_]), 10000.0)
+        dots.append(float(np.sum(qm * kn)))
+    np.testing.assert_allclose(dots, dots[0], rtol=1e-9)
+    # the first pair rotates by exactly `pos` radians, the last by pos * base^(-(hd-2)/hd)
+    e = np.zeros((1, 1, 64))
+    e[0, 0, 0] = 1.0
+    y = oracle.rope_rotate(e, np.array([3]), 10000.0)
+    assert abs(y[0, 0, 0] - math.cos(3.0)) < 1e-15 and abs(y[0, 0, 32] - math.sin(3.0)) < 1e-15
+
+
+def test_attention_closed_forms():
+    rng = np.random.default_rng(1)
+    n, nq, nkv, hd = 9, 4, 2, 8
+    q = rng.standard_normal((n, nq, hd))
+    k = rng.standard_normal((n, nkv, hd))
+    v = rng.standard_normal((n, nkv, hd))
+    pos = np.arange(n)
+    o = oracle.causal_gqa_attention(q, k, v, pos, pos).reshape(n, nq, hd)
+    # the first query sees one key: output is that key's value
+    for h in range(nq):
+        np.testing.assert_allclose(o[0, h], v[0, h // 2], rtol=1e-14)
+    # zero queries give uniform weights: the mean of the visible values
+    o0 = oracle.causal_gqa_attention(np.zeros_like(q), k, v, pos, pos).reshape(n, nq, hd)
+    for i in range(n):
+        np.testing.assert_allclose(o0[i, 3], v[:i + 1, 1].mean(axis=0), rtol=1e-13)
+    # value component = key position: uniform weights give position / 2
+    v2 = np.zeros_like(v)
+    v2[:, :, 0] = pos[:, None]
+    o2 = oracle.causal_gqa_attention(np.zeros_like(q), k, v2, pos, pos).reshape(n, nq, hd)
+    np.testing.assert_allclose(o2[:, 0, 0], pos / 2.0, rtol=1e-14)
+
+
+def test_attention_matches_torch_sdpa():
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    rng = np.random.default_rng(2)
+    n, nq, nkv, hd = 13, 8, 2, 16
+    q = rng.standard_normal((n, nq, hd))
+    k = rng.standard_normal((n, nkv, hd))
+    v = rng.standard_normal((n, nkv, hd))
+    pos = np.arange(n)
+    o = oracle.causal_gqa_attention(q, k, v, pos, pos).reshape(n, nq, hd)
+    tq = torch.tensor(q).permute(1, 0, 2)[None]
+    tk = torch.tensor(k).permute(1, 0, 2)[None]
+    tv = torch.tensor(v).permute(1, 0, 2)[None]
+    ref = F.scaled_dot_product_attention(tq, tk, tv, is_causal=True, enable_gqa=True)
+    np.testing.assert_allclose(o, ref[0].permute(1, 0, 2).numpy(), rtol=1e-12, atol=1e-13)
+
+
+def test_rmsnorm_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((5, 32))
+    g = rng.standard_normal(32)
+    ref = torch.nn.functional.rms_norm(torch.tensor(x), (32,), torch.tensor(g), eps=1e-5)
+    np.testing.assert_allclose(oracle.rmsnorm(x, g, 1e-5), ref.numpy(), rtol=1e-13)
+
+
+def test_zero_layer_model_pools_normed_embeddings():
+    cfg = micro_config(n_layers=0)
+    W = make_weights(cfg, 4)
+    ids = draw_tokens(9, 1, 11, cfg.vocab)
+    E = W["tok_emb"][ids].astype(np.float64)
+    normed = E / np.sqrt((E * E).mean(axis=1, keepdims=True) + cfg.rms_eps)
+    mean = normed.mean(axis=0)
+    out = oracle.embed_single_pass(cfg, W, ids, "mean")
+    np.testing.assert_allclose(out, mean / np.linalg.norm(mean), rtol=1e-13)
+    assert abs(np.linalg.norm(out) - 1.0) < 1e-14
+    same = oracle.pool_single_pass(np.tile(normed[:1], (6, 1)), "mean")
+    np.testing.assert_allclose(same, normed[0], rtol=1e-15)
+    np.testing.assert_array_equal(oracle.l2_normalize(np.zeros(4)), np.zeros(4))
+
+
+# ---------------------------------------------------------------------------
+# the paper's equivalences, through the step contract
+# ---------------------------------------------------------------------------
+def _fresh_kv(cfg, n_seq, max_tokens, seed, n_pages=None):
+    P = cfg.page_size
+    mb = -(-max_tokens // P)
+    if n_pages is None:
+        n_pages = n_seq * mb + 5
+    pk = PagedKV(cfg, n_pages, n_seq, mb, seed)
+    return pk
+
+
+def run_chunked_embedding(cfg, W, ids, C, head, seq=0, seed=0):
+    pk = _fresh_kv(cfg, 1 + seq, len(ids), seed)
+    pk.reserve(seq, len(ids))
+    kv = OracleKV.from_paged(pk)
+    S = np.zeros((1 + seq, cfg.d_model))
+    Wc = np.zeros(1 + seq)
+    out = None
+    for off in range(0, len(ids), C):
+        ln = min(C, len(ids) - off)
+        b = Batch(chunks=[EmbChunk(seq, off, ln, last=off + ln == len(ids), pool=head)],
+                  rows=[], token_ids=ids[off:off + ln])
+        r = step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        S, Wc = r["acc_sum"], r["acc_w"]
+        assert Wc[seq] == off + ln
+        out = r["out_emb"][0]
+    return out, kv, S, Wc
+
+
+@pytest.mark.parametrize("head", ["mean", "last", "cls"])
+@pytest.mark.parametrize("C", [1, 7, 16, 23])
+def test_chunked_equals_single_pass(head, C):
+    cfg = micro_config()
+    W = sharp_weights(cfg, 21)
+    ids = draw_tokens(5, 2, 23, cfg.vocab)
+    ref = oracle.embed_single_pass(cfg, W, ids, head)
+    got, _, _, _ = run_chunked_embedding(cfg, W, ids, C, head)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_pooling_equivalence_table_protocol():
+    """Appendix, pooling-equivalence table: mean and CLS heads at C = 256/512/1024.
+
+    The paper's worst observed agreement (fixture) bounds what the oracle must meet
+    on a random-weight model; in float64 the two paths agree to rounding.
+    """
+    bounds = {}
+    with open(os.path.join(GOLDEN, "pooling_equivalence.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            head, C, min_cos, rel_l2_p99 = line.split()
+            bounds[(head, int(C))] = (float(min_cos), float(rel_l2_p99))
+    assert len(bounds) == 9
+    cfg = micro_config(n_layers=1, d_model=32, head_dim=8, d_ff=32, vocab=64)
+    W = sharp_weights(cfg, 31)
+    ids = draw_tokens(6, 3, 1100, cfg.vocab)
+    for (head, C), (min_cos, p99) in bounds.items():
+        if head == "weighted_mean":
+            continue  # weights undefined in the paper; that head is not built
+        ref = oracle.embed_single_pass(cfg, W, ids, head)
+        got, _, _, _ = run_chunked_embedding(cfg, W, ids, C, head)
+        cos = float(got @ ref / (np.linalg.norm(got) * np.linalg.norm(ref)))
+        rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        assert cos >= min_cos and rel <= p99
+        assert rel < 1e-12
+
+
+def test_decode_through_cache_equals_recompute():
+    cfg = micro_config()
+    W = sharp_weights(cfg, 41)
+    prompt = draw_tokens(7, 0, 21, cfg.vocab)
+    nxt = draw_tokens(7, 1, 4, cfg.vocab)
+    pk = _fresh_kv(cfg, 3, 40, 1)
+    pk.reserve(2, 40)
+    kv = OracleKV.from_paged(pk)
+    S = np.zeros((3, cfg.d_model))
+    Wc = np.zeros(3)
+    # prompt written by a cache-only chunk, then one decode token per step
+    b = Batch(chunks=[EmbChunk(2, 0, len(prompt), False, "none")], rows=[], token_ids=prompt)
+    step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+    seqs = list(prompt)
+    for i, t in enumerate(nxt):
+        b = Batch(chunks=[], rows=[DecodeRow(2, len(seqs))], token_ids=np.array([t], np.int32))
+        r = step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        seqs.append(int(t))
+        ref = oracle.decode_full_recompute(cfg, W, np.array(seqs))
+        np.testing.assert_allclose(r["logits"][0], ref, rtol=1e-11, atol=1e-13)
+
+
+def test_mixed_batch_equals_each_request_alone_and_permutes():
+    cfg = micro_config()
+    W = sharp_weights(cfg, 51)
+    n_seq = 5
+    toks = {s: draw_tokens(8, s, 30, cfg.vocab) for s in range(n_seq)}
+
+    def setup():
+        pk = _fresh_kv(cfg, n_seq, 64, 2)
+        for s in range(n_seq):
+            pk.reserve(s, 40)
+        kv = OracleKV.from_paged(pk)
+        S = np.zeros((n_seq, cfg.d_model))
+        Wc = np.zeros(n_seq)
+        # sequences 2..4 get a prompt through cache-only chunks; 0 and 1 start an embedding
+        for s in (2, 3, 4):
+            n = 10 + 3 * s
+            b = Batch([EmbChunk(s, 0, n, False, "none")], [], toks[s][:n])
+            step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        return kv, S, Wc
+
+    chunks = [EmbChunk(0, 0, 9, False, "mean"), EmbChunk(1, 0, 14, True, "last")]
+    rows = [DecodeRow(2, 16), DecodeRow(3, 19), DecodeRow(4, 22)]
+    ids_c = [toks[0][:9], toks[1][:14]]
+    ids_r = [toks[2][16:17], toks[3][19:20], toks[4][22:23]]
+    kv, S, Wc = setup()
+    mixed = step_oracle((cfg, W), (cfg, W), Batch(chunks, rows, np.concatenate(ids_c + ids_r)),
+                        kv, kv, S, Wc)
+    # alone
+    kv1, S1, W1 = setup()
+    for i, c in enumerate(chunks):
+        r = step_oracle((cfg, W), (cfg, W), Batch([c], [], ids_c[i]), kv1, kv1, S1, W1)
+        S1, W1 = r["acc_sum"], r["acc_w"]
+        if c.last:
+            np.testing.assert_allclose(mixed["out_emb"][i], r["out_emb"][0], rtol=1e-13)
+        np.testing.assert_allclose(mixed["acc_sum"][c.seq], S1[c.seq], rtol=1e-13)
+    for j, row in enumerate(rows):
+        r = step_oracle((cfg, W), (cfg, W), Batch([], [row], ids_r[j]), kv1, kv1, S1, W1)
+        np.testing.assert_allclose(mixed["logits"][j], r["logits"][0], rtol=1e-12)
+    np.testing.assert_array_equal(np.isnan(kv.k), np.isnan(kv1.k))
+    # permuted order permutes outputs
+    kv2, S2, W2 = setup()
+    perm = Batch(chunks[::-1], rows[::-1], np.concatenate(ids_c[::-1] + ids_r[::-1]))
+    r2 = step_oracle((cfg, W), (cfg, W), perm, kv2, kv2, S2, W2)
+    np.testing.assert_allclose(r2["logits"][::-1], mixed["logits"], rtol=1e-12)
+    np.testing.assert_allclose(r2["out_emb"][0], mixed["out_emb"][1], rtol=1e-12)
+
+
+def test_page_coverage_closed_form():
+    """Zero query weights make attention uniform; value channel 0 = key position.
+
+    Then the attention output's channel 0 is exactly pos / 2 for every row, so a
+    dropped, duplicated or misplaced key (wrong page, wrong slot) changes it.
+    """
+    cfg = micro_config(n_layers=1, n_kv_heads=2)
+    W = make_weights(cfg, 61)
+    lw = W["layers"][0]
+    lw["w_qkv"][:cfg.q_dim] = 0.0
+    pk = _fresh_kv(cfg, 2, 80, 3, n_pages=20)
+    pk.reserve(1, 70)
+    # fill positions 0..68 with value channel 0 = position
+    for p in range(69):
+        page = pk.block_table[1, p // 16]
+        pk.k[0, page, :, p % 16, :] = 0.5
+        pk.v[0, page, :, p % 16, :] = 0.0
+        pk.v[0, page, :, p % 16, 0] = p
+    kv = OracleKV.from_paged(pk)
+    # capture the attention output by reading it back from the oracle's internals:
+    # with Wo = identity-like selection we instead check the cached value directly
+    from oracle.model import causal_gqa_attention
+    K, V = kv.read(0, 1, 69)
+    q = np.zeros((1, cfg.n_q_heads, cfg.head_dim))
+    o = causal_gqa_attention(q, K, V, np.array([68]), np.arange(69)).reshape(cfg.n_q_heads, -1)
+    assert o[0, 0] == 34.0
+    assert np.all(np.isnan(kv.k[0, pk.block_table[1, 4], :, 5:, :]))
+
+
+def test_contract_errors():
+    cfg = micro_config()
+    W = make_weights(cfg, 71)
+    pk = _fresh_kv(cfg, 3, 32, 4)
+    pk.reserve(0, 32)
+    kv = OracleKV.from_paged(pk)
+    S = np.zeros((3, cfg.d_model))
+    Wc = np.zeros(3)
+    ids = np.arange(8, dtype=np.int32)
+
+    def kind(b, S=S, Wc=Wc):
+        with pytest.raises(StepError) as e:
+            step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        return e.value.kind
+
+    assert kind(Batch([EmbChunk(0, 0, 4, False), EmbChunk(0, 4, 4, False)], [], ids)) == "dupseq"
+    assert kind(Batch([EmbChunk(0, 0, 7, False)], [DecodeRow(0, 3)], ids)) == "dupseq"
+    assert kind(Batch([EmbChunk(3, 0, 8, False)], [], ids)) == "desc"
+    assert kind(Batch([EmbChunk(0, 0, 8, True, "none")], [], ids)) == "desc"
+    assert kind(Batch([EmbChunk(0, 0, 9, False)], [], ids)) == "desc"
+    assert kind(Batch([EmbChunk(0, 30, 8, False)], [], ids)) == "capacity"
+    assert kind(Batch([EmbChunk(0, 8, 8, False)], [], ids)) == "device"   # W = 0, offset 8
+    assert kind(Batch([EmbChunk(1, 0, 8, False)], [], ids)) == "device"   # no pages
+    assert kind(Batch([], [DecodeRow(1, -1)], ids[:1])) == "desc"
+    bad = ids.copy()
+    bad[0] = cfg.vocab
+    assert kind(Batch([EmbChunk(0, 0, 8, False)], [], bad)) == "desc"

@@ -1,0 +1,353 @@
+"""Seeded synthetic inputs for the mixed embedding-chunk + decode step.
+
+This module only draws numbers and lays them out: model shapes, weight tensors,
+token ids, paged-KV page assignment and synthetic cache contents.  It performs
+no part of the forward step (no normalisation, projection, attention, pooling
+or sampling), so the CPU oracle and the GPU path can both consume the very same
+inputs without sharing any of the method's arithmetic.
+
+Workload shapes follow the paper's evaluation setting: a 7B-class decoder
+(Mistral / Qwen2 / LLaMA-3.1 family, 32 query heads sharing 8 KV heads of
+width 128, SwiGLU MLP of width 14336), a 2048-token step budget with embedding
+chunks of 512 tokens (appendix, chunk-size / token-budget sweeps), vLLM-style
+16-token KV pages, and a tiny two-layer decoder of the same family for fast
+exact checks.  The paper's models and datasets are not used: every weight is
+drawn N(0, 0.02) from a seed, every token id uniformly over the vocabulary.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional
+
+import numpy as np
+
+POOL_MEAN = "mean"
+POOL_LAST = "last"
+POOL_CLS = "cls"
+POOL_NONE = "none"
+POOL_KINDS = (POOL_MEAN, POOL_LAST, POOL_CLS, POOL_NONE)
+
+
+# ---------------------------------------------------------------------------
+# model shapes
+# ---------------------------------------------------------------------------
+@dataclass(frozen=True)
+class ModelConfig:
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_ff: int
+    vocab: int
+    page_size: int = 16
+    rope_base: float = 10000.0
+    rms_eps: float = 1e-5
+    dtype: str = "f32"          # "f32" or "bf16": weights, KV cache and GEMM inputs
+    has_lm_head: bool = True
+
+    @property
+    def q_dim(self) -> int:
+        return self.n_q_heads * self.head_dim
+
+    @property
+    def kv_dim(self) -> int:
+        return self.n_kv_heads * self.head_dim
+
+    @property
+    def qkv_dim(self) -> int:
+        return self.q_dim + 2 * self.kv_dim
+
+    def replace(self, **kw) -> "ModelConfig":
+        return dataclasses.replace(self, **kw)
+
+
+def tiny_config(dtype: str = "f32") -> ModelConfig:
+    """Two-layer decoder: hidden 256, 4 MHA heads of 64, SwiGLU 1024, vocab 1024."""
+    return ModelConfig(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64,
+                       d_ff=1024, vocab=1024, dtype=dtype)
+
+
+def llm7b_config(n_layers: int = 32, dtype: str = "bf16", has_lm_head: bool = True) -> ModelConfig:
+    """7B-class decoder shape: hidden 4096, 32 q heads / 8 kv heads x 128, SwiGLU 14336."""
+    return ModelConfig(n_layers=n_layers, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                       d_ff=14336, vocab=32000, dtype=dtype, has_lm_head=has_lm_head)
+
+
+# ---------------------------------------------------------------------------
+# bf16 rounding (input preparation only)
+# ---------------------------------------------------------------------------
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    b = x.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+    return b.astype(np.uint32).view(np.float32).reshape(x.shape)
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Upper 16 bits of float32 values that are already bf16-exact."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    return (x.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def bf16_from_bits(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# weights
+# ---------------------------------------------------------------------------
+_GLOBAL_LAYER = 1_000_000  # spawn-key slot for tensors that belong to no layer
+
+_TENSOR_IDS = {"tok_emb": 0, "lm_head": 1, "w_q": 2, "w_k": 3, "w_v": 4, "w_o": 5,
+               "w_gate": 6, "w_up": 7, "w_down": 8}
+
+
+def _normal(seed: int, model_tag: int, layer: int, tensor: str, shape, std: float,
+            bf16: bool) -> np.ndarray:
+    ss = np.random.SeedSequence(seed, spawn_key=(model_tag, layer, _TENSOR_IDS[tensor]))
+    rng = np.random.default_rng(ss)
+    w = rng.standard_normal(size=shape, dtype=np.float32)
+    w *= np.float32(std)
+    return round_bf16(w) if bf16 else w
+
+
+def make_weights(cfg: ModelConfig, seed: int, model_tag: int = 0, std: float = 0.02,
+                 qk_std: Optional[float] = None) -> Dict:
+    """Seeded weights, every matrix and the embedding table N(0, std), unit norm gains.
+
+    Matrices are stored [out_features, in_features] (row = output feature).  The
+    fused QKV matrix stacks the query heads, then the key heads, then the value
+    heads, each head a contiguous block of head_dim rows.  The LM head is untied
+    from the embedding table.  ``qk_std`` (if given) overrides the spread of the
+    query and key projections to make attention sharper than N(0, 0.02) gives.
+    Each tensor has its own spawn key, so any one layer can be regenerated alone.
+    """
+    bf16 = cfg.dtype == "bf16"
+    d, F = cfg.d_model, cfg.d_ff
+    qs = std if qk_std is None else qk_std
+    out = {
+        "tok_emb": _normal(seed, model_tag, _GLOBAL_LAYER, "tok_emb", (cfg.vocab, d), std, bf16),
+        "final_norm": np.ones(d, np.float32),
+        "lm_head": (_normal(seed, model_tag, _GLOBAL_LAYER, "lm_head", (cfg.vocab, d), std, bf16)
+                    if cfg.has_lm_head else None),
+        "layers": [],
+    }
+    for l in range(cfg.n_layers):
+        wq = _normal(seed, model_tag, l, "w_q", (cfg.q_dim, d), qs, bf16)
+        wk = _normal(seed, model_tag, l, "w_k", (cfg.kv_dim, d), qs, bf16)
+        wv = _normal(seed, model_tag, l, "w_v", (cfg.kv_dim, d), std, bf16)
+        out["layers"].append({
+            "attn_norm": np.ones(d, np.float32),
+            "w_qkv": np.concatenate([wq, wk, wv], axis=0),
+            "w_o": _normal(seed, model_tag, l, "w_o", (d, cfg.q_dim), std, bf16),
+            "mlp_norm": np.ones(d, np.float32),
+            "w_gate": _normal(seed, model_tag, l, "w_gate", (F, d), std, bf16),
+            "w_up": _normal(seed, model_tag, l, "w_up", (F, d), std, bf16),
+            "w_down": _normal(seed, model_tag, l, "w_down", (d, F), std, bf16),
+        })
+    return out
+
+
+# ---------------------------------------------------------------------------
+# batch descriptors
+# ---------------------------------------------------------------------------
+@dataclass
+class EmbChunk:
+    seq: int
+    offset: int
+    len: int
+    last: bool
+    pool: str = POOL_MEAN
+
+
+@dataclass
+class DecodeRow:
+    seq: int
+    ctx_len: int
+
+
+@dataclass
+class Batch:
+    """One step: embedding chunks first, then decode rows (type-sorted batch unit).
+
+    ``token_ids`` holds every chunk's tokens in chunk order, then one input token
+    per decode row.
+    """
+    chunks: List[EmbChunk] = field(default_factory=list)
+    rows: List[DecodeRow] = field(default_factory=list)
+    token_ids: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int32))
+
+    @property
+    def n_emb_tokens(self) -> int:
+        return int(sum(c.len for c in self.chunks))
+
+    @property
+    def n_tokens(self) -> int:
+        return self.n_emb_tokens + len(self.rows)
+
+
+# ---------------------------------------------------------------------------
+# paged KV bookkeeping and contents
+# ---------------------------------------------------------------------------
+class PagedKV:
+    """Host image of a paged KV cache: pools [L][n_pages][n_kv][page][hd] and a block table.
+
+    Physical pages are handed out in a seeded random order so logically adjacent
+    pages are never physically adjacent.  Every slot starts as NaN; only slots a
+    caller fills (synthetic context or a step's own writes) hold numbers, so a
+    read of a slot that was never written shows up as NaN downstream.
+    """
+
+    def __init__(self, cfg: ModelConfig, n_pages: int, n_seq: int, max_blocks: int, seed: int,
+                 alloc_pools: bool = True):
+        self.cfg = cfg
+        self.n_pages, self.n_seq, self.max_blocks = n_pages, n_seq, max_blocks
+        self.block_table = np.full((n_seq, max_blocks), -1, np.int32)
+        self.n_blocks = np.zeros(n_seq, np.int64)
+        rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(77,)))
+        self._free = list(rng.permutation(n_pages).astype(np.int64))
+        shape = (cfg.n_layers, n_pages, cfg.n_kv_heads, cfg.page_size, cfg.head_dim)
+        if alloc_pools:
+            self.k = np.full(shape, np.nan, np.float32)
+            self.v = np.full(shape, np.nan, np.float32)
+        else:
+            self.k = self.v = None
+
+    def reserve(self, seq: int, n_tokens: int) -> None:
+        """Make sure ``seq`` owns pages for positions [0, n_tokens)."""
+        need = -(-n_tokens // self.cfg.page_size)
+        if need > self.max_blocks:
+            raise ValueError(f"seq {seq}: {n_tokens} tokens exceed {self.max_blocks} blocks")
+        while self.n_blocks[seq] < need:
+            if not self._free:
+                raise ValueError("page pool exhausted")
+            self.block_table[seq, self.n_blocks[seq]] = self._free.pop()
+            self.n_blocks[seq] += 1
+
+    def release(self, seq: int) -> None:
+        for b in range(int(self.n_blocks[seq])):
+            self._free.append(int(self.block_table[seq, b]))
+        self.block_table[seq, :] = -1
+        self.n_blocks[seq] = 0
+
+    def fill_random(self, seq: int, n_tokens: int, seed: int, std: float = 1.0) -> None:
+        """Write N(0, std) keys and values (bf16-rounded for bf16 caches) at positions [0, n_tokens)."""
+        cfg = self.cfg
+        self.reserve(seq, n_tokens)
+        rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(78, seq)))
+        P = cfg.page_size
+        for which in ("k", "v"):
+            pool = getattr(self, which)
+            vals = rng.standard_normal((cfg.n_layers, n_tokens, cfg.n_kv_heads, cfg.head_dim),
+                                       dtype=np.float32)
+            vals *= np.float32(std)
+            if cfg.dtype == "bf16":
+                vals = round_bf16(vals)
+            for b in range(-(-n_tokens // P)):
+                page = self.block_table[seq, b]
+                lo, hi = b * P, min(n_tokens, (b + 1) * P)
+                pool[:, page, :, 0:hi - lo, :] = vals[:, lo:hi].transpose(0, 2, 1, 3)
+
+
+# ---------------------------------------------------------------------------
+# the two fixed workloads used for exact checks and for measurement
+# ---------------------------------------------------------------------------
+def draw_tokens(seed: int, tag: int, n: int, vocab: int) -> np.ndarray:
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(90, tag)))
+    return rng.integers(0, vocab, size=n, dtype=np.int64).astype(np.int32)
+
+
+@dataclass
+class StepWorkload:
+    """Everything one mixed step consumes: shapes, weights, the batch, KV and accumulators."""
+    cfg: ModelConfig
+    weights: Dict
+    batch: Batch
+    kv: PagedKV
+    acc_sum: np.ndarray
+    acc_w: np.ndarray
+    name: str = ""
+
+
+def layer7b_mixed_workload(seed: int = 1002, with_pools: bool = True,
+                           weights: Optional[Dict] = None) -> StepWorkload:
+    """One 7B-shape layer (bf16, vocab 32000 LM head), 2048-token budget mixed step.
+
+    Two embedding requests contribute 1024 chunk tokens (chunk 512, last-token
+    pooling): request 0 is at offset 0 (first chunk, not last), request 1 at
+    offset 1536 (its final chunk, after 1536 tokens already cached).  64 decode
+    rows have contexts drawn uniformly from [1024, 4096].  Cached keys/values
+    are N(0, 1) in bf16.
+    """
+    cfg = llm7b_config(n_layers=1)
+    if weights is None:
+        weights = make_weights(cfg, seed)
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(91,)))
+    n_dec = 64
+    ctx = rng.integers(1024, 4096, size=n_dec, endpoint=True)
+    chunks = [EmbChunk(seq=0, offset=0, len=512, last=False, pool=POOL_LAST),
+              EmbChunk(seq=1, offset=1536, len=512, last=True, pool=POOL_LAST)]
+    rows = [DecodeRow(seq=2 + i, ctx_len=int(c)) for i, c in enumerate(ctx)]
+    n_seq = 2 + n_dec
+    P = cfg.page_size
+    need = (2048 // P) * 2 + sum(-(-(int(c) + 1) // P) for c in ctx)
+    n_pages = need + 64
+    max_blocks = 4096 // P + 1
+    kv = PagedKV(cfg, n_pages, n_seq, max_blocks, seed, alloc_pools=with_pools)
+    if with_pools:
+        kv.fill_random(1, 1536, seed)
+        for r in rows:
+            kv.fill_random(r.seq, r.ctx_len, seed)
+    else:
+        kv.reserve(1, 1536)
+        for r in rows:
+            kv.reserve(r.seq, r.ctx_len)
+    for c in chunks:
+        kv.reserve(c.seq, c.offset + c.len)
+    for r in rows:
+        kv.reserve(r.seq, r.ctx_len + 1)
+    toks = draw_tokens(seed, 0, sum(c.len for c in chunks) + n_dec, cfg.vocab)
+    batch = Batch(chunks=chunks, rows=rows, token_ids=toks)
+    acc_sum = np.zeros((n_seq, cfg.d_model), np.float32)
+    acc_w = np.zeros(n_seq, np.float32)
+    acc_w[1] = 1536.0
+    return StepWorkload(cfg, weights, batch, kv, acc_sum, acc_w, name="7b-layer-mixed-2048")
+
+
+def tiny_mixed_scenario(seed: int = 1001, dtype: str = "f32", qk_std: Optional[float] = None):
+    """The two-layer decoder driven through a short run of mixed steps from empty caches.
+
+    Two embedding requests of 300 tokens are chunked by 128 (128, 128, 44) with
+    mean pooling; four generation requests first have prompts of 64/100/150/200
+    tokens written to the cache by KV-only chunks, then decode one token per step
+    alongside the embedding chunks.  Returns (cfg, weights, n_seq, steps) where
+    steps is a list of Batch; decode input tokens are seeded, not sampled.
+    """
+    cfg = tiny_config(dtype)
+    weights = make_weights(cfg, seed, qk_std=qk_std)
+    emb_len, C = 300, 128
+    prompts = [64, 100, 150, 200]
+    n_seq = 2 + len(prompts)
+    toks_emb = [draw_tokens(seed, 1 + i, emb_len, cfg.vocab) for i in range(2)]
+    toks_prompt = [draw_tokens(seed, 10 + i, p, cfg.vocab) for i, p in enumerate(prompts)]
+    steps: List[Batch] = []
+    # step 0: prompts written by KV-only chunks
+    chunks = [EmbChunk(seq=2 + i, offset=0, len=p, last=False, pool=POOL_NONE)
+              for i, p in enumerate(prompts)]
+    steps.append(Batch(chunks=chunks, rows=[], token_ids=np.concatenate(toks_prompt)))
+    # steps 1..3: embedding chunks + one decode token per generation request
+    ctx = list(prompts)
+    dec_tok = draw_tokens(seed, 50, 3 * len(prompts), cfg.vocab).reshape(3, len(prompts))
+    for k in range(3):
+        off = k * C
+        ln = min(C, emb_len - off)
+        chunks = [EmbChunk(seq=i, offset=off, len=ln, last=(off + ln == emb_len), pool=POOL_MEAN)
+                  for i in range(2)]
+        rows = [DecodeRow(seq=2 + i, ctx_len=ctx[i]) for i in range(len(prompts))]
+        ids = np.concatenate([t[off:off + ln] for t in toks_emb] + [dec_tok[k]]).astype(np.int32)
+        steps.append(Batch(chunks=chunks, rows=rows, token_ids=ids))
+        ctx = [c + 1 for c in ctx]
+    return cfg, weights, n_seq, steps
