@@ -1,0 +1,192 @@
+/*
+ * orthrus.h -- C ABI of the mixed embedding-chunk + decode step on one MI355X (gfx950).
+ *
+ * One call of orthrus_step() is the body of the heterogeneous-batching inference loop
+ * (Algorithm 1) minus scheduling and sampling: a single forward pass over a type-sorted
+ * batch holding embedding chunks and generation decode tokens (Section 3.2, "Batch
+ * Unit"), followed by the incremental pooler on the embedding slice (Section 3.3,
+ * Eq. (1)-(2) and the positional heads) and the LM head on the decode slice.  Every
+ * request type shares the same attention and feed-forward layers (Section 3.1).
+ *
+ * Model family: pre-norm decoder with RMSNorm, rotary position embedding (half-split
+ * pairs, angle = pos * base^(-2i/head_dim)), grouped-query attention (query head h reads
+ * KV head h / (n_q_heads / n_kv_heads)), SwiGLU MLP, untied LM head.
+ *
+ * Conventions shared by every entry point:
+ *   - All "device" pointers are HIP device memory on the current device; all "host"
+ *     pointers are ordinary host memory.  The caller owns every buffer; the library
+ *     never frees caller memory.  orthrus_step() allocates no device memory.
+ *   - Matrices are row-major.  Weight matrices are [out_features][in_features].
+ *   - dtype ORTHRUS_BF16: weights, KV cache, GEMM inputs in bfloat16; accumulation,
+ *     softmax, norm statistics and the residual stream in fp32; logits, pooling state
+ *     and embeddings in fp32.  dtype ORTHRUS_F32: everything fp32.
+ *   - Return value: ORTHRUS_OK (0) or a negative ORTHRUS_E* code.  On a nonzero return
+ *     nothing has been enqueued and no caller buffer has been touched.
+ */
+#ifndef ORTHRUS_H
+#define ORTHRUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define ORTHRUS_OK 0
+#define ORTHRUS_EINVAL (-1)       /* null pointer, negative count, malformed config   */
+#define ORTHRUS_EDESC (-2)        /* bad seq / offset / len / ctx_len / flags / token */
+#define ORTHRUS_EDUPSEQ (-3)      /* a sequence appears twice in one batch             */
+#define ORTHRUS_ECAPACITY (-4)    /* block table or workspace too small for the batch  */
+#define ORTHRUS_EUNSUPPORTED (-5) /* shape or dtype without a kernel instantiation     */
+#define ORTHRUS_EHIP (-6)         /* a HIP runtime call failed                         */
+#define ORTHRUS_EDEVICE (-7)      /* a kernel flagged bad device-side state            */
+
+/* element types */
+#define ORTHRUS_F32 0
+#define ORTHRUS_BF16 1
+
+/* orthrus_emb_chunk.flags: bit 0 = final chunk of its request; bits 1-2 = pooling head */
+#define ORTHRUS_CHUNK_LAST 1
+#define ORTHRUS_POOL_SHIFT 1
+#define ORTHRUS_POOL_MEAN 0 /* S += sum of rows, W += len; emits S / W (Eq. (1)-(2), w = 1) */
+#define ORTHRUS_POOL_LAST 1 /* keeps the last row of the final chunk                      */
+#define ORTHRUS_POOL_CLS 2  /* keeps the first row of the offset-0 chunk                  */
+#define ORTHRUS_POOL_NONE 3 /* writes keys/values only (cache-filling prefill chunk)      */
+
+/* device error bits reported by orthrus_device_error() */
+#define ORTHRUS_DEVERR_PAGE 1 /* block-table entry outside [0, n_pages) on a used block     */
+#define ORTHRUS_DEVERR_ACC 2  /* chunk offset > 0 but the request's W differs from offset */
+
+/* Model shape.  Supported: head_dim 64 or 128; n_q_heads a multiple of n_kv_heads with
+ * group size 1, 2 or 4; d_model and d_ff multiples of 256 (bf16) or 64 (f32); page_size 16. */
+typedef struct orthrus_config {
+    int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab, page_size;
+    float rope_base, rms_eps;
+    int32_t dtype; /* ORTHRUS_F32 or ORTHRUS_BF16 */
+} orthrus_config;
+
+/* Per-layer weights (device).  w_qkv: [(nq + 2 nkv) * hd][d] with the query heads, then the
+ * key heads, then the value heads, each head hd contiguous rows.  w_o: [d][nq * hd].
+ * w_gate, w_up: [d_ff][d].  w_down: [d][d_ff].  Norm gains are fp32 [d]. */
+typedef struct orthrus_layer_weights {
+    const float *attn_norm;
+    const void *w_qkv;
+    const void *w_o;
+    const float *mlp_norm;
+    const void *w_gate;
+    const void *w_up;
+    const void *w_down;
+} orthrus_layer_weights;
+
+/* Model weights.  tok_emb [vocab][d] and lm_head [vocab][d] (may be NULL for an embedding-only
+ * model) are device memory of the model dtype; final_norm is fp32 [d] device memory.  `layers`
+ * is a HOST array of n_layers entries, copied by orthrus_model_create(). */
+typedef struct orthrus_weights {
+    const void *tok_emb;
+    const float *final_norm;
+    const void *lm_head;
+    const orthrus_layer_weights *layers;
+} orthrus_weights;
+
+typedef struct orthrus_model orthrus_model; /* opaque host-side handle */
+
+/* One embedding chunk: tokens at positions [offset, offset + len) of request `seq`
+ * (Section 3.3: the n-token input split into chunks c_1..c_K across iterations). */
+typedef struct orthrus_emb_chunk {
+    int32_t seq, offset, len, flags;
+} orthrus_emb_chunk;
+
+/* One generation decode token: `ctx_len` tokens of request `seq` are already cached; the
+ * input token sits at position ctx_len, its key/value are appended there and it attends to
+ * ctx_len + 1 keys including its own. */
+typedef struct orthrus_decode_row {
+    int32_t seq, ctx_len;
+} orthrus_decode_row;
+
+/* The batch (HOST memory).  token_ids holds sum(len) chunk tokens in chunk order, then one
+ * input token per decode row: the type-sorted layout of Section 3.2. */
+typedef struct orthrus_batch {
+    int32_t n_chunks, n_decode;
+    const orthrus_emb_chunk *chunks;
+    const orthrus_decode_row *rows;
+    const int32_t *token_ids;
+} orthrus_batch;
+
+/* A paged KV cache (device).  k_cache, v_cache: [n_layers][n_pages][n_kv_heads][page][hd] of
+ * the model dtype (keys stored after rotation).  block_table: int32 [n_seq][max_blocks]; the
+ * slot of position p of request s is block_table[s][p / page] * page + p % page. */
+typedef struct orthrus_kv {
+    void *k_cache;
+    void *v_cache;
+    const int32_t *block_table;
+    int32_t n_pages, n_seq, max_blocks;
+} orthrus_kv;
+
+/* Validates `cfg` (EINVAL / EUNSUPPORTED) and `w` (EINVAL on a null pointer other than
+ * lm_head) and returns a host handle that keeps copies of both.  No device work. */
+int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, orthrus_model **out);
+void orthrus_model_destroy(orthrus_model *m);
+
+/* Device workspace bytes for steps of at most max_tokens tokens (chunks + decode rows), at
+ * most max_chunks chunks, at most max_decode decode rows, and decode contexts of at most
+ * max_ctx tokens.  `gen` may equal `emb`.  Returns 0 for invalid arguments. */
+size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *gen, int32_t max_tokens,
+                               int32_t max_chunks, int32_t max_decode, int32_t max_ctx);
+
+/* One mixed step, enqueued on `stream` (a hipStream_t; NULL = default stream); returns after
+ * enqueueing.  Embedding chunks run through `emb` and read/append `emb_kv`; decode rows run
+ * through `gen` (needs an LM head) and read/append `gen_kv`.  `gen` may equal `emb` (shared
+ * backbone) and `gen_kv` may equal `emb_kv`; two distinct models must have equal configs.
+ *   acc_sum  [emb_kv->n_seq][d] fp32 device, acc_w [emb_kv->n_seq] fp32 device: pooling state S,
+ *            W of Eq. (1)-(2) per embedding request, updated in place.  A chunk at offset 0
+ *            resets its request's state; a later chunk requires W == offset (else device error
+ *            ORTHRUS_DEVERR_ACC and the chunk's pooling update is skipped).
+ *   out_logits [n_decode][vocab] fp32 device: next-token logits of each decode row.
+ *   out_emb  [n_chunks][d] fp32 device: row i is written only if chunk i has ORTHRUS_CHUNK_LAST;
+ *            it holds v / max(||v||_2, 1e-12) with v = S / W (mean) or S (last, CLS).
+ *   workspace: device buffer of ws_bytes >= orthrus_workspace_bytes(...) for this batch.
+ * Host-side validation (EINVAL, EDESC, EDUPSEQ, ECAPACITY) runs before anything is enqueued.
+ * One step in flight per workspace.  Outputs are valid once the stream has synchronised. */
+int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                 const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
+                 float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream);
+
+/* Zeroes the device error word at the start of `workspace` (enqueued on `stream`).  Call once
+ * on a freshly allocated workspace before its first step. */
+int orthrus_workspace_init(void *workspace, void *stream);
+
+/* Synchronises `stream`, then reads and clears the device error word of `workspace`.
+ * Returns ORTHRUS_OK, ORTHRUS_EDEVICE (bits in *bits if non-NULL) or ORTHRUS_EHIP. */
+int orthrus_device_error(void *workspace, void *stream, int32_t *bits);
+
+/* Host-side plan of a batch without touching the GPU (for inspection and tests).  Counts the
+ * attention work items the step would launch: n_prefill_items (query tiles of embedding
+ * chunks), n_decode_items (key-range splits of decode rows, one per KV head and split).  If
+ * `items` is non-NULL it receives up to `cap` items of 8 int32 each:
+ *   {kind (0 prefill, 1 decode), chunk or row index, kv head, q_begin or split index,
+ *    q_count or n_splits, key_begin, key_end (exclusive), partial slot or -1}. */
+int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                 const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, int32_t *n_prefill_items,
+                 int32_t *n_decode_items, int32_t *items, int32_t cap);
+
+/* Per-launch kernel timing, for measurement.  Between orthrus_profile_begin() and
+ * orthrus_profile_end() every orthrus_step() whose `emb` is `m` records a hipEvent pair on its
+ * stream around each kernel launch.  orthrus_profile_end() synchronises those events and writes
+ * up to `cap` entries (one per kernel name, in first-launch order) with the launch count and the
+ * summed event time; *n_out receives the number of names.  Returns EHIP on a runtime failure. */
+typedef struct orthrus_kernel_time {
+    char name[32];
+    int32_t launches;
+    double total_ms;
+} orthrus_kernel_time;
+int orthrus_profile_begin(orthrus_model *m);
+int orthrus_profile_end(orthrus_model *m, orthrus_kernel_time *out, int32_t cap, int32_t *n_out);
+
+const char *orthrus_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ORTHRUS_H */

@@ -1,0 +1,18 @@
+"""MI355X (gfx950) implementation of the mixed embedding-chunk + decode step of heterogeneous
+batching: one forward over a type-sorted batch of embedding chunks and decode tokens, with the
+incremental pooler on the embedding slice and the LM head on the decode slice.
+
+The compute lives in liborthrus.so (hand-written HIP kernels behind the C ABI declared in
+include/orthrus.h).  ``_abi`` mirrors that ABI with the same names; ``runtime`` holds device
+memory in torch tensors and marshals arguments.  Build with
+``python -m paper_2609_25405_amd.build``.
+"""
+from ._abi import (LIB_PATH, OrthrusError, load, orthrus_device_error, orthrus_model_create,
+                   orthrus_model_destroy, orthrus_plan, orthrus_profile_begin,
+                   orthrus_profile_end, orthrus_step, orthrus_strerror,
+                   orthrus_workspace_bytes, orthrus_workspace_init)
+
+__all__ = ["LIB_PATH", "OrthrusError", "load", "orthrus_device_error", "orthrus_model_create",
+           "orthrus_model_destroy", "orthrus_plan",
+           "orthrus_profile_begin", "orthrus_profile_end", "orthrus_step", "orthrus_strerror",
+           "orthrus_workspace_bytes", "orthrus_workspace_init"]

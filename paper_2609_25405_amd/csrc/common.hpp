@@ -1,0 +1,121 @@
+// Device helpers shared by the gfx950 kernels: bf16 conversion, MFMA operand types,
+// wave reductions and the launcher declarations each kernel file provides.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace orthrus {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+
+// round-to-nearest-even float -> bf16 bits (inputs here are finite)
+__device__ __forceinline__ uint32_t f2bf_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return f2bf_bits(lo) | (f2bf_bits(hi) << 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16>(bf16 v) {
+    return __uint_as_float((uint32_t)__builtin_bit_cast(uint16_t, v) << 16);
+}
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) {
+    return __builtin_bit_cast(bf16, (uint16_t)f2bf_bits(v));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// sticky device error word (vector atomics only)
+__device__ __forceinline__ void flag_error(int *err, int bit) { atomicOr(err, bit); }
+
+// ---------------------------------------------------------------------------------------
+// launchers (host functions defined next to their kernels)
+// ---------------------------------------------------------------------------------------
+enum GemmEpilogue { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+
+struct GemmArgs {
+    const void *A;   // [M][K] activations, row stride lda (elements)
+    const void *B0;  // [N][K] weights (gate for SwiGLU)
+    const void *B1;  // [N][K] up-projection weights (SwiGLU only)
+    void *out;       // fp32 [M][N] (store/add) or activation dtype [M][N] (SwiGLU)
+    int M, N, K, lda, ldo;
+};
+hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
+
+struct NormArgs {
+    const float *x;         // fp32 residual rows [rows][d]
+    float *x_out;           // gather mode: fp32 rows written here
+    const void *table;      // gather mode: token table [vocab][d] of the model dtype
+    const int32_t *tok;     // gather mode: token per row
+    const float *gain;      // [d]
+    void *y;                // normalised rows [rows][d], model dtype
+    int rows, d;
+    float eps;
+};
+hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t s);
+
+struct RopeArgs {
+    const float *qkv;        // fp32 [T][qkv_dim]
+    void *q_out;             // [T][nq][hd] model dtype
+    const int32_t *pos, *seq;
+    void *k_cache[2], *v_cache[2];          // layer base per pool
+    const int32_t *block_table[2];
+    int n_pages[2], max_blocks[2];
+    int Te;                  // tokens < Te use pool 0, others pool 1
+    int T, nq, nkv, hd, page;
+    float rope_base;
+    int *err;
+};
+hipError_t launch_rope_append(int dtype, const RopeArgs &a, hipStream_t s);
+
+struct AttnArgs {
+    const void *q;            // [T][nq][hd]
+    void *o;                  // [T][nq * hd]
+    const void *k_cache[2], *v_cache[2];
+    const int32_t *block_table[2];
+    int n_pages[2], max_blocks[2];
+    const int32_t *chunks, *rows, *items;
+    float *partials;          // [slot][group][hd + 2]
+    int n_prefill, n_items, Te, nq, nkv, hd, page;
+    int *err;
+};
+hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
+hipError_t launch_attn_combine(int dtype, const AttnArgs &a, int n_decode, hipStream_t s);
+
+struct PoolArgs {
+    const float *x;           // fp32 residual rows of the embedding slice [Te][d]
+    const float *gain;        // final norm gain [d]
+    const int32_t *chunks;
+    float *inv_rms;           // [Te] scratch
+    float *acc_sum, *acc_w, *out_emb;
+    int n_chunks, Te, d;
+    float eps;
+    int *err;
+};
+hipError_t launch_pool(const PoolArgs &a, hipStream_t s);
+
+}  // namespace orthrus

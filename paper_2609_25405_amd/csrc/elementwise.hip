@@ -1,0 +1,208 @@
+// Row-wise kernels of the step: token gather + RMSNorm, RMSNorm, rotary embedding with
+// KV-cache append, and the incremental pooler (Section 3.3) with the final L2 normalisation.
+#include "common.hpp"
+#include "plan.hpp"
+
+namespace orthrus {
+
+namespace {
+
+__device__ __forceinline__ float block_sum(float v, float *red) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v = wave_sum(v);
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float s = 0.f;
+    for (int w = 0; w < nw; ++w) s += red[w];
+    return s;
+}
+
+// y = x / sqrt(mean(x^2) + eps) * gain; gather mode first sets x = table[tok] (fp32 copy kept)
+template <typename T, bool GATHER>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    float ss = 0.f;
+    if (GATHER) {
+        const T *src = (const T *)a.table + (size_t)a.tok[r] * a.d;
+        float *dst = a.x_out + (size_t)r * a.d;
+        for (int i = threadIdx.x; i < a.d; i += 256) {
+            const float v = to_f32(src[i]);
+            dst[i] = v;
+            ss += v * v;
+        }
+    } else {
+        const float *x = a.x + (size_t)r * a.d;
+        for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
+    }
+    const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
+    const float *x = GATHER ? a.x_out + (size_t)r * a.d : a.x + (size_t)r * a.d;
+    T *y = (T *)a.y + (size_t)r * a.d;
+    for (int i = threadIdx.x; i < a.d; i += 256) y[i] = from_f32<T>(x[i] * inv * a.gain[i]);
+}
+
+// q, k rotated at their absolute positions (pairs (i, i + hd/2), angle pos * base^(-2i/hd),
+// evaluated in double), q stored for attention, rotated k and raw v appended to the cache slot
+// block_table[seq][pos / page] * page + pos % page.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
+    __shared__ float cs[64], sn[64];
+    const int t = blockIdx.x;
+    const int half = a.hd / 2;
+    const int pos = a.pos[t];
+    if (threadIdx.x < half) {
+        const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
+        double sv, cv;
+        sincos((double)pos * inv_freq, &sv, &cv);
+        cs[threadIdx.x] = (float)cv;
+        sn[threadIdx.x] = (float)sv;
+    }
+    __syncthreads();
+    const int p = t < a.Te ? 0 : 1;
+    const int seq = a.seq[t];
+    const int page = a.block_table[p][(size_t)seq * a.max_blocks[p] + pos / a.page];
+    const bool ok = page >= 0 && page < a.n_pages[p];
+    if (!ok && threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+    const int qkv_dim = (a.nq + 2 * a.nkv) * a.hd;
+    const float *src = a.qkv + (size_t)t * qkv_dim;
+    const size_t slot = ok ? (((size_t)page * a.nkv) * a.page + pos % a.page) * a.hd : 0;
+    // rotations: (nq + nkv) heads x half pairs
+    for (int w = threadIdx.x; w < (a.nq + a.nkv) * half; w += 256) {
+        const int head = w / half, i = w % half;
+        const float x1 = src[head * a.hd + i], x2 = src[head * a.hd + i + half];
+        const float y1 = x1 * cs[i] - x2 * sn[i];
+        const float y2 = x2 * cs[i] + x1 * sn[i];
+        if (head < a.nq) {
+            T *q = (T *)a.q_out + ((size_t)t * a.nq + head) * a.hd;
+            q[i] = from_f32<T>(y1);
+            q[i + half] = from_f32<T>(y2);
+        } else if (ok) {
+            const int g = head - a.nq;
+            T *k = (T *)a.k_cache[p] + slot + (size_t)g * a.page * a.hd;
+            k[i] = from_f32<T>(y1);
+            k[i + half] = from_f32<T>(y2);
+        }
+    }
+    if (ok) {
+        const float *vs = src + (size_t)(a.nq + a.nkv) * a.hd;
+        for (int w = threadIdx.x; w < a.nkv * a.hd; w += 256) {
+            const int g = w / a.hd, i = w % a.hd;
+            T *v = (T *)a.v_cache[p] + slot + (size_t)g * a.page * a.hd;
+            v[i] = from_f32<T>(vs[w]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------- incremental pooler
+// 1/rms of each embedding-slice row (the final RMSNorm's scale)
+__global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    const float *x = a.x + (size_t)r * a.d;
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
+    const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
+    if (threadIdx.x == 0) a.inv_rms[r] = inv;
+}
+
+__device__ __forceinline__ bool chunk_state_ok(const int32_t *ch, const float *acc_w) {
+    const int seq = ch[0], off = ch[1];
+    return off == 0 || acc_w[seq] == (float)off;
+}
+
+// S update of Eq. (1) for mean (w = 1), positional heads keep their one row.
+// Block = 64 columns x 4 row slices; grid = (chunks, d / 64).
+__global__ __launch_bounds__(256) void pool_accum_kernel(PoolArgs a) {
+    __shared__ float part[4][64];
+    const int ci = blockIdx.x;
+    const int32_t *ch = a.chunks + kChunkInts * ci;
+    const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3], t0 = ch[4];
+    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
+    const bool last = flags & ORTHRUS_CHUNK_LAST;
+    if (pool == ORTHRUS_POOL_NONE) return;
+    if (!chunk_state_ok(ch, a.acc_w)) {
+        if (blockIdx.y == 0 && threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_ACC);
+        return;
+    }
+    const int c = blockIdx.y * 64 + (threadIdx.x & 63), slice = threadIdx.x >> 6;
+    const float gc = a.gain[c];
+    float *S = a.acc_sum + (size_t)seq * a.d + c;
+    if (pool == ORTHRUS_POOL_MEAN) {
+        float s = 0.f;
+        for (int r = slice; r < len; r += 4) s += a.x[(size_t)(t0 + r) * a.d + c] * a.inv_rms[t0 + r];
+        part[slice][threadIdx.x & 63] = s;
+        __syncthreads();
+        if (slice == 0) {
+            const float tot = ((part[0][c & 63] + part[1][c & 63]) + part[2][c & 63]) + part[3][c & 63];
+            *S = (off == 0 ? 0.f : *S) + tot * gc;
+        }
+        return;
+    }
+    if (slice != 0) return;
+    if (pool == ORTHRUS_POOL_LAST) {
+        if (last) *S = a.x[(size_t)(t0 + len - 1) * a.d + c] * a.inv_rms[t0 + len - 1] * gc;
+        else if (off == 0) *S = 0.f;
+    } else {  // CLS
+        if (off == 0) *S = a.x[(size_t)t0 * a.d + c] * a.inv_rms[t0] * gc;
+    }
+}
+
+// W update of Eq. (2) and, for a request's final chunk, v / max(||v||, 1e-12)
+__global__ __launch_bounds__(256) void pool_finish_kernel(PoolArgs a) {
+    __shared__ float red[4];
+    const int ci = blockIdx.x;
+    const int32_t *ch = a.chunks + kChunkInts * ci;
+    const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3];
+    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
+    if (pool == ORTHRUS_POOL_NONE) return;
+    const bool ok = chunk_state_ok(ch, a.acc_w);
+    __syncthreads();
+    if (!ok) return;
+    const float W = (off == 0 ? 0.f : a.acc_w[seq]) + (float)len;
+    __syncthreads();  // every thread has read the old W
+    if (threadIdx.x == 0) a.acc_w[seq] = W;
+    if (!(flags & ORTHRUS_CHUNK_LAST)) return;
+    const float *S = a.acc_sum + (size_t)seq * a.d;
+    const float div = pool == ORTHRUS_POOL_MEAN ? W : 1.f;
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < a.d; i += 256) {
+        const float v = S[i] / div;
+        ss += v * v;
+    }
+    const float nrm = sqrtf(block_sum(ss, red));
+    const float inv = 1.f / fmaxf(nrm, 1e-12f);
+    float *out = a.out_emb + (size_t)ci * a.d;
+    for (int i = threadIdx.x; i < a.d; i += 256) out[i] = (S[i] / div) * inv;
+}
+
+}  // namespace
+
+hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t s) {
+    if (a.rows <= 0) return hipSuccess;
+    if (dtype == 1) {
+        if (gather) hipLaunchKernelGGL((rmsnorm_kernel<bf16, true>), dim3(a.rows), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((rmsnorm_kernel<bf16, false>), dim3(a.rows), dim3(256), 0, s, a);
+    } else {
+        if (gather) hipLaunchKernelGGL((rmsnorm_kernel<float, true>), dim3(a.rows), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((rmsnorm_kernel<float, false>), dim3(a.rows), dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_rope_append(int dtype, const RopeArgs &a, hipStream_t s) {
+    if (a.T <= 0) return hipSuccess;
+    if (dtype == 1) hipLaunchKernelGGL(rope_append_kernel<bf16>, dim3(a.T), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(a.T), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pool(const PoolArgs &a, hipStream_t s) {
+    if (a.n_chunks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(pool_rows_kernel, dim3(a.Te), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(pool_accum_kernel, dim3(a.n_chunks, a.d / 64), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(pool_finish_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace orthrus

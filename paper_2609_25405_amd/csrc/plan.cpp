@@ -1,0 +1,172 @@
+// Host planner for the mixed step (Section 3.2 batch unit, Section 3.3 chunk bookkeeping).
+//
+// Turns the caller's descriptor into the metadata the kernels read: per token its id,
+// absolute position and request; per chunk its request, offset, length, flags and first
+// token; per decode row its request, context and split layout; and the attention work
+// list.  Validation mirrors the step contract: every check here runs before anything is
+// enqueued, so a rejected batch leaves all caller buffers untouched.
+#include "plan.hpp"
+
+#include <algorithm>
+#include <numeric>
+#include <set>
+#include <utility>
+
+namespace orthrus {
+
+int validate_config(const orthrus_config &c) {
+    if (c.n_layers < 0 || c.d_model <= 0 || c.n_q_heads <= 0 || c.n_kv_heads <= 0 ||
+        c.head_dim <= 0 || c.d_ff <= 0 || c.vocab <= 0 || c.page_size <= 0 || !(c.rms_eps > 0.f) ||
+        !(c.rope_base > 1.f))
+        return ORTHRUS_EINVAL;
+    if (c.n_q_heads % c.n_kv_heads) return ORTHRUS_EINVAL;
+    if (c.dtype != ORTHRUS_F32 && c.dtype != ORTHRUS_BF16) return ORTHRUS_EINVAL;
+    const int group = c.n_q_heads / c.n_kv_heads;
+    if (c.head_dim != 64 && c.head_dim != 128) return ORTHRUS_EUNSUPPORTED;
+    if (group != 1 && group != 2 && group != 4) return ORTHRUS_EUNSUPPORTED;
+    if (c.page_size != 16) return ORTHRUS_EUNSUPPORTED;
+    const int align = c.dtype == ORTHRUS_BF16 ? 256 : 64;
+    if (c.d_model % align || c.d_ff % align) return ORTHRUS_EUNSUPPORTED;
+    if ((c.n_q_heads * c.head_dim) % align) return ORTHRUS_EUNSUPPORTED;
+    return ORTHRUS_OK;
+}
+
+int max_splits_for_ctx(int max_ctx, int page_size) {
+    const int pages = (max_ctx + 1 + page_size - 1) / page_size;
+    return std::max(1, (pages + kSplitPages - 1) / kSplitPages);
+}
+
+int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const orthrus_kv &ekv,
+              const orthrus_kv &gkv, StepPlan &p) {
+    if (b.n_chunks < 0 || b.n_decode < 0) return ORTHRUS_EINVAL;
+    if ((b.n_chunks && !b.chunks) || (b.n_decode && !b.rows)) return ORTHRUS_EINVAL;
+    const int P = emb.cfg.page_size;
+    p = StepPlan();
+    p.n_chunks = b.n_chunks;
+    p.D = b.n_decode;
+    p.shared_kv = ekv.k_cache == gkv.k_cache;
+    long long Te = 0;
+    std::set<std::pair<int, int>> seen;  // (namespace, seq)
+    for (int i = 0; i < b.n_chunks; ++i) {
+        const orthrus_emb_chunk &c = b.chunks[i];
+        const int pool = (c.flags >> ORTHRUS_POOL_SHIFT) & 3;
+        if (c.seq < 0 || c.seq >= ekv.n_seq || c.offset < 0 || c.len < 1) return ORTHRUS_EDESC;
+        if (c.flags & ~(ORTHRUS_CHUNK_LAST | (3 << ORTHRUS_POOL_SHIFT))) return ORTHRUS_EDESC;
+        if (pool == ORTHRUS_POOL_NONE && (c.flags & ORTHRUS_CHUNK_LAST)) return ORTHRUS_EDESC;
+        if ((long long)c.offset + c.len > (long long)ekv.max_blocks * P) return ORTHRUS_ECAPACITY;
+        if (!seen.insert({0, c.seq}).second) return ORTHRUS_EDUPSEQ;
+        Te += c.len;
+    }
+    for (int j = 0; j < b.n_decode; ++j) {
+        const orthrus_decode_row &r = b.rows[j];
+        if (r.seq < 0 || r.seq >= gkv.n_seq || r.ctx_len < 0) return ORTHRUS_EDESC;
+        if ((long long)r.ctx_len + 1 > (long long)gkv.max_blocks * P) return ORTHRUS_ECAPACITY;
+        if (!seen.insert({p.shared_kv ? 0 : 1, r.seq}).second) return ORTHRUS_EDUPSEQ;
+    }
+    if (Te + b.n_decode > (1LL << 30)) return ORTHRUS_ECAPACITY;
+    p.Te = (int)Te;
+    p.T = p.Te + p.D;
+    if (p.T > 0 && !b.token_ids) return ORTHRUS_EINVAL;
+    if (p.D > 0 && !gen.w.lm_head) return ORTHRUS_EDESC;
+    for (int t = 0; t < p.T; ++t) {
+        const int v = t < p.Te ? emb.cfg.vocab : gen.cfg.vocab;
+        if (b.token_ids[t] < 0 || b.token_ids[t] >= v) return ORTHRUS_EDESC;
+    }
+
+    const int nkv = emb.cfg.n_kv_heads;
+    const int group = emb.group();
+    const int qrows = kPrefillRows / group;  // tokens per prefill item
+
+    // --- attention work list: prefill query tiles (heaviest first), then decode splits
+    struct Pre { long long work; int chunk, kvh, qb, qn, kend; };
+    std::vector<Pre> pre;
+    for (int i = 0; i < b.n_chunks; ++i) {
+        const orthrus_emb_chunk &c = b.chunks[i];
+        for (int qb = 0; qb < c.len; qb += qrows) {
+            const int qn = std::min(qrows, c.len - qb);
+            const int kend = c.offset + qb + qn;
+            for (int g = 0; g < nkv; ++g) pre.push_back({(long long)kend * qn, i, g, qb, qn, kend});
+        }
+    }
+    std::stable_sort(pre.begin(), pre.end(), [](const Pre &a, const Pre &b2) { return a.work > b2.work; });
+    p.n_prefill = (int)pre.size();
+
+    std::vector<int32_t> rows(kRowInts * p.D);
+    std::vector<int32_t> items(kItemInts * pre.size());
+    for (size_t k = 0; k < pre.size(); ++k) {
+        int32_t *it = &items[kItemInts * k];
+        it[IT_KIND] = 0;
+        it[IT_INDEX] = pre[k].chunk;
+        it[IT_KVHEAD] = pre[k].kvh;
+        it[IT_A] = pre[k].qb;
+        it[IT_B] = pre[k].qn;
+        it[IT_KEY_BEGIN] = 0;
+        it[IT_KEY_END] = pre[k].kend;
+        it[IT_PARTIAL] = -1;
+    }
+    int partial = 0;
+    for (int j = 0; j < p.D; ++j) {
+        const orthrus_decode_row &r = b.rows[j];
+        const int n_keys = r.ctx_len + 1;
+        const int n_pages = (n_keys + P - 1) / P;
+        const int n_splits = (n_pages + kSplitPages - 1) / kSplitPages;
+        rows[kRowInts * j + 0] = r.seq;
+        rows[kRowInts * j + 1] = r.ctx_len;
+        rows[kRowInts * j + 2] = p.Te + j;
+        rows[kRowInts * j + 3] = n_splits;
+        rows[kRowInts * j + 4] = n_splits > 1 ? partial : -1;
+        if (n_splits > 1) p.n_split_rows++;
+        for (int g = 0; g < nkv; ++g) {
+            for (int s = 0; s < n_splits; ++s) {
+                int32_t it[kItemInts];
+                it[IT_KIND] = 1;
+                it[IT_INDEX] = j;
+                it[IT_KVHEAD] = g;
+                it[IT_A] = s;
+                it[IT_B] = n_splits;
+                it[IT_KEY_BEGIN] = s * kSplitPages * P;
+                it[IT_KEY_END] = std::min(n_keys, (s + 1) * kSplitPages * P);
+                // partial slots: [first slot of row][kv head][split], each holding `group` heads
+                it[IT_PARTIAL] = n_splits > 1 ? partial + g * n_splits + s : -1;
+                items.insert(items.end(), it, it + kItemInts);
+            }
+        }
+        if (n_splits > 1) partial += nkv * n_splits;
+    }
+    p.n_decode_items = (int)(items.size() / kItemInts) - p.n_prefill;
+    p.n_partials = partial;
+
+    // --- pack
+    p.off_tok = 0;
+    p.off_pos = p.T;
+    p.off_seq = 2 * p.T;
+    p.off_chunks = 3 * p.T;
+    p.off_rows = p.off_chunks + kChunkInts * p.n_chunks;
+    p.off_items = p.off_rows + kRowInts * p.D;
+    p.meta.assign(p.off_items + items.size(), 0);
+    int t = 0;
+    for (int i = 0; i < b.n_chunks; ++i) {
+        const orthrus_emb_chunk &c = b.chunks[i];
+        int32_t *ch = &p.meta[p.off_chunks + kChunkInts * i];
+        ch[0] = c.seq;
+        ch[1] = c.offset;
+        ch[2] = c.len;
+        ch[3] = c.flags;
+        ch[4] = t;
+        for (int k = 0; k < c.len; ++k, ++t) {
+            p.meta[p.off_tok + t] = b.token_ids[t];
+            p.meta[p.off_pos + t] = c.offset + k;
+            p.meta[p.off_seq + t] = c.seq;
+        }
+    }
+    for (int j = 0; j < p.D; ++j, ++t) {
+        p.meta[p.off_tok + t] = b.token_ids[t];
+        p.meta[p.off_pos + t] = b.rows[j].ctx_len;
+        p.meta[p.off_seq + t] = b.rows[j].seq;
+    }
+    std::copy(rows.begin(), rows.end(), p.meta.begin() + p.off_rows);
+    std::copy(items.begin(), items.end(), p.meta.begin() + p.off_items);
+    return ORTHRUS_OK;
+}
+
+}  // namespace orthrus

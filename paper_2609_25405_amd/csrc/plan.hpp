@@ -1,0 +1,48 @@
+// Host-side planning of one mixed step: descriptor validation, per-token metadata and the
+// attention work list.  Plain C++17, no HIP calls, so it is exercised on machines without a GPU.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "orthrus.h"
+
+namespace orthrus {
+
+// Query-head rows per prefill work item; a work item covers (128 / group) tokens of one
+// chunk times the `group` query heads that share one KV head.
+constexpr int kPrefillRows = 128;
+// Pages of one decode key-range split (16 pages = 256 keys of a 16-token page).
+constexpr int kSplitPages = 16;
+
+struct Model {
+    orthrus_config cfg;
+    orthrus_weights w;
+    std::vector<orthrus_layer_weights> layers;
+    int group() const { return cfg.n_q_heads / cfg.n_kv_heads; }
+    int q_dim() const { return cfg.n_q_heads * cfg.head_dim; }
+    int kv_dim() const { return cfg.n_kv_heads * cfg.head_dim; }
+    int qkv_dim() const { return q_dim() + 2 * kv_dim(); }
+};
+
+// int32 fields of one attention work item
+enum ItemField { IT_KIND = 0, IT_INDEX, IT_KVHEAD, IT_A, IT_B, IT_KEY_BEGIN, IT_KEY_END, IT_PARTIAL };
+constexpr int kItemInts = 8;
+constexpr int kChunkInts = 5;  // seq, offset, len, flags, first token
+constexpr int kRowInts = 5;    // seq, ctx_len, token index, n_splits, first partial slot
+
+struct StepPlan {
+    int T = 0, Te = 0, D = 0, n_chunks = 0;
+    bool shared_kv = true;
+    int n_prefill = 0, n_decode_items = 0, n_partials = 0, n_split_rows = 0;
+    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items
+    std::vector<int32_t> meta;
+    int off_tok = 0, off_pos = 0, off_seq = 0, off_chunks = 0, off_rows = 0, off_items = 0;
+};
+
+int validate_config(const orthrus_config &c);
+int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const orthrus_kv &ekv,
+              const orthrus_kv &gkv, StepPlan &out);
+int max_splits_for_ctx(int max_ctx, int page_size);
+
+}  // namespace orthrus

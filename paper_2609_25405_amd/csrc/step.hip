@@ -1,0 +1,478 @@
+// C ABI of the mixed step: model handles, workspace sizing, and the per-step launch sequence
+// (one iteration of the heterogeneous-batching loop, Algorithm 1, without scheduling and
+// sampling; the forward is shared by all request types, Section 3.1; the pooler and the LM
+// head read contiguous slices of the type-sorted batch, Section 3.2).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+#include "orthrus.h"
+#include "plan.hpp"
+
+struct orthrus_model : public orthrus::Model {
+    // pinned host staging for the per-step metadata upload, double-buffered with events
+    std::mutex mu;
+    void *stage[2] = {nullptr, nullptr};
+    size_t stage_bytes[2] = {0, 0};
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    int next = 0;
+    // kernel timing (orthrus_profile_begin / _end)
+    bool profiling = false;
+    struct Mark { int name; hipEvent_t a, b; };
+    std::vector<std::string> prof_names;
+    std::vector<Mark> marks;
+};
+
+namespace orthrus {
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, total;
+};
+
+Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials) {
+    const size_t es = m.cfg.dtype == ORTHRUS_BF16 ? 2 : 4;
+    const size_t d = m.cfg.d_model;
+    Layout L;
+    size_t o = 0;
+    L.err = o; o += kAlign;
+    L.meta = o; o += up(meta_ints * 4);
+    L.x = o; o += up(T * d * 4);
+    L.act = o; o += up(T * d * es);
+    L.qkv = o; o += up(T * (size_t)m.qkv_dim() * 4);
+    L.q = o; o += up(T * (size_t)m.q_dim() * es);
+    L.o = o; o += up(T * (size_t)m.q_dim() * es);
+    L.u = o; o += up(T * (size_t)m.cfg.d_ff * es);
+    L.inv_rms = o; o += up(T * 4);
+    L.partials = o; o += up(n_partials * (size_t)m.group() * (m.cfg.head_dim + 2) * 4);
+    L.total = o;
+    return L;
+}
+
+bool same_shape(const orthrus_config &a, const orthrus_config &b) {
+    return a.n_layers == b.n_layers && a.d_model == b.d_model && a.n_q_heads == b.n_q_heads &&
+           a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim && a.d_ff == b.d_ff &&
+           a.page_size == b.page_size && a.dtype == b.dtype && a.rope_base == b.rope_base &&
+           a.rms_eps == b.rms_eps;
+}
+
+bool kv_ok(const orthrus_kv *kv) {
+    return kv && kv->k_cache && kv->v_cache && kv->block_table && kv->n_pages > 0 && kv->n_seq > 0 &&
+           kv->max_blocks > 0;
+}
+
+#define HIP_TRY(expr)                                   \
+    do {                                                \
+        if ((expr) != hipSuccess) return ORTHRUS_EHIP;  \
+    } while (0)
+
+int upload_meta(orthrus_model *m, const StepPlan &p, void *dst, hipStream_t s) {
+    std::lock_guard<std::mutex> lk(m->mu);
+    const int i = m->next;
+    m->next ^= 1;
+    const size_t bytes = p.meta.size() * 4;
+    if (m->ev[i]) HIP_TRY(hipEventSynchronize(m->ev[i]));
+    else HIP_TRY(hipEventCreateWithFlags(&m->ev[i], hipEventDisableTiming));
+    if (m->stage_bytes[i] < bytes) {
+        if (m->stage[i]) HIP_TRY(hipHostFree(m->stage[i]));
+        m->stage[i] = nullptr;
+        m->stage_bytes[i] = 0;
+        HIP_TRY(hipHostMalloc(&m->stage[i], bytes * 2, hipHostMallocDefault));
+        m->stage_bytes[i] = bytes * 2;
+    }
+    std::memcpy(m->stage[i], p.meta.data(), bytes);
+    HIP_TRY(hipMemcpyAsync(dst, m->stage[i], bytes, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipEventRecord(m->ev[i], s));
+    return ORTHRUS_OK;
+}
+
+// hipEvent pair around one launch when the model handle is profiling
+struct Prof {
+    orthrus_model *m;
+    hipStream_t s;
+    hipEvent_t a = nullptr;
+    int id = -1;
+    bool on() const { return m && m->profiling; }
+    int begin(const char *name) {
+        if (!on()) return ORTHRUS_OK;
+        std::lock_guard<std::mutex> lk(m->mu);
+        id = -1;
+        for (size_t i = 0; i < m->prof_names.size(); ++i)
+            if (m->prof_names[i] == name) id = (int)i;
+        if (id < 0) {
+            id = (int)m->prof_names.size();
+            m->prof_names.push_back(name);
+        }
+        HIP_TRY(hipEventCreate(&a));
+        HIP_TRY(hipEventRecord(a, s));
+        return ORTHRUS_OK;
+    }
+    int end() {
+        if (!on()) return ORTHRUS_OK;
+        hipEvent_t b = nullptr;
+        HIP_TRY(hipEventCreate(&b));
+        HIP_TRY(hipEventRecord(b, s));
+        std::lock_guard<std::mutex> lk(m->mu);
+        m->marks.push_back({id, a, b});
+        return ORTHRUS_OK;
+    }
+};
+
+size_t layer_stride(const Model &m, const orthrus_kv &kv) {
+    const size_t es = m.cfg.dtype == ORTHRUS_BF16 ? 2 : 4;
+    return (size_t)kv.n_pages * m.cfg.n_kv_heads * m.cfg.page_size * m.cfg.head_dim * es;
+}
+
+}  // namespace
+}  // namespace orthrus
+
+using namespace orthrus;
+
+extern "C" {
+
+const char *orthrus_strerror(int code) {
+    switch (code) {
+        case ORTHRUS_OK: return "ok";
+        case ORTHRUS_EINVAL: return "invalid argument";
+        case ORTHRUS_EDESC: return "malformed batch descriptor";
+        case ORTHRUS_EDUPSEQ: return "sequence appears twice in one batch";
+        case ORTHRUS_ECAPACITY: return "block table or workspace too small";
+        case ORTHRUS_EUNSUPPORTED: return "unsupported shape or dtype";
+        case ORTHRUS_EHIP: return "HIP runtime error";
+        case ORTHRUS_EDEVICE: return "device-side check failed";
+        default: return "unknown status";
+    }
+}
+
+int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, orthrus_model **out) {
+    if (!cfg || !w || !out) return ORTHRUS_EINVAL;
+    *out = nullptr;
+    const int rc = validate_config(*cfg);
+    if (rc) return rc;
+    if (!w->tok_emb || !w->final_norm || (cfg->n_layers > 0 && !w->layers)) return ORTHRUS_EINVAL;
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        const orthrus_layer_weights &lw = w->layers[l];
+        if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.mlp_norm || !lw.w_gate || !lw.w_up || !lw.w_down)
+            return ORTHRUS_EINVAL;
+    }
+    orthrus_model *m = new (std::nothrow) orthrus_model;
+    if (!m) return ORTHRUS_EINVAL;
+    m->cfg = *cfg;
+    m->w = *w;
+    m->layers.assign(w->layers, w->layers + cfg->n_layers);
+    m->w.layers = m->layers.data();
+    *out = m;
+    return ORTHRUS_OK;
+}
+
+void orthrus_model_destroy(orthrus_model *m) {
+    if (!m) return;
+    for (int i = 0; i < 2; ++i) {
+        if (m->ev[i]) {
+            (void)hipEventSynchronize(m->ev[i]);
+            (void)hipEventDestroy(m->ev[i]);
+        }
+        if (m->stage[i]) (void)hipHostFree(m->stage[i]);
+    }
+    delete m;
+}
+
+size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *gen, int32_t max_tokens,
+                               int32_t max_chunks, int32_t max_decode, int32_t max_ctx) {
+    if (!emb || !gen || max_tokens < 0 || max_chunks < 0 || max_decode < 0 || max_ctx < 0) return 0;
+    if (gen != emb && !same_shape(emb->cfg, gen->cfg)) return 0;
+    const Model &m = *emb;
+    const size_t nkv = m.cfg.n_kv_heads;
+    const size_t qrows = kPrefillRows / m.group();
+    const size_t splits = max_splits_for_ctx(max_ctx, m.cfg.page_size);
+    const size_t pre_items = ((size_t)max_tokens / qrows + max_chunks) * nkv;
+    const size_t dec_items = (size_t)max_decode * nkv * splits;
+    const size_t meta = 3 * (size_t)max_tokens + kChunkInts * (size_t)max_chunks +
+                        kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items);
+    return make_layout(m, max_tokens, meta, dec_items).total;
+}
+
+int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                 const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, int32_t *n_prefill_items,
+                 int32_t *n_decode_items, int32_t *items, int32_t cap) {
+    if (!emb || !gen || !batch || !kv_ok(emb_kv) || !kv_ok(gen_kv)) return ORTHRUS_EINVAL;
+    if (gen != emb && !same_shape(emb->cfg, gen->cfg)) return ORTHRUS_EUNSUPPORTED;
+    StepPlan p;
+    const int rc = plan_step(*emb, *gen, *batch, *emb_kv, *gen_kv, p);
+    if (rc) return rc;
+    if (n_prefill_items) *n_prefill_items = p.n_prefill;
+    if (n_decode_items) *n_decode_items = p.n_decode_items;
+    if (items) {
+        const int n = std::min<int>(cap, p.n_prefill + p.n_decode_items);
+        std::memcpy(items, p.meta.data() + p.off_items, (size_t)n * kItemInts * 4);
+    }
+    return ORTHRUS_OK;
+}
+
+int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                 const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
+                 float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream) {
+    if (!emb || !gen || !batch || !workspace || !kv_ok(emb_kv) || !kv_ok(gen_kv)) return ORTHRUS_EINVAL;
+    if (gen != emb && !same_shape(emb->cfg, gen->cfg)) return ORTHRUS_EUNSUPPORTED;
+    if (batch->n_chunks > 0 && (!acc_sum || !acc_w || !out_emb)) return ORTHRUS_EINVAL;
+    if (batch->n_decode > 0 && !out_logits) return ORTHRUS_EINVAL;
+    StepPlan p;
+    int rc = plan_step(*emb, *gen, *batch, *emb_kv, *gen_kv, p);
+    if (rc) return rc;
+    if (p.T == 0) return ORTHRUS_OK;
+    const Model &M = *emb;
+    const orthrus_config &c = M.cfg;
+    const Layout L = make_layout(M, p.T, p.meta.size(), p.n_partials);
+    if (ws_bytes < L.total) return ORTHRUS_ECAPACITY;
+
+    hipStream_t s = (hipStream_t)stream;
+    Prof prof{const_cast<orthrus_model *>(emb), s};
+    auto timed = [&](const char *name, auto &&launch) -> int {
+        int r = prof.begin(name);
+        if (r) return r;
+        if (launch() != hipSuccess) return ORTHRUS_EHIP;
+        return prof.end();
+    };
+#define RUN(name, expr)                                          \
+    do {                                                         \
+        const int r_ = timed(name, [&]() { return (expr); });    \
+        if (r_) return r_;                                       \
+    } while (0)
+    char *ws = (char *)workspace;
+    int *err = (int *)(ws + L.err);
+    const int32_t *meta = (const int32_t *)(ws + L.meta);
+    rc = upload_meta(const_cast<orthrus_model *>(emb), p, ws + L.meta, s);
+    if (rc) return rc;
+
+    const int dt = c.dtype;
+    const size_t es = dt == ORTHRUS_BF16 ? 2 : 4;
+    const int d = c.d_model, T = p.T, Te = p.Te;
+    float *x = (float *)(ws + L.x);
+    char *act = ws + L.act;
+    float *qkv = (float *)(ws + L.qkv);
+    char *qb = ws + L.q;
+    char *ob = ws + L.o;
+    char *ub = ws + L.u;
+    const bool one_model = emb == gen;
+    const int32_t *tok = meta + p.off_tok;
+
+    // row groups: [0, Te) through the embedding model, [Te, T) through the generator
+    struct Group { const orthrus_model *m; int r0, r1; };
+    Group groups[2];
+    int n_groups = 0;
+    if (one_model) groups[n_groups++] = {emb, 0, T};
+    else {
+        if (Te > 0) groups[n_groups++] = {emb, 0, Te};
+        if (T > Te) groups[n_groups++] = {gen, Te, T};
+    }
+
+    auto norm = [&](bool gather, const Group &g, const float *gain) -> hipError_t {
+        NormArgs n{};
+        n.x = x + (size_t)g.r0 * d;
+        n.x_out = x + (size_t)g.r0 * d;
+        n.table = g.m->w.tok_emb;
+        n.tok = tok + g.r0;
+        n.gain = gain;
+        n.y = act + (size_t)g.r0 * d * es;
+        n.rows = g.r1 - g.r0;
+        n.d = d;
+        n.eps = c.rms_eps;
+        return launch_rmsnorm(dt, gather, n, s);
+    };
+    auto gemm = [&](int epi, const Group &g, const char *A, int lda, const void *B0, const void *B1,
+                    void *out, int ldo, size_t out_es, int N, int K) -> hipError_t {
+        GemmArgs ga{};
+        ga.A = A + (size_t)g.r0 * lda * es;
+        ga.B0 = B0;
+        ga.B1 = B1;
+        ga.out = (char *)out + (size_t)g.r0 * ldo * out_es;
+        ga.M = g.r1 - g.r0;
+        ga.N = N;
+        ga.K = K;
+        ga.lda = lda;
+        ga.ldo = ldo;
+        return launch_gemm(dt, epi, ga, s);
+    };
+
+    // token gather fused with the first RMSNorm (the final norm when there are no layers)
+    for (int gi = 0; gi < n_groups; ++gi) {
+        const Group &g = groups[gi];
+        const float *gain = c.n_layers > 0 ? g.m->layers[0].attn_norm : g.m->w.final_norm;
+        RUN("gather_norm", norm(true, g, gain));
+    }
+
+    AttnArgs aa{};
+    aa.q = qb;
+    aa.o = ob;
+    aa.chunks = meta + p.off_chunks;
+    aa.rows = meta + p.off_rows;
+    aa.items = meta + p.off_items;
+    aa.partials = (float *)(ws + L.partials);
+    aa.n_prefill = p.n_prefill;
+    aa.n_items = p.n_prefill + p.n_decode_items;
+    aa.Te = Te;
+    aa.nq = c.n_q_heads;
+    aa.nkv = c.n_kv_heads;
+    aa.hd = c.head_dim;
+    aa.page = c.page_size;
+    aa.err = err;
+    aa.block_table[0] = emb_kv->block_table;
+    aa.block_table[1] = gen_kv->block_table;
+    aa.n_pages[0] = emb_kv->n_pages;
+    aa.n_pages[1] = gen_kv->n_pages;
+    aa.max_blocks[0] = emb_kv->max_blocks;
+    aa.max_blocks[1] = gen_kv->max_blocks;
+
+    RopeArgs ra{};
+    ra.qkv = qkv;
+    ra.q_out = qb;
+    ra.pos = meta + p.off_pos;
+    ra.seq = meta + p.off_seq;
+    ra.Te = Te;
+    ra.T = T;
+    ra.nq = c.n_q_heads;
+    ra.nkv = c.n_kv_heads;
+    ra.hd = c.head_dim;
+    ra.page = c.page_size;
+    ra.rope_base = c.rope_base;
+    ra.err = err;
+    for (int i = 0; i < 2; ++i) {
+        ra.block_table[i] = aa.block_table[i];
+        ra.n_pages[i] = aa.n_pages[i];
+        ra.max_blocks[i] = aa.max_blocks[i];
+    }
+    const size_t e_stride = layer_stride(M, *emb_kv), g_stride = layer_stride(M, *gen_kv);
+    const int qd = M.q_dim(), qkvd = M.qkv_dim(), F = c.d_ff;
+
+    for (int l = 0; l < c.n_layers; ++l) {
+        if (l > 0)
+            for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].attn_norm));
+        for (int gi = 0; gi < n_groups; ++gi) {
+            const orthrus_layer_weights &lw = groups[gi].m->layers[l];
+            RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d));
+        }
+        ra.k_cache[0] = (char *)emb_kv->k_cache + l * e_stride;
+        ra.v_cache[0] = (char *)emb_kv->v_cache + l * e_stride;
+        ra.k_cache[1] = (char *)gen_kv->k_cache + l * g_stride;
+        ra.v_cache[1] = (char *)gen_kv->v_cache + l * g_stride;
+        RUN("rope_append", launch_rope_append(dt, ra, s));
+        for (int i = 0; i < 2; ++i) {
+            aa.k_cache[i] = ra.k_cache[i];
+            aa.v_cache[i] = ra.v_cache[i];
+        }
+        RUN("attention", launch_attention(dt, aa, s));
+        if (p.n_split_rows > 0) RUN("attn_combine", launch_attn_combine(dt, aa, p.D, s));
+        for (int gi = 0; gi < n_groups; ++gi) {
+            const orthrus_layer_weights &lw = groups[gi].m->layers[l];
+            RUN("gemm_o", gemm(EPI_ADD_F32, groups[gi], ob, qd, lw.w_o, nullptr, x, d, 4, d, qd));
+        }
+        for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].mlp_norm));
+        for (int gi = 0; gi < n_groups; ++gi) {
+            const orthrus_layer_weights &lw = groups[gi].m->layers[l];
+            RUN("gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d));
+        }
+        for (int gi = 0; gi < n_groups; ++gi) {
+            const orthrus_layer_weights &lw = groups[gi].m->layers[l];
+            RUN("gemm_down", gemm(EPI_ADD_F32, groups[gi], ub, F, lw.w_down, nullptr, x, d, 4, d, F));
+        }
+    }
+
+    // incremental pooler on the embedding slice
+    if (p.n_chunks > 0) {
+        PoolArgs pa{};
+        pa.x = x;
+        pa.gain = emb->w.final_norm;
+        pa.chunks = meta + p.off_chunks;
+        pa.inv_rms = (float *)(ws + L.inv_rms);
+        pa.acc_sum = acc_sum;
+        pa.acc_w = acc_w;
+        pa.out_emb = out_emb;
+        pa.n_chunks = p.n_chunks;
+        pa.Te = Te;
+        pa.d = d;
+        pa.eps = c.rms_eps;
+        pa.err = err;
+        RUN("pool", launch_pool(pa, s));
+    }
+    // LM head on the decode slice
+    if (p.D > 0) {
+        const Group gd{gen, Te, T};
+        if (c.n_layers > 0) RUN("rmsnorm", norm(false, gd, gen->w.final_norm));
+        GemmArgs ga{};
+        ga.A = act + (size_t)Te * d * es;
+        ga.B0 = gen->w.lm_head;
+        ga.out = out_logits;
+        ga.M = p.D;
+        ga.N = gen->cfg.vocab;
+        ga.K = d;
+        ga.lda = d;
+        ga.ldo = gen->cfg.vocab;
+        RUN("lm_head", launch_gemm(dt, EPI_STORE_F32, ga, s));
+    }
+    return ORTHRUS_OK;
+#undef RUN
+}
+
+int orthrus_profile_begin(orthrus_model *m) {
+    if (!m) return ORTHRUS_EINVAL;
+    std::lock_guard<std::mutex> lk(m->mu);
+    m->profiling = true;
+    return ORTHRUS_OK;
+}
+
+int orthrus_profile_end(orthrus_model *m, orthrus_kernel_time *out, int32_t cap, int32_t *n_out) {
+    if (!m) return ORTHRUS_EINVAL;
+    std::lock_guard<std::mutex> lk(m->mu);
+    m->profiling = false;
+    std::vector<double> ms(m->prof_names.size(), 0.0);
+    std::vector<int> cnt(m->prof_names.size(), 0);
+    int rc = ORTHRUS_OK;
+    for (const auto &mk : m->marks) {
+        float t = 0.f;
+        if (hipEventSynchronize(mk.b) != hipSuccess || hipEventElapsedTime(&t, mk.a, mk.b) != hipSuccess)
+            rc = ORTHRUS_EHIP;
+        ms[mk.name] += t;
+        cnt[mk.name] += 1;
+        (void)hipEventDestroy(mk.a);
+        (void)hipEventDestroy(mk.b);
+    }
+    m->marks.clear();
+    const int n = (int)m->prof_names.size();
+    if (n_out) *n_out = n;
+    for (int i = 0; i < n && out && i < cap; ++i) {
+        std::memset(out[i].name, 0, sizeof(out[i].name));
+        std::strncpy(out[i].name, m->prof_names[i].c_str(), sizeof(out[i].name) - 1);
+        out[i].launches = cnt[i];
+        out[i].total_ms = ms[i];
+    }
+    m->prof_names.clear();
+    return rc;
+}
+
+int orthrus_workspace_init(void *workspace, void *stream) {
+    if (!workspace) return ORTHRUS_EINVAL;
+    HIP_TRY(hipMemsetAsync(workspace, 0, kAlign, (hipStream_t)stream));
+    return ORTHRUS_OK;
+}
+
+int orthrus_device_error(void *workspace, void *stream, int32_t *bits) {
+    if (!workspace) return ORTHRUS_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    int32_t v = 0, zero = 0;
+    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(hipMemcpy(&v, workspace, 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(workspace, &zero, 4, hipMemcpyHostToDevice));
+    if (bits) *bits = v;
+    return v ? ORTHRUS_EDEVICE : ORTHRUS_OK;
+}
+
+}  // extern "C"

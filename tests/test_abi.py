@@ -1,0 +1,191 @@
+"""The C-ABI library on the CPU: symbols, host-side validation and the attention work plan.
+
+No GPU work happens here: every call below either only reads host memory (orthrus_plan,
+model handles) or is rejected by host validation before anything is enqueued.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_25405_amd as P
+from paper_2609_25405_amd import _abi as A
+from paper_2609_25405_amd import runtime as R
+from workload import (Batch, DecodeRow, EmbChunk, ModelConfig, PagedKV, draw_tokens, make_weights,
+                      tiny_config, llm7b_config)
+from oracle import OracleKV, StepError, step_oracle
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "orthrus.h")
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(orthrus_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = P.load()
+    names = header_functions()
+    assert len(names) == 10
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in A.SIGNATURES, n
+    assert set(A.SIGNATURES) == set(names)
+    assert P.orthrus_strerror(A.ORTHRUS_EDUPSEQ).startswith("sequence")
+
+
+def test_struct_layouts_match_header():
+    # sizes follow the header's field lists (int32/float fields, 8-byte pointers)
+    assert ctypes.sizeof(A.orthrus_config) == 11 * 4
+    assert ctypes.sizeof(A.orthrus_emb_chunk) == 16
+    assert ctypes.sizeof(A.orthrus_decode_row) == 8
+    assert ctypes.sizeof(A.orthrus_kv) == 3 * 8 + 3 * 4 + 4
+    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8
+
+
+def test_model_create_validates_config():
+    cfg = tiny_config()
+    W = make_weights(cfg, 1)
+    m = R.DeviceModel(cfg, W, device="cpu")
+    assert m.handle.value
+    m.close()
+    for bad, code in ((dict(head_dim=32), A.ORTHRUS_EUNSUPPORTED),
+                      (dict(n_kv_heads=3), A.ORTHRUS_EINVAL),
+                      (dict(page_size=32), A.ORTHRUS_EUNSUPPORTED),
+                      (dict(d_model=200), A.ORTHRUS_EUNSUPPORTED)):
+        c = cfg.replace(**bad)
+        with pytest.raises(A.OrthrusError) as e:
+            R.DeviceModel(c, make_weights(c, 1) if "d_model" not in bad else W, device="cpu")
+        assert e.value.code == code
+
+
+def _cpu_setup(cfg=None, n_seq=6, n_pages=64, max_blocks=8):
+    cfg = cfg or tiny_config()
+    W = make_weights(cfg, 2)
+    m = R.DeviceModel(cfg, W, device="cpu")
+    pk = PagedKV(cfg, n_pages, n_seq, max_blocks, 3)
+    for s in range(n_seq):
+        pk.reserve(s, 40)
+    kv = R.DeviceKV.from_paged(pk, device="cpu")
+    return cfg, W, m, pk, kv
+
+
+KIND_CODE = {"desc": A.ORTHRUS_EDESC, "dupseq": A.ORTHRUS_EDUPSEQ, "capacity": A.ORTHRUS_ECAPACITY}
+
+
+def test_host_validation_matches_oracle_contract():
+    cfg, W, m, pk, kv = _cpu_setup()
+    ids = draw_tokens(1, 0, 12, cfg.vocab)
+    bad = [
+        Batch([EmbChunk(0, 0, 4, False), EmbChunk(0, 4, 4, False)], [], ids[:8]),
+        Batch([EmbChunk(0, 0, 7, False)], [DecodeRow(0, 3)], ids[:8]),
+        Batch([EmbChunk(6, 0, 8, False)], [], ids[:8]),
+        Batch([EmbChunk(0, 0, 8, True, "none")], [], ids[:8]),
+        Batch([EmbChunk(0, 0, 9, False)], [], ids[:8]),
+        Batch([EmbChunk(0, 121, 8, False)], [], ids[:8]),
+        Batch([], [DecodeRow(1, -1)], ids[:1]),
+        Batch([], [DecodeRow(1, 128)], ids[:1]),
+        Batch([EmbChunk(0, 0, 0, False)], [], ids[:0]),
+        Batch([EmbChunk(0, -1, 4, False)], [], ids[:4]),
+    ]
+    big = ids[:8].copy()
+    big[3] = cfg.vocab
+    bad.append(Batch([EmbChunk(0, 0, 8, False)], [], big))
+    okv = OracleKV.from_paged(pk)
+    t = R.torch
+    acc, accw = t.zeros((6, cfg.d_model)), t.zeros(6)
+    logits, emb = t.zeros((4, cfg.vocab)), t.zeros((4, cfg.d_model))
+    ws = type("WS", (), {"buf": t.zeros(64, dtype=t.uint8), "nbytes": 64})()
+    for b in bad:
+        with pytest.raises(StepError) as e:
+            step_oracle((cfg, W), (cfg, W), b, okv, okv, np.zeros((6, cfg.d_model)), np.zeros(6))
+        want = KIND_CODE[e.value.kind]
+        # descriptor checks run before the (too small) workspace is looked at
+        with pytest.raises(A.OrthrusError) as g:
+            R.step(m, m, b, kv, kv, acc, accw, logits, emb, ws)
+        assert g.value.code == want, (b, e.value.kind, g.value.code)
+        with pytest.raises(A.OrthrusError) as p:
+            R.plan(m, m, b, kv, kv)
+        assert p.value.code == want
+
+
+def test_undersized_workspace_is_rejected_before_launch():
+    cfg, W, m, pk, kv = _cpu_setup()
+    ids = draw_tokens(1, 0, 8, cfg.vocab)
+    b = Batch([EmbChunk(0, 0, 8, False)], [], ids)
+    t = R.torch
+    acc = t.zeros((6, cfg.d_model))
+    accw = t.zeros(6)
+    out = t.zeros((1, cfg.d_model))
+    ws = type("WS", (), {"buf": t.zeros(256, dtype=t.uint8), "nbytes": 256})()
+    with pytest.raises(A.OrthrusError) as e:
+        R.step(m, m, b, kv, kv, acc, accw, None, out, ws)
+    assert e.value.code == A.ORTHRUS_ECAPACITY
+
+
+def _check_coverage(batch, cfg, npre, ndec, items):
+    """Every (chunk token, kv head) in exactly one prefill tile with the causal key bound, and
+    every (decode row, kv head, key) in exactly one decode split."""
+    P_ = cfg.page_size
+    group = cfg.n_q_heads // cfg.n_kv_heads
+    seen_q = {}
+    work = []
+    for it in items[:npre]:
+        kind, ci, g, qb, qn, kb, ke, ps = it
+        assert kind == 0 and ps == -1 and kb == 0
+        c = batch.chunks[ci]
+        assert 1 <= qn <= 128 // group and qb + qn <= c.len
+        assert ke == c.offset + qb + qn
+        for r in range(qb, qb + qn):
+            key = (ci, g, r)
+            assert key not in seen_q
+            seen_q[key] = True
+        work.append(ke * qn)
+    assert len(seen_q) == sum(c.len for c in batch.chunks) * cfg.n_kv_heads
+    assert work == sorted(work, reverse=True)  # heaviest first
+    seen_k = {}
+    slots = set()
+    for it in items[npre:npre + ndec]:
+        kind, j, g, s, ns, kb, ke, ps = it
+        assert kind == 1
+        r = batch.rows[j]
+        assert 0 <= s < ns and kb % P_ == 0 and kb < ke <= r.ctx_len + 1
+        assert ke - kb <= 256
+        for k in range(kb, ke):
+            assert (j, g, k) not in seen_k
+            seen_k[(j, g, k)] = True
+        if ns == 1:
+            assert ps == -1
+        else:
+            assert ps not in slots
+            slots.add(ps)
+    assert len(seen_k) == sum(r.ctx_len + 1 for r in batch.rows) * cfg.n_kv_heads
+    if slots:
+        assert slots == set(range(len(slots)))
+
+
+@pytest.mark.parametrize("cfgname", ["tiny", "7b"])
+def test_plan_covers_every_key_exactly_once(cfgname):
+    if cfgname == "tiny":
+        cfg = tiny_config()
+        chunks = [EmbChunk(0, 0, 128, False), EmbChunk(1, 256, 44, True)]
+        rows = [DecodeRow(2, 0), DecodeRow(3, 255), DecodeRow(4, 256), DecodeRow(5, 1000)]
+    else:
+        cfg = llm7b_config(n_layers=1)
+        chunks = [EmbChunk(0, 0, 512, False, "last"), EmbChunk(1, 1536, 512, True, "last")]
+        rng = np.random.default_rng(0)
+        rows = [DecodeRow(2 + i, int(c)) for i, c in enumerate(rng.integers(1024, 4097, 64))]
+    n_seq = 2 + len(rows)
+    # planning reads no weight memory: tiny stand-in tensors carry the shapes' pointers
+    small = cfg.replace(n_layers=0, vocab=64) if cfgname == "7b" else cfg
+    W = make_weights(small, 0)
+    m = R.DeviceModel(small.replace(vocab=cfg.vocab) if cfgname == "7b" else small, W, device="cpu")
+    kv = type("KV", (), {})()
+    kv.struct = lambda: A.orthrus_kv(1, 1, 1, 100000, n_seq, 600)
+    ids = np.zeros(sum(c.len for c in chunks) + len(rows), np.int32)
+    b = Batch(chunks, rows, ids)
+    npre, ndec, items = R.plan(m, m, b, kv, kv)
+    _check_coverage(b, cfg if cfgname == "tiny" else small, npre, ndec, items)

@@ -1,0 +1,165 @@
+"""GPU parity of orthrus_step against the float64 oracle (needs an MI355X and the built library).
+
+Every case runs the same seeded inputs through the oracle and through the C ABI, step by step,
+and compares logits, finished embeddings, the pooling state and the cache writes.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from workload import (Batch, DecodeRow, EmbChunk, ModelConfig, PagedKV, draw_tokens, make_weights,
+                      tiny_config, tiny_mixed_scenario, layer7b_mixed_workload)
+from tests.parity import Pair, assert_vectors_close
+from paper_2609_25405_amd import runtime as R
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu(request):
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    print(f"\n[case] {request.node.name}", flush=True)
+
+
+def _tiny_pair(dtype, qk_std=None, seed=1001):
+    cfg, W, n_seq, steps = tiny_mixed_scenario(seed=seed, dtype=dtype, qk_std=qk_std)
+    max_tok = 512
+    pk = PagedKV(cfg, n_pages=n_seq * (max_tok // 16) + 7, n_seq=n_seq, max_blocks=max_tok // 16, seed=seed)
+    for s in range(n_seq):
+        pk.reserve(s, 320)
+    pair = Pair(cfg, W, pk)
+    pair.workspace(max_tokens=max(b.n_tokens for b in steps), max_chunks=4, max_decode=4, max_ctx=max_tok)
+    return pair, steps
+
+
+# qk_std sets the attention logit spread: std(q.k / sqrt(hd)) ~ qk_std^2 * d_model, i.e. ~10
+# at 0.2 (near one-hot softmax: exact fp32 only, bf16 rounding of q and k alone moves such
+# weights by several percent) and ~2 at 0.09 (sharp enough that a wrong key or position shows).
+@pytest.mark.parametrize("dtype,qk_std", [("f32", None), ("f32", 0.2), ("bf16", None), ("bf16", 0.09)])
+def test_tiny_mixed_scenario(dtype, qk_std):
+    """Two-layer decoder: KV-only prompt chunks, then three mixed steps (300-token embeddings
+    chunked 128/128/44 with mean pooling, four decode rows)."""
+    pair, steps = _tiny_pair(dtype, qk_std)
+    for b in steps:
+        pair.step(b)
+    print(pair.report, flush=True)
+
+
+def _gqa_config(dtype="bf16", n_layers=2):
+    return ModelConfig(n_layers=n_layers, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                       d_ff=1024, vocab=512, dtype=dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gqa_long_context_splits(dtype):
+    """Grouped-query shape (group 4, head_dim 128) with multi-split decode rows, chunk offsets
+    past earlier cached tokens, ragged chunk tails and every pooling head."""
+    cfg = _gqa_config(dtype)
+    W = make_weights(cfg, 7, qk_std=0.06 if dtype == "bf16" else 0.15)
+    n_seq, max_blocks = 8, 64
+    pk = PagedKV(cfg, n_seq * max_blocks + 3, n_seq, max_blocks, 7)
+    ctx = [0, 17, 255, 256, 700]
+    for i, c in enumerate(ctx):
+        pk.fill_random(3 + i, c, 7)
+        pk.reserve(3 + i, c + 1)
+    pk.fill_random(1, 300, 8)          # request 1 resumes at offset 300
+    for s, n in ((0, 200), (1, 433), (2, 97)):
+        pk.reserve(s, n)
+    acc_w = np.zeros(n_seq)
+    acc_w[1] = 300
+    pair = Pair(cfg, W, pk, acc_w=acc_w)
+    pair.workspace(max_tokens=512, max_chunks=3, max_decode=5, max_ctx=1024)
+    chunks = [EmbChunk(0, 0, 200, True, "mean"), EmbChunk(1, 300, 133, True, "last"),
+              EmbChunk(2, 0, 97, True, "cls")]
+    rows = [DecodeRow(3 + i, c) for i, c in enumerate(ctx)]
+    ids = draw_tokens(7, 1, 200 + 133 + 97 + len(rows), cfg.vocab)
+    pair.step(Batch(chunks, rows, ids))
+    print(pair.report, flush=True)
+
+
+def test_two_models_two_pools():
+    """Separate embedding and generation models (same shape) with separate caches."""
+    cfg = tiny_config("bf16")
+    We = make_weights(cfg, 21, model_tag=1)
+    Wg = make_weights(cfg, 21, model_tag=2)
+    pe = PagedKV(cfg, 80, 4, 20, 1)
+    pg = PagedKV(cfg, 80, 4, 20, 2)
+    for s in range(4):
+        pe.reserve(s, 300)
+        pg.fill_random(s, 40 + 30 * s, 3)
+        pg.reserve(s, 41 + 30 * s)
+    pair = Pair(cfg, We, pe, cfg, Wg, pg)
+    pair.workspace(max_tokens=300, max_chunks=2, max_decode=4, max_ctx=320)
+    ids = draw_tokens(3, 3, 150 + 4, cfg.vocab)
+    # seq 0 appears in both sections: legal, the two pools are separate namespaces
+    b = Batch([EmbChunk(0, 0, 100, True, "mean"), EmbChunk(1, 0, 50, False, "mean")],
+              [DecodeRow(s, 40 + 30 * s) for s in range(4)], ids)
+    pair.step(b)
+
+
+def test_chunked_equals_single_pass_on_gpu():
+    """Section 3.3 equivalence on the device: 300 tokens in chunks of 128 vs one chunk."""
+    cfg = tiny_config("bf16")
+    W = make_weights(cfg, 5, qk_std=0.09)
+    ids = draw_tokens(5, 9, 300, cfg.vocab)
+    outs = {}
+    for C in (128, 300, 37):
+        pk = PagedKV(cfg, 40, 1, 20, 4)
+        pk.reserve(0, 300)
+        dm = R.DeviceModel(cfg, W)
+        kv = R.DeviceKV.from_paged(pk)
+        ws = R.Workspace(dm, dm, 300, 1, 0, 320)
+        S = torch.zeros((1, cfg.d_model), device="cuda")
+        Wc = torch.zeros(1, device="cuda")
+        out = torch.zeros((1, cfg.d_model), device="cuda")
+        for off in range(0, 300, C):
+            ln = min(C, 300 - off)
+            R.step(dm, dm, Batch([EmbChunk(0, off, ln, off + ln == 300, "mean")], [], ids[off:off + ln]),
+                   kv, kv, S, Wc, None, out, ws)
+        torch.cuda.synchronize()
+        assert ws.device_error() == 0
+        assert Wc.item() == 300
+        outs[C] = out[0].cpu().numpy()
+    for C in (128, 37):
+        assert_vectors_close(outs[C][None], outs[300][None], "bf16", f"chunk {C} vs single pass")
+
+
+def test_layer7b_mixed_step():
+    """One 7B-shape layer (bf16, vocab 32000): 1024 chunk tokens (two requests, chunk 512,
+    last-token pooling, one of them resuming after 1536 cached tokens) + 64 decode rows with
+    contexts in [1024, 4096] over N(0,1) bf16 caches.  Full comparison of every output."""
+    wl = layer7b_mixed_workload()
+    pair = Pair(wl.cfg, wl.weights, wl.kv, acc_w=wl.acc_w)
+    pair.workspace(max_tokens=wl.batch.n_tokens, max_chunks=2, max_decode=64, max_ctx=4096)
+    pair.step(wl.batch)
+    print(pair.report, flush=True)
+
+
+def test_device_errors_are_flagged_not_faulted():
+    """A chunk whose pooling state does not match its offset, and a block-table entry past the
+    pool, raise device error bits; the step still completes and nothing outside is written."""
+    cfg = tiny_config("f32")
+    W = make_weights(cfg, 3)
+    pk = PagedKV(cfg, 20, 3, 8, 1)
+    for s in range(3):
+        pk.reserve(s, 64)
+    dm = R.DeviceModel(cfg, W)
+    kv = R.DeviceKV.from_paged(pk)
+    ws = R.Workspace(dm, dm, 64, 2, 2, 128)
+    S = torch.zeros((3, cfg.d_model), device="cuda")
+    Wc = torch.zeros(3, device="cuda")
+    out = torch.zeros((2, cfg.d_model), device="cuda")
+    lg = torch.zeros((2, cfg.vocab), device="cuda")
+    ids = draw_tokens(1, 1, 16, cfg.vocab)
+    R.step(dm, dm, Batch([EmbChunk(0, 16, 16, True, "mean")], [], ids), kv, kv, S, Wc, None, out, ws)
+    assert ws.device_error() == 2
+    assert Wc[0].item() == 0.0                      # the rejected chunk left its state alone
+    assert ws.device_error() == 0                   # reading cleared the word
+    bt = pk.block_table.copy()
+    bt[1, 0] = pk.n_pages                           # one past the pool
+    kv.set_block_table(bt)
+    R.step(dm, dm, Batch([], [DecodeRow(1, 3)], ids[:1]), kv, kv, S, Wc, lg, None, ws)
+    assert ws.device_error() == 1

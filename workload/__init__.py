@@ -81,9 +81,11 @@ def llm7b_config(n_layers: int = 32, dtype: str = "bf16", has_lm_head: bool = Tr
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    b = x.view(np.uint32).astype(np.uint64)
-    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
-    return b.astype(np.uint32).view(np.float32).reshape(x.shape)
+    b = x.view(np.uint32)
+    # finite inputs only: the rounding increment cannot carry out of 32 bits
+    r = b + (np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1)))
+    r &= np.uint32(0xFFFF0000)
+    return r.view(np.float32).reshape(x.shape)
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -149,6 +151,14 @@ def make_weights(cfg: ModelConfig, seed: int, model_tag: int = 0, std: float = 0
             "w_down": _normal(seed, model_tag, l, "w_down", (d, F), std, bf16),
         })
     return out
+
+
+def as_float64(weights: Dict) -> Dict:
+    """The same weights as float64 arrays (a one-time upcast for float64 consumers)."""
+    f = lambda a: None if a is None else np.asarray(a, dtype=np.float64)
+    return {"tok_emb": f(weights["tok_emb"]), "final_norm": f(weights["final_norm"]),
+            "lm_head": f(weights.get("lm_head")),
+            "layers": [{k: f(v) for k, v in lw.items()} for lw in weights["layers"]]}
 
 
 # ---------------------------------------------------------------------------
