@@ -84,13 +84,15 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
         for (int i = 0; i < B_LOADS; ++i) rb[i] = *(const u32x4 *)(b_src[i] + b_off[i] + kb);
     };
-    auto lstore = [&](int buf) {
-        char *s = smem + buf * STAGE;
+    auto lstore_to = [&](char *s) {
 #pragma unroll
         for (int i = 0; i < A_LOADS; ++i) *(u32x4 *)(s + a_lds[i]) = ra[i];
 #pragma unroll
         for (int i = 0; i < B_LOADS; ++i) *(u32x4 *)(s + b_lds[i]) = rb[i];
     };
+    auto lstore = [&](int buf) { lstore_to(smem + buf * STAGE); };
+    int next_k = 0;
+    auto gload_next = [&]() { gload(next_k); };
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -100,33 +102,67 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    const int nk = a.K / BK;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
-        const char *s = smem + cur * STAGE;
+    // fragment rows of this lane; the swizzle key (row >> 1) & 7 is the same for every
+    // 32-row fragment of the lane, so the LDS offsets differ only by constants
+    const int arow = wm * TM + (lane & 31), brow = BM + wn * TN + (lane & 31);
+    const int akey = (arow >> 1) & 7, bkey = (brow >> 1) & 7;
+    bf16x8 fa[2][FM], fb[2][FN];
+    auto lds_frag = [&](const char *s, int kk, int buf) {
+        const int chk = kk * 2 + (lane >> 5);
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi)
+            fa[buf][mi] = *(const bf16x8 *)(s + (arow + mi * 32) * 128 + ((chk ^ akey) << 4));
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni)
+            fb[buf][ni] = *(const bf16x8 *)(s + (brow + ni * 32) * 128 + ((chk ^ bkey) << 4));
+    };
+
+    // One K stage per iteration, software-pipelined by hand (the scheduler is told the order):
+    //   LDS fragments of k-step 0, then per k-step its MFMAs interleaved with the LDS reads of the
+    //   next k-step's fragments; the next stage's global loads ride along k-step 0 and its LDS
+    //   stores (other buffer, not read this iteration) along k-step 3.  One barrier per stage.
+    constexpr int NMF = FM * FN, NFR = FM + FN, NLD = A_LOADS + B_LOADS;
+    auto stage = [&](const char *s, char *s_next, bool more) {
+        lds_frag(s, 0, 0);
+        if (more) gload_next();
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
-            const int chk = kk * 2 + (lane >> 5);
-            bf16x8 af[FM], bfr[FN];
-#pragma unroll
-            for (int mi = 0; mi < FM; ++mi)
-                af[mi] = *(const bf16x8 *)(s + swz(wm * TM + mi * 32 + (lane & 31), chk));
-#pragma unroll
-            for (int ni = 0; ni < FN; ++ni)
-                bfr[ni] = *(const bf16x8 *)(s + swz(BM + wn * TN + ni * 32 + (lane & 31), chk));
+            if (kk + 1 < BK / 16) lds_frag(s, kk + 1, (kk + 1) & 1);
 #pragma unroll
             for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < FN; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][mi], fb[kk & 1][ni],
+                                                                          acc[mi][ni], 0, 0, 0);
+            if (kk == BK / 16 - 1 && more) lstore_to(s_next);
         }
-        if (kt + 1 < nk) lstore(cur ^ 1);
+        // schedule: DS_READ=0x100, DS_WRITE=0x200, VMEM_READ=0x020, MFMA=0x008
+        __builtin_amdgcn_sched_group_barrier(0x100, NFR, 0);
+#pragma unroll
+        for (int kk = 0; kk < BK / 16; ++kk) {
+#pragma unroll
+            for (int i = 0; i < NMF; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if (kk == 0 && more) {
+                    if (i < NLD) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                }
+                if (kk + 1 < BK / 16 && i < NFR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                if (kk == BK / 16 - 1 && more && i < NLD) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            }
+        }
+    };
+
+    const int nk = a.K / BK;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 1 < nk; ++kt) {
+        next_k = kt + 1;
+        stage(smem + (kt & 1) * STAGE, smem + ((kt + 1) & 1) * STAGE, true);
         __syncthreads();
     }
+    stage(smem + (kt & 1) * STAGE, nullptr, false);
 
     // epilogue: lane holds column (lane & 31) of each 32x32 tile, rows 8*(r/4) + 4*(lane/32) + r%4
 #pragma unroll
