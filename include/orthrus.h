@@ -114,9 +114,11 @@ typedef struct orthrus_batch {
     const int32_t *token_ids;
 } orthrus_batch;
 
-/* A paged KV cache (device).  k_cache, v_cache: [n_layers][n_pages][n_kv_heads][page][hd] of
- * the model dtype (keys stored after rotation).  block_table: int32 [n_seq][max_blocks]; the
- * slot of position p of request s is block_table[s][p / page] * page + p % page. */
+/* A paged KV cache (device), model dtype.  k_cache: [n_layers][n_pages][n_kv_heads][page][hd]
+ * (keys stored after rotation, position-major inside a page); v_cache:
+ * [n_layers][n_pages][n_kv_heads][hd][page] (dim-major inside a page, so that 8 consecutive
+ * positions of one value dim are contiguous).  block_table: int32 [n_seq][max_blocks]; position
+ * p of request s lives in page block_table[s][p / page] at in-page position p % page. */
 typedef struct orthrus_kv {
     void *k_cache;
     void *v_cache;

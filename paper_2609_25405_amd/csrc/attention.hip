@@ -1,19 +1,24 @@
 // Ragged attention over the mixed batch in one launch (Section 3.2: every batch item goes
 // through the same attention layer, differing only in length).
 //
+// Cache layout (one page = 16 positions of one KV head): keys key-major [16][hd], values
+// dim-major [hd][16].  Both MFMA operands of a 32x32x16 step then read 16 contiguous bytes per
+// lane (a key row for S^T = K Q^T, a value row over 8 positions for O^T = V^T P^T), and the
+// decode dot products pair adjacent dims (q.k) or adjacent positions (p.v) without shuffles.
+//
 // The host planner emits a work list; block b runs item b:
-//   * prefill items (embedding-chunk rows, heaviest first): a tile of (128 / group) tokens of
-//     one chunk times the `group` query heads of one KV head.  Rows attend causally to every
-//     key of their request at positions <= their own: earlier chunks' keys from the paged
-//     cache plus this chunk's keys, which the step appended before this launch.
-//     bf16: each wave owns 32 query rows of one head; S^T = K Q^T and O^T += V^T P^T run on
-//     v_mfma_f32_32x32x16_bf16 over 32-key blocks staged in LDS (V transposed on the way in),
-//     with an online softmax in fp32 (exp2 domain).
-//   * decode items: one (decode row, KV head, 256-key split).  All `group` query heads that
-//     share the KV head are served from one read of each 4 KiB K / V page slice.  Scores go to
-//     LDS, the softmax is taken over the split, then P V is accumulated.  Rows with more than
-//     one split write (max, sum, unnormalised output) partials that attn_combine merges in
-//     split order, so results do not depend on scheduling.
+//   * prefill items (embedding-chunk rows, heaviest first): (128 / group) tokens of one chunk
+//     times the `group` query heads of one KV head; each wave owns 32 query rows of one head
+//     and walks the keys of its request in 32-key blocks, with operands loaded straight from
+//     the cache (L2-resident, shared by the group's waves) one block ahead of the MFMAs, an
+//     online softmax in fp32 (exp2 domain) and causal masking on the diagonal blocks.  Waves
+//     never synchronise, so each stops at its own causal bound.
+//   * decode items: one (decode row, KV head, <= 256-key split).  Each wave owns up to four of
+//     the split's pages and issues all their K and V loads at once (128 KiB in flight per item),
+//     scores with v_dot2_f32_bf16 for all `group` query heads at once, takes the softmax over the
+//     split through LDS, then accumulates P V from registers.  Rows with several splits write
+//     (max, sum, unnormalised output) partials merged by attn_combine in split order, so results
+//     do not depend on scheduling.
 // Page ids read from the block table are range-checked; a bad id sets the sticky device error
 // word and its keys are skipped (never dereferenced).
 #include "common.hpp"
@@ -24,6 +29,8 @@ namespace orthrus {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kPage = 16;
+constexpr int kPrefillPageWindow = 512;  // page ids staged in LDS at a time (even)
 
 struct PoolView {
     const char *k, *v;
@@ -31,8 +38,7 @@ struct PoolView {
     int n_pages, max_blocks;
 };
 
-__device__ __forceinline__ PoolView pool_view(const AttnArgs &a, int p, size_t elem) {
-    (void)elem;
+__device__ __forceinline__ PoolView pool_view(const AttnArgs &a, int p) {
     PoolView pv;
     pv.k = (const char *)a.k_cache[p];
     pv.v = (const char *)a.v_cache[p];
@@ -42,84 +48,217 @@ __device__ __forceinline__ PoolView pool_view(const AttnArgs &a, int p, size_t e
     return pv;
 }
 
-// ----------------------------------------------------------------------------- decode split
-template <typename T, int HD, int G>
-__device__ void decode_item(const AttnArgs &a, const int32_t *it, char *smem) {
-    constexpr int DPL = HD / 4;    // dims per lane in the score pass (4 lanes per key)
-    constexpr int VPL = HD / 16;   // dims per lane in the value pass (16 lanes per key)
-    constexpr int MAXK = kSplitPages * 16;
-    float *sc = (float *)smem;                         // [MAXK][G] scores, then weights
-    float *red = sc + MAXK * G;                        // [4][2 * G] cross-wave reductions
-    float *part = red + 8 * G;                         // [16 key groups][16 lanes][G][VPL]
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c,
+                                           false);
+}
+
+// ------------------------------------------------------------------ decode split, bf16 path
+// Loads are issued branch-free and before any use: every page id of the wave first, then every
+// K and V line of those pages; invalid or absent pages read page 0 and are masked afterwards.
+template <int HD, int G>
+__device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *smem) {
+    constexpr int KL = HD / 32;     // 16-byte loads per lane per page, for K and for V
+    constexpr int QD = HD / 4;      // head dims per lane in the score pass (4 lanes per key)
+    constexpr int VD = HD / 64;     // head dims per lane in the value pass
+    constexpr int PPW = kSplitPages / 4;
+    constexpr int KPW = PPW * kPage;                       // keys per wave
+    uint32_t *pk_all = (uint32_t *)smem;                   // [4 waves][KPW / 2][G] bf16 weight pairs
+    float *mw = (float *)(pk_all + 4 * (KPW / 2) * G);     // [4][G] wave maxima
+    float *lw = mw + 4 * G;                                // [4][G] wave sums
+    float *part = lw + 4 * G;                              // [4][G][HD] wave outputs
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = it[IT_INDEX], g = it[IT_KVHEAD];
     const int k0 = it[IT_KEY_BEGIN], k1 = it[IT_KEY_END], pslot = it[IT_PARTIAL];
     const int nk = k1 - k0;
-    const int P = a.page;
+    const int n_pg = (nk + kPage - 1) / kPage;
     const int32_t *row = a.rows + kRowInts * j;
     const int seq = row[0], tok = row[2];
-    const PoolView pv = pool_view(a, 1, sizeof(T));
-    const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks + k0 / P;
-    const int n_pg = (nk + P - 1) / P;
-    const size_t page_elems = (size_t)a.nkv * P * HD;
-    const float scale = kLog2e / sqrtf((float)HD);
-
-    // ---- scores: lane = (key in page, quarter of the head dims)
+    const PoolView pv = pool_view(a, 1);
+    const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks + k0 / kPage;
+    const size_t page_bytes = (size_t)a.nkv * kPage * HD * 2;
     const int kin = lane >> 2, qtr = lane & 3;
-    const T *qrow = (const T *)a.q + ((size_t)tok * a.nq + g * G) * HD + qtr * DPL;
-    float q[G][DPL];
+
+    int page[PPW];
+    bool pok[PPW];
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) page[i] = bt[min(wave + 4 * i, n_pg - 1)];
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) {
+        const bool present = wave + 4 * i < n_pg;
+        pok[i] = present && page[i] >= 0 && page[i] < pv.n_pages;
+        if (present && !pok[i] && lane == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+        page[i] = pok[i] ? page[i] : 0;
+    }
+    // query heads g*G .. g*G+G-1, this lane's quarter of the head dims, as bf16 pairs; loaded
+    // first so the score pass waits only for them and its own page's keys (loads retire in order)
+    uint32_t qp[G][QD / 2];
+    const char *qrow = (const char *)a.q + ((size_t)tok * a.nq + g * G) * HD * 2 + qtr * QD * 2;
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) q[h][e] = to_f32(qrow[h * HD + e]);
-    for (int pg = wave; pg < n_pg; pg += 4) {
-        const int page = bt[pg];
-        const bool ok = page >= 0 && page < pv.n_pages;
-        if (!ok && lane == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
-        const int key = pg * P + kin;  // relative to k0
-        float s[G];
+        for (int c = 0; c < QD / 8; ++c) {
+            const u32x4 v = *(const u32x4 *)(qrow + h * HD * 2 + 16 * c);
 #pragma unroll
-        for (int h = 0; h < G; ++h) s[h] = 0.f;
-        if (ok && key < nk) {
-            const T *kp = (const T *)pv.k + (size_t)page * page_elems + ((size_t)g * P + kin) * HD + qtr * DPL;
-            if constexpr (sizeof(T) == 2) {
-                const u32x4 *k4 = (const u32x4 *)kp;
-#pragma unroll
-                for (int c = 0; c < DPL / 8; ++c) {
-                    const u32x4 kv = k4[c];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float klo = bf16_lo(kv[e]), khi = bf16_hi(kv[e]);
-#pragma unroll
-                        for (int h = 0; h < G; ++h)
-                            s[h] = fmaf(q[h][c * 8 + 2 * e + 1], khi, fmaf(q[h][c * 8 + 2 * e], klo, s[h]));
-                    }
-                }
-            } else {
-                const f32x4 *k4 = (const f32x4 *)kp;
-#pragma unroll
-                for (int c = 0; c < DPL / 4; ++c) {
-                    const f32x4 kv = k4[c];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-#pragma unroll
-                        for (int h = 0; h < G; ++h) s[h] = fmaf(q[h][c * 4 + e], kv[e], s[h]);
-                }
-            }
+            for (int e = 0; e < 4; ++e) qp[h][4 * c + e] = v[e];
         }
+    u32x4 kr[PPW][KL], vr[PPW][KL];
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) {
+        const char *kp = pv.k + page[i] * page_bytes + (size_t)((g * kPage + kin) * HD + qtr * QD) * 2;
+#pragma unroll
+        for (int c = 0; c < KL; ++c) kr[i][c] = *(const u32x4 *)(kp + 16 * c);
+    }
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) {
+        const char *vp = pv.v + page[i] * page_bytes + (size_t)((g * HD + lane * VD) * kPage) * 2;
+#pragma unroll
+        for (int c = 0; c < KL; ++c) vr[i][c] = *(const u32x4 *)(vp + 16 * c);
+    }
+
+    // ---- scores of this wave's keys (4 lanes per key), softmax statistics inside the wave
+    const float scale = kLog2e / sqrtf((float)HD);
+    float s[PPW][G];
+    float mloc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) mloc[h] = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) {
+        const bool vis = pok[i] && (wave + 4 * i) * kPage + kin < nk;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            s[h] += __shfl_xor(s[h], 1, 64);
-            s[h] += __shfl_xor(s[h], 2, 64);
-        }
-        if (qtr == 0 && key < nk) {
+            float acc = 0.f;
 #pragma unroll
-            for (int h = 0; h < G; ++h) sc[key * G + h] = ok ? s[h] * scale : -INFINITY;
+            for (int c = 0; c < KL; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc = dot2(qp[h][4 * c + e], kr[i][c][e], acc);
+            acc += __shfl_xor(acc, 1, 64);
+            acc += __shfl_xor(acc, 2, 64);
+            s[i][h] = vis ? acc * scale : -INFINITY;
+            mloc[h] = fmaxf(mloc[h], s[i][h]);
+        }
+    }
+    float l[G];
+    uint16_t *pk16 = (uint16_t *)(pk_all + wave * (KPW / 2) * G);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        float mh = mloc[h];
+#pragma unroll
+        for (int o = 4; o <= 32; o <<= 1) mh = fmaxf(mh, __shfl_xor(mh, o, 64));
+        mloc[h] = mh;
+        float ls = 0.f;
+#pragma unroll
+        for (int i = 0; i < PPW; ++i) {
+            const float p = mh == -INFINITY ? 0.f : exp2f(s[i][h] - mh);
+            ls += p;
+            // key i*16 + kin of this wave; adjacent keys share one 32-bit word
+            const int key = i * kPage + kin;
+            if (qtr == 0) pk16[((key >> 1) * G + h) * 2 + (key & 1)] = (uint16_t)f2bf_bits(p);
+        }
+#pragma unroll
+        for (int o = 4; o <= 32; o <<= 1) ls += __shfl_xor(ls, o, 64);
+        l[h] = ls;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // ---- P V from registers: this lane owns head dims lane*VD .. lane*VD+VD-1 of its pages
+    const uint32_t *pkw = pk_all + wave * (KPW / 2) * G;
+    float acc[G][VD];
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int d = 0; d < VD; ++d) acc[h][d] = 0.f;
+#pragma unroll
+    for (int i = 0; i < PPW; ++i) {
+        // positions of page i inside the split (0 when the page is absent or invalid)
+        const int valid = pok[i] ? min(kPage, nk - (wave + 4 * i) * kPage) : 0;
+#pragma unroll
+        for (int d = 0; d < VD; ++d) {
+#pragma unroll
+            for (int jp = 0; jp < 8; ++jp) {
+                uint32_t vv = vr[i][(d * 8 + jp) >> 2][(d * 8 + jp) & 3];
+                // positions past the split hold other data (or NaN poison): zero them
+                vv = (2 * jp + 1 < valid) ? vv : ((2 * jp < valid) ? (vv & 0xffffu) : 0u);
+                const uint32_t *pw = pkw + (i * 8 + jp) * G;
+#pragma unroll
+                for (int h = 0; h < G; ++h) acc[h][d] = dot2(pw[h], vv, acc[h][d]);
+            }
+        }
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            mw[wave * G + h] = mloc[h];
+            lw[wave * G + h] = l[h];
+        }
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int d = 0; d < VD; ++d) part[(wave * G + h) * HD + lane * VD + d] = acc[h][d];
+    __syncthreads();
+    // ---- merge the four waves in a fixed order
+    for (int o = tid; o < G * HD; o += 256) {
+        const int h = o / HD, d = o % HD;
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, mw[w * G + h]);
+        float L = 0.f, sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float sc_w = mw[w * G + h] == -INFINITY ? 0.f : exp2f(mw[w * G + h] - M);
+            L += lw[w * G + h] * sc_w;
+            sum += part[(w * G + h) * HD + d] * sc_w;
+        }
+        if (pslot < 0) {
+            const float out = L > 0.f ? sum / L : 0.f;
+            ((bf16 *)a.o)[((size_t)tok * a.nq + g * G + h) * HD + d] = from_f32<bf16>(out);
+        } else {
+            float *pp = a.partials + ((size_t)pslot * G + h) * (HD + 2);
+            if (d == 0) {
+                pp[0] = M;
+                pp[1] = L;
+            }
+            pp[2 + d] = sum;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ decode split, fp32 path
+template <int HD, int G>
+__device__ void decode_item_f32(const AttnArgs &a, const int32_t *it, char *smem) {
+    constexpr int MAXK = kSplitPages * kPage;
+    float *sc = (float *)smem;  // [MAXK][G]
+    float *red = sc + MAXK * G;
+    float *part = red + 8 * G;  // [4][G][HD]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j = it[IT_INDEX], g = it[IT_KVHEAD];
+    const int k0 = it[IT_KEY_BEGIN], k1 = it[IT_KEY_END], pslot = it[IT_PARTIAL];
+    const int nk = k1 - k0;
+    const int32_t *row = a.rows + kRowInts * j;
+    const int seq = row[0], tok = row[2];
+    const PoolView pv = pool_view(a, 1);
+    const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks + k0 / kPage;
+    const size_t page_elems = (size_t)a.nkv * kPage * HD;
+    const float scale = kLog2e / sqrtf((float)HD);
+    const float *q = (const float *)a.q + ((size_t)tok * a.nq + g * G) * HD;
+    // scores: one key per thread
+    for (int key = tid; key < nk; key += 256) {
+        const int page = bt[key / kPage];
+        const bool ok = page >= 0 && page < pv.n_pages;
+        if (!ok) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+        const float *kr = (const float *)pv.k + page * page_elems + ((size_t)g * kPage + key % kPage) * HD;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            float s = 0.f;
+            if (ok)
+                for (int d = 0; d < HD; ++d) s = fmaf(q[h * HD + d], kr[d], s);
+            sc[key * G + h] = ok ? s * scale : -INFINITY;
         }
     }
     __syncthreads();
-
-    // ---- softmax statistics over the split (one key per thread)
     float v[G], m[G], l[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -131,63 +270,36 @@ __device__ void decode_item(const AttnArgs &a, const int32_t *it, char *smem) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
         m[h] = fmaxf(fmaxf(red[h], red[2 * G + h]), fmaxf(red[4 * G + h], red[6 * G + h]));
-        const float pv_ = (tid < nk && m[h] != -INFINITY) ? exp2f(v[h] - m[h]) : 0.f;
-        if (tid < nk) sc[tid * G + h] = pv_;
-        const float ws = wave_sum(pv_);
+        const float p = (tid < nk && m[h] != -INFINITY) ? exp2f(v[h] - m[h]) : 0.f;
+        if (tid < nk) sc[tid * G + h] = p;
+        const float ws = wave_sum(p);
         if (lane == 0) red[wave * 2 * G + G + h] = ws;
     }
     __syncthreads();
 #pragma unroll
     for (int h = 0; h < G; ++h) l[h] = red[G + h] + red[3 * G + h] + red[5 * G + h] + red[7 * G + h];
-
-    // ---- P V: a page per step, wave w takes keys 4w..4w+3 of it, 16 lanes per key
-    const int kq = lane >> 4, dl = lane & 15;
-    float acc[G][VPL];
+    // P V: wave w sums keys w, w+4, ...; thread owns dims lane, lane+64
+    for (int o = lane; o < HD; o += 64) {
+        float acc[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+        for (int h = 0; h < G; ++h) acc[h] = 0.f;
+        for (int key = wave; key < nk; key += 4) {
+            const int page = bt[key / kPage];
+            if (page < 0 || page >= pv.n_pages) continue;
+            const float vv = ((const float *)pv.v)[page * page_elems + ((size_t)g * HD + o) * kPage + key % kPage];
 #pragma unroll
-        for (int e = 0; e < VPL; ++e) acc[h][e] = 0.f;
-    for (int pg = 0; pg < n_pg; ++pg) {
-        const int page = bt[pg];
-        const int kin2 = wave * 4 + kq;
-        const int key = pg * P + kin2;
-        if (page < 0 || page >= pv.n_pages || key >= nk) continue;
-        const T *vp = (const T *)pv.v + (size_t)page * page_elems + ((size_t)g * P + kin2) * HD + dl * VPL;
-        float w[G];
-#pragma unroll
-        for (int h = 0; h < G; ++h) w[h] = sc[key * G + h];
-        float vv[VPL];
-        if constexpr (sizeof(T) == 2) {
-#pragma unroll
-            for (int c = 0; c < VPL / 2; ++c) {
-                const uint32_t u = ((const uint32_t *)vp)[c];
-                vv[2 * c] = bf16_lo(u);
-                vv[2 * c + 1] = bf16_hi(u);
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < VPL; ++e) vv[e] = to_f32(vp[e]);
+            for (int h = 0; h < G; ++h) acc[h] = fmaf(sc[key * G + h], vv, acc[h]);
         }
 #pragma unroll
-        for (int h = 0; h < G; ++h)
-#pragma unroll
-            for (int e = 0; e < VPL; ++e) acc[h][e] = fmaf(w[h], vv[e], acc[h][e]);
+        for (int h = 0; h < G; ++h) part[(wave * G + h) * HD + o] = acc[h];
     }
-    // cross key-group reduction in a fixed order
-    float *mine = part + ((wave * 4 + kq) * 16 + dl) * G * VPL;
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < VPL; ++e) mine[h * VPL + e] = acc[h][e];
     __syncthreads();
     for (int o = tid; o < G * HD; o += 256) {
         const int h = o / HD, d = o % HD;
-        const int dlo = d / VPL, e = d % VPL;
-        float sum = 0.f;
-        for (int kg = 0; kg < 16; ++kg) sum += part[((kg * 16 + dlo) * G + h) * VPL + e];
+        const float sum = ((part[(0 * G + h) * HD + d] + part[(1 * G + h) * HD + d]) +
+                           part[(2 * G + h) * HD + d]) + part[(3 * G + h) * HD + d];
         if (pslot < 0) {
-            const float out = l[h] > 0.f ? sum / l[h] : 0.f;
-            ((T *)a.o)[((size_t)tok * a.nq + g * G + h) * HD + d] = from_f32<T>(out);
+            ((float *)a.o)[((size_t)tok * a.nq + g * G + h) * HD + d] = l[h] > 0.f ? sum / l[h] : 0.f;
         } else {
             float *pp = a.partials + ((size_t)pslot * G + h) * (HD + 2);
             if (d == 0) {
@@ -200,8 +312,8 @@ __device__ void decode_item(const AttnArgs &a, const int32_t *it, char *smem) {
 }
 
 // --------------------------------------------------------------- prefill, fp32 scalar path
-template <typename T, int HD, int G>
-__device__ void prefill_item_scalar(const AttnArgs &a, const int32_t *it) {
+template <int HD, int G>
+__device__ void prefill_item_f32(const AttnArgs &a, const int32_t *it) {
     const int tid = threadIdx.x;
     const int ci = it[IT_INDEX], g = it[IT_KVHEAD], qb = it[IT_A], qn = it[IT_B];
     if (tid >= qn * G) return;
@@ -209,64 +321,145 @@ __device__ void prefill_item_scalar(const AttnArgs &a, const int32_t *it) {
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], tok = ch[4] + qb + r;
     const int qpos = off + qb + r;
-    const PoolView pv = pool_view(a, 0, sizeof(T));
-    const int P = a.page;
-    const size_t page_elems = (size_t)a.nkv * P * HD;
-    const T *qp = (const T *)a.q + ((size_t)tok * a.nq + h) * HD;
+    const PoolView pv = pool_view(a, 0);
+    const size_t page_elems = (size_t)a.nkv * kPage * HD;
+    const float *qp = (const float *)a.q + ((size_t)tok * a.nq + h) * HD;
     float q[HD], acc[HD];
     const float scale = kLog2e / sqrtf((float)HD);
 #pragma unroll
     for (int d = 0; d < HD; ++d) {
-        q[d] = to_f32(qp[d]) * scale;
+        q[d] = qp[d] * scale;
         acc[d] = 0.f;
     }
     float m = -INFINITY, l = 0.f;
     for (int kp = 0; kp <= qpos; ++kp) {
-        const int page = pv.bt[(size_t)seq * pv.max_blocks + kp / P];
+        const int page = pv.bt[(size_t)seq * pv.max_blocks + kp / kPage];
         if (page < 0 || page >= pv.n_pages) {
             flag_error(a.err, ORTHRUS_DEVERR_PAGE);
             continue;
         }
-        const size_t base = (size_t)page * page_elems + ((size_t)g * P + kp % P) * HD;
-        const T *kr = (const T *)pv.k + base;
-        const T *vr = (const T *)pv.v + base;
+        const float *kr = (const float *)pv.k + page * page_elems + ((size_t)g * kPage + kp % kPage) * HD;
+        const float *vr = (const float *)pv.v + page * page_elems + (size_t)g * HD * kPage + kp % kPage;
         float s = 0.f;
 #pragma unroll
-        for (int d = 0; d < HD; ++d) s = fmaf(q[d], to_f32(kr[d]), s);
+        for (int d = 0; d < HD; ++d) s = fmaf(q[d], kr[d], s);
         const float mn = fmaxf(m, s);
         const float alpha = exp2f(m - mn), p = exp2f(s - mn);
         l = l * alpha + p;
 #pragma unroll
-        for (int d = 0; d < HD; ++d) acc[d] = fmaf(p, to_f32(vr[d]), acc[d] * alpha);
+        for (int d = 0; d < HD; ++d) acc[d] = fmaf(p, vr[d * kPage], acc[d] * alpha);
         m = mn;
     }
-    T *op = (T *)a.o + ((size_t)tok * a.nq + h) * HD;
+    float *op = (float *)a.o + ((size_t)tok * a.nq + h) * HD;
 #pragma unroll
-    for (int d = 0; d < HD; ++d) op[d] = from_f32<T>(l > 0.f ? acc[d] / l : 0.f);
+    for (int d = 0; d < HD; ++d) op[d] = l > 0.f ? acc[d] / l : 0.f;
 }
 
 // ------------------------------------------------------------------ prefill, bf16 MFMA path
+// 32-key blocks (two pages) are staged cooperatively into LDS: keys as [key][dim] rows, values
+// as [dim][key] rows (the cache already stores each page dim-major, so this is a plain copy).
+// Global loads of block kb+1 (and the page ids of block kb+2) are issued before block kb is
+// computed and land in the other LDS buffer after it; one barrier per block.
+template <int HD>
+struct PrefillStage {
+    static constexpr int KROW = HD * 2 + 16;      // padded key row (bytes)
+    static constexpr int VROW = 32 * 2 + 8;       // padded value row over 32 keys (bytes)
+    static constexpr int KCH = 32 * HD / 8;       // 16-byte chunks of the key block
+    static constexpr int VCH = 2 * HD * 2;        // 16-byte chunks of the value block
+    static constexpr int PER_THREAD = (KCH + VCH) / 256;
+    static constexpr int BYTES = 32 * KROW + HD * VROW;
+    static_assert((KCH + VCH) % 256 == 0, "chunks per thread");
+};
+
 template <int HD, int G>
 __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *smem) {
-    constexpr int KS = HD / 16;        // 16-wide k steps of S^T = K Q^T
-    constexpr int DB = HD / 32;        // 32-row dim blocks of O^T
-    constexpr int KROW = HD * 2 + 16;  // padded K row bytes in LDS
-    constexpr int VROW = 32 * 2 + 8;   // padded V^T row bytes in LDS (32 keys)
-    char *k_lds = smem;
-    char *v_lds = smem + 32 * KROW;
+    using St = PrefillStage<HD>;
+    constexpr int KS = HD / 16, DB = HD / 32;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int ci = it[IT_INDEX], g = it[IT_KVHEAD], qb = it[IT_A], qn = it[IT_B], kend = it[IT_KEY_END];
+    const int ci = it[IT_INDEX], g = it[IT_KVHEAD], qb = it[IT_A], qn = it[IT_B];
+    const int kend = it[IT_KEY_END];               // causal bound of the whole tile
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], tok0 = ch[4];
-    const int h = g * G + (wave % G), sb = wave / G;
+    const int sb = wave / G;
+    const int h = g * G + (wave % G);
     const int col = lane & 31, half = lane >> 5;
-    // this lane's query (clamped into the tile so padded rows stay finite)
-    const int r = min(sb * 32 + col, qn - 1);
-    const int tok = tok0 + qb + r;
-    const int qpos = off + qb + r;
-    const PoolView pv = pool_view(a, 0, 2);
-    const int P = a.page;
-    const size_t page_elems = (size_t)a.nkv * P * HD;
+    const int rows = max(0, min(32, qn - sb * 32));
+    const int r = sb * 32 + min(col, max(rows, 1) - 1);   // padded rows repeat a valid row
+    const int tok = tok0 + qb + min(r, qn - 1);
+    const int qpos = off + qb + min(r, qn - 1);
+    const PoolView pv = pool_view(a, 0);
+    const size_t page_bytes = (size_t)a.nkv * kPage * HD * 2;
+    const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks;
+    const int nkb = (kend + 31) / 32;
+    const int last_block = (kend - 1) / kPage;      // last page index the tile reads
+
+    // page ids of the tile's keys, staged in LDS a window at a time (validated there, -1 = bad)
+    int *pg_lds = (int *)(smem + 2 * St::BYTES);
+    auto load_window = [&](int w0) {
+        bool bad = false;
+        for (int i = tid; i < kPrefillPageWindow && w0 + i <= last_block; i += 256) {
+            const int pg = bt[w0 + i];
+            const bool ok = pg >= 0 && pg < pv.n_pages;
+            bad |= !ok;
+            pg_lds[i] = ok ? pg : -1;
+        }
+        if (bad) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+    };
+    int w0 = 0;
+    auto page_of = [&](int blk) -> int2 {  // pages of the block's two halves; -1 = bad
+        const int p0 = min(2 * blk, last_block), p1 = min(2 * blk + 1, last_block);
+        return int2{pg_lds[p0 - w0], pg_lds[p1 - w0]};
+    };
+
+    // chunk assignment of this thread: PER_THREAD chunks c = tid + 256 * i over [K | V]; two
+    // register stages keep the loads of the next two blocks in flight
+    u32x4 stg0[St::PER_THREAD], stg1[St::PER_THREAD];
+    auto issue = [&](u32x4 (&stg)[St::PER_THREAD], int2 pg) {
+        const int sp0 = pg.x >= 0 ? pg.x : 0, sp1 = pg.y >= 0 ? pg.y : 0;
+#pragma unroll
+        for (int i = 0; i < St::PER_THREAD; ++i) {
+            const int c = tid + 256 * i;
+            const char *src;
+            if (c < St::KCH) {
+                const int key = c / (HD / 8), part = c % (HD / 8);
+                const int pgid = key < kPage ? sp0 : sp1;
+                src = pv.k + pgid * page_bytes + (size_t)((g * kPage + (key & 15)) * HD + part * 8) * 2;
+            } else {
+                const int v = c - St::KCH;
+                const int p2 = v / (HD * 2), rem = v % (HD * 2);
+                const int d = rem >> 1, h2 = rem & 1;
+                const int pgid = p2 ? sp1 : sp0;
+                src = pv.v + pgid * page_bytes + (size_t)((g * HD + d) * kPage) * 2 + h2 * 16;
+            }
+            stg[i] = *(const u32x4 *)src;
+        }
+    };
+    auto stash = [&](const u32x4 (&stg)[St::PER_THREAD], char *buf, int blk, int2 pg) {
+        const bool ok0 = pg.x >= 0, ok1 = pg.y >= 0;
+#pragma unroll
+        for (int i = 0; i < St::PER_THREAD; ++i) {
+            const int c = tid + 256 * i;
+            u32x4 v = stg[i];
+            if (c < St::KCH) {
+                const int key = c / (HD / 8), part = c % (HD / 8);
+                const bool keep = (key < kPage ? ok0 : ok1) && blk * 32 + key < kend;
+                if (!keep) v = u32x4{0u, 0u, 0u, 0u};
+                *(u32x4 *)(buf + key * St::KROW + part * 16) = v;
+            } else {
+                const int vi = c - St::KCH;
+                const int p2 = vi / (HD * 2), rem = vi % (HD * 2);
+                const int d = rem >> 1, h2 = rem & 1;
+                // zero positions at or past the causal bound (other data or NaN poison)
+                const int nvalid = (p2 ? ok1 : ok0) ? kend - (blk * 32 + p2 * kPage + h2 * 8) : 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t m = (2 * e + 1 < nvalid) ? 0xffffffffu : ((2 * e < nvalid) ? 0xffffu : 0u);
+                    v[e] &= m;
+                }
+                *(u32x4 *)(buf + 32 * St::KROW + d * St::VROW + p2 * 32 + h2 * 16) = v;
+            }
+        }
+    };
 
     bf16x8 qf[KS];
     const bf16 *qp = (const bf16 *)a.q + ((size_t)tok * a.nq + h) * HD;
@@ -280,84 +473,108 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         for (int e = 0; e < 16; ++e) acc[d][e] = 0.f;
     float m = -INFINITY, l = 0.f;
     const float scale = kLog2e / sqrtf((float)HD);
-    const int nkb = (kend + 31) / 32;
+    const int wave_first = off + qb + sb * 32;    // first query position of this wave
 
-    for (int kb = 0; kb < nkb; ++kb) {
-        // stage 32 keys: K rows as-is, V transposed to [dim][key]
-        for (int c = tid; c < 32 * (HD / 8); c += 256) {
-            const int key = c / (HD / 8), part = c % (HD / 8);
-            const int kpos = kb * 32 + key;
-            u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-            if (kpos < kend) {
-                const int page = pv.bt[(size_t)seq * pv.max_blocks + kpos / P];
-                if (page >= 0 && page < pv.n_pages) {
-                    const size_t base = ((size_t)page * page_elems + ((size_t)g * P + kpos % P) * HD + part * 8) * 2;
-                    kv = *(const u32x4 *)(pv.k + base);
-                    vv = *(const u32x4 *)(pv.v + base);
-                } else if (part == 0) {
-                    flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+    // page ids of block b, switching the LDS window when b leaves it (blocks never straddle a
+    // window: windows start at even pages); called at the same point by every thread
+    auto block_pages = [&](int b) -> int2 {
+        if (2 * b - w0 >= kPrefillPageWindow) {
+            __syncthreads();
+            w0 += kPrefillPageWindow;
+            load_window(w0);
+            __syncthreads();
+        }
+        return page_of(b);
+    };
+    auto compute = [&](int kb) {
+        const char *buf = smem + (kb & 1) * St::BYTES;
+        if (rows > 0 && kb * 32 <= wave_first + rows - 1) {
+            const char *kl = buf, *vl = buf + 32 * St::KROW;
+            f32x16 s;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) s[e] = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) {
+                const bf16x8 kf = *(const bf16x8 *)(kl + col * St::KROW + (kk * 16 + half * 8) * 2);
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+            }
+            // lane's query = col; register e holds key 8*(e/4) + 4*half + e%4 of the block
+            const bool diag = (kb + 1) * 32 > wave_first;
+            float mloc = -INFINITY;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int kpos = kb * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                const bool vis = !diag || kpos <= qpos;
+                s[e] = vis ? s[e] * scale : -INFINITY;
+                mloc = fmaxf(mloc, s[e]);
+            }
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+            const float mn = fmaxf(m, mloc);
+            const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mn);
+            float psum = 0.f;
+            bf16x8 pf[2];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const float p = (mn == -INFINITY) ? 0.f : exp2f(s[e] - mn);
+                psum += p;
+                pf[e >> 3][e & 7] = from_f32<bf16>(p);
+            }
+            psum += __shfl_xor(psum, 32, 64);
+            l = l * alpha + psum;
+            m = mn;
+#pragma unroll
+            for (int d = 0; d < DB; ++d)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[d][e] *= alpha;
+            // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; lane half `half` holds keys
+            // 16*k2 + 4*half .. +3 and 16*k2 + 8 + 4*half .. +3 of the block
+#pragma unroll
+            for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+                for (int d = 0; d < DB; ++d) {
+                    const char *vrow = vl + (d * 32 + col) * St::VROW + k2 * 32;
+                    const uint64_t lo = *(const uint64_t *)(vrow + half * 8);
+                    const uint64_t hi = *(const uint64_t *)(vrow + 16 + half * 8);
+                    u32x4 vu = {(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
+                    acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pf[k2],
+                                                                     acc[d], 0, 0, 0);
                 }
-            }
-            *(u32x4 *)(k_lds + key * KROW + part * 16) = kv;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                *(uint16_t *)(v_lds + (part * 8 + 2 * e) * VROW + key * 2) = (uint16_t)(vv[e] & 0xffffu);
-                *(uint16_t *)(v_lds + (part * 8 + 2 * e + 1) * VROW + key * 2) = (uint16_t)(vv[e] >> 16);
-            }
+        }
+    };
+    load_window(0);
+    __syncthreads();
+    int2 pg_b0 = page_of(0);
+    issue(stg0, pg_b0);
+    stash(stg0, smem, 0, pg_b0);
+    int2 pg_b1 = nkb > 1 ? page_of(1) : int2{-1, -1};
+    int2 pg_b2 = nkb > 2 ? page_of(2) : int2{-1, -1};
+    if (nkb > 1) issue(stg1, pg_b1);
+    if (nkb > 2) issue(stg0, pg_b2);
+    __syncthreads();
+    // iteration kb: compute block kb, stash block kb + 1 from its stage, reuse that stage for
+    // block kb + 3; stage of block b is stg1 for odd b, stg0 for even b
+    for (int kb = 0; kb < nkb; kb += 2) {
+        compute(kb);
+        if (kb + 1 < nkb) stash(stg1, smem + St::BYTES, kb + 1, pg_b1);
+        int2 pg_b3 = {-1, -1};
+        if (kb + 3 < nkb) {
+            pg_b3 = block_pages(kb + 3);
+            issue(stg1, pg_b3);
         }
         __syncthreads();
-
-        // S^T[key][query] for this wave's 32 queries
-        f32x16 s;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[e] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-            const bf16x8 kf = *(const bf16x8 *)(k_lds + col * KROW + (kk * 16 + half * 8) * 2);
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
-        }
-        // mask + online softmax (lane's query = col; keys of register e: 8*(e/4) + 4*half + e%4)
-        float mloc = -INFINITY;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int kpos = kb * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-            const bool vis = kpos <= qpos && kpos < kend;
-            s[e] = vis ? s[e] * scale : -INFINITY;
-            mloc = fmaxf(mloc, s[e]);
-        }
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-        const float mn = fmaxf(m, mloc);
-        const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mn);
-        float psum = 0.f;
-        bf16x8 pf[2];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const float p = (mn == -INFINITY) ? 0.f : exp2f(s[e] - mn);
-            psum += p;
-            pf[e >> 3][e & 7] = from_f32<bf16>(p);
-        }
-        psum += __shfl_xor(psum, 32, 64);
-        l = l * alpha + psum;
-        m = mn;
-#pragma unroll
-        for (int d = 0; d < DB; ++d)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[d][e] *= alpha;
-        // O^T[dim][query] += V^T[dim][keys] P^T[keys][query], two 16-key steps
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2) {
-#pragma unroll
-            for (int d = 0; d < DB; ++d) {
-                const char *vr = v_lds + (d * 32 + col) * VROW;
-                const uint64_t lo = *(const uint64_t *)(vr + (k2 * 16 + half * 4) * 2);
-                const uint64_t hi = *(const uint64_t *)(vr + (k2 * 16 + 8 + half * 4) * 2);
-                u32x4 vu = {(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
-                acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pf[k2], acc[d], 0, 0, 0);
-            }
+        if (kb + 1 >= nkb) break;
+        compute(kb + 1);
+        if (kb + 2 < nkb) stash(stg0, smem, kb + 2, pg_b2);
+        int2 pg_b4 = {-1, -1};
+        if (kb + 4 < nkb) {
+            pg_b4 = block_pages(kb + 4);
+            issue(stg0, pg_b4);
         }
         __syncthreads();
+        pg_b1 = pg_b3;
+        pg_b2 = pg_b4;
     }
-    if (sb * 32 + col >= qn) return;
+    if (col >= rows) return;
     const float inv = l > 0.f ? 1.f / l : 0.f;
     bf16 *op = (bf16 *)a.o + ((size_t)tok * a.nq + h) * HD;
 #pragma unroll
@@ -371,22 +588,25 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         }
 }
 
-template <typename T, int HD, int G>
+template <bool BF16, int HD, int G>
 constexpr size_t attn_smem() {
-    constexpr size_t dec = (kSplitPages * 16 * G + 8 * G + 16 * 16 * G * (HD / 16)) * sizeof(float);
-    constexpr size_t pre = sizeof(T) == 2 ? 32 * (HD * 2 + 16) + HD * (32 * 2 + 8) : 0;
+    constexpr int MAXK = kSplitPages * kPage;
+    constexpr size_t dec = BF16 ? (4 * (MAXK / 4 / 2) * G + 8 * G + 4 * G * HD) * 4
+                                : (MAXK * G + 8 * G + 4 * G * HD) * 4;
+    constexpr size_t pre = BF16 ? 2 * PrefillStage<HD>::BYTES + 4 * kPrefillPageWindow : 0;
     return dec > pre ? dec : pre;
 }
 
-template <typename T, int HD, int G>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) char smem[attn_smem<T, HD, G>()];
+template <bool BF16, int HD, int G>
+__global__ __launch_bounds__(256, BF16 ? 2 : 1) void attn_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) char smem[attn_smem<BF16, HD, G>()];
     const int32_t *it = a.items + kItemInts * blockIdx.x;
     if (it[IT_KIND] == 0) {
-        if constexpr (sizeof(T) == 2) prefill_item_mfma<HD, G>(a, it, smem);
-        else prefill_item_scalar<T, HD, G>(a, it);
+        if constexpr (BF16) prefill_item_mfma<HD, G>(a, it, smem);
+        else prefill_item_f32<HD, G>(a, it);
     } else {
-        decode_item<T, HD, G>(a, it, smem);
+        if constexpr (BF16) decode_item_bf16<HD, G>(a, it, smem);
+        else decode_item_f32<HD, G>(a, it, smem);
     }
 }
 
@@ -410,25 +630,24 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a) {
     ((T *)a.o)[((size_t)tok * a.nq + h) * HD + d] = from_f32<T>(L > 0.f ? acc / L : 0.f);
 }
 
-template <typename T, int HD, int G>
-hipError_t run_attn(const AttnArgs &a, hipStream_t s) {
+template <bool BF16, int HD, int G>
+hipError_t run(const AttnArgs &a, int n_decode, bool combine, hipStream_t s) {
+    if (combine) {
+        if (n_decode <= 0) return hipSuccess;
+        if (BF16) hipLaunchKernelGGL((attn_combine_kernel<bf16, HD, G>), dim3(n_decode, a.nq), dim3(HD), 0, s, a);
+        else hipLaunchKernelGGL((attn_combine_kernel<float, HD, G>), dim3(n_decode, a.nq), dim3(HD), 0, s, a);
+        return hipGetLastError();
+    }
     if (a.n_items <= 0) return hipSuccess;
-    hipLaunchKernelGGL((attn_kernel<T, HD, G>), dim3(a.n_items), dim3(256), 0, s, a);
-    return hipGetLastError();
-}
-template <typename T, int HD, int G>
-hipError_t run_combine(const AttnArgs &a, int n_decode, hipStream_t s) {
-    if (n_decode <= 0) return hipSuccess;
-    hipLaunchKernelGGL((attn_combine_kernel<T, HD, G>), dim3(n_decode, a.nq), dim3(HD), 0, s, a);
+    hipLaunchKernelGGL((attn_kernel<BF16, HD, G>), dim3(a.n_items), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-template <typename T>
+template <bool BF16>
 hipError_t dispatch(const AttnArgs &a, int n_decode, bool combine, hipStream_t s) {
     const int G = a.nq / a.nkv;
-#define ORTHRUS_ATTN_CASE(HDV, GV)                                                         \
-    if (a.hd == HDV && G == GV)                                                            \
-        return combine ? run_combine<T, HDV, GV>(a, n_decode, s) : run_attn<T, HDV, GV>(a, s);
+#define ORTHRUS_ATTN_CASE(HDV, GV) \
+    if (a.hd == HDV && G == GV) return run<BF16, HDV, GV>(a, n_decode, combine, s);
     ORTHRUS_ATTN_CASE(128, 4)
     ORTHRUS_ATTN_CASE(128, 2)
     ORTHRUS_ATTN_CASE(128, 1)
@@ -442,11 +661,11 @@ hipError_t dispatch(const AttnArgs &a, int n_decode, bool combine, hipStream_t s
 }  // namespace
 
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
-    return dtype == 1 ? dispatch<bf16>(a, 0, false, s) : dispatch<float>(a, 0, false, s);
+    return dtype == 1 ? dispatch<true>(a, 0, false, s) : dispatch<false>(a, 0, false, s);
 }
 
 hipError_t launch_attn_combine(int dtype, const AttnArgs &a, int n_decode, hipStream_t s) {
-    return dtype == 1 ? dispatch<bf16>(a, n_decode, true, s) : dispatch<float>(a, n_decode, true, s);
+    return dtype == 1 ? dispatch<true>(a, n_decode, true, s) : dispatch<false>(a, n_decode, true, s);
 }
 
 }  // namespace orthrus

@@ -43,8 +43,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
 }
 
 // q, k rotated at their absolute positions (pairs (i, i + hd/2), angle pos * base^(-2i/hd),
-// evaluated in double), q stored for attention, rotated k and raw v appended to the cache slot
-// block_table[seq][pos / page] * page + pos % page.
+// evaluated in double), q stored for attention, rotated k and raw v appended at position
+// pos % page of page block_table[seq][pos / page] (keys [kv head][slot][dim], values
+// [kv head][dim][slot]).
 template <typename T>
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
     __shared__ float cs[64], sn[64];
@@ -85,12 +86,10 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
         }
     }
     if (ok) {
+        // values are stored dim-major inside a page: [kv head][dim][slot]
         const float *vs = src + (size_t)(a.nq + a.nkv) * a.hd;
-        for (int w = threadIdx.x; w < a.nkv * a.hd; w += 256) {
-            const int g = w / a.hd, i = w % a.hd;
-            T *v = (T *)a.v_cache[p] + slot + (size_t)g * a.page * a.hd;
-            v[i] = from_f32<T>(vs[w]);
-        }
+        T *v = (T *)a.v_cache[p] + (size_t)page * a.nkv * a.hd * a.page + pos % a.page;
+        for (int w = threadIdx.x; w < a.nkv * a.hd; w += 256) v[(size_t)w * a.page] = from_f32<T>(vs[w]);
     }
 }
 

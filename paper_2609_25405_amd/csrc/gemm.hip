@@ -1,10 +1,11 @@
 // Dense projections of the step: C[M][N] = A[M][K] * W[N][K]^T over the concatenated token
 // batch (QKV, attention output, gate/up, down, LM head), with fused epilogues.
 //
-// bf16 path: CDNA4 MFMA v_mfma_f32_32x32x16_bf16, 256 threads (4 wave64s in a WM x WN grid),
-// K staged 64 elements at a time through two LDS buffers with a register prefetch of the
-// next stage, so each K step costs one barrier.  LDS rows are 128 B; 16-byte chunks are
-// XOR-swizzled by row so the per-lane 16-byte operand reads of one MFMA spread over banks.
+// bf16 path: CDNA4 MFMA v_mfma_f32_32x32x16_bf16, WM x WN wave64s per workgroup, K staged 64
+// elements at a time through two LDS buffers filled by direct global->LDS copies
+// (global_load_lds_dwordx4, no register staging), so each K stage costs one barrier.  LDS rows
+// are 128 B; 16-byte chunks are XOR-swizzled by row so the per-lane 16-byte operand reads of
+// one MFMA hit distinct banks (the copies pick their source chunk to land in swizzled order).
 // Tiles are mapped to blocks so that consecutive tiles of one weight column block land on
 // the same XCD (blocks are dealt round-robin to the 8 XCDs), which keeps re-reads of a
 // weight tile inside one L2.
@@ -23,15 +24,22 @@ __device__ __forceinline__ int swz(int row, int chunk) {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
 
+// 16-byte global -> LDS copy: lane i of the wave writes lds + 16 * i (lds is wave-uniform)
+__device__ __forceinline__ void copy16_to_lds(const void *src, char *lds) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
+}
+
 template <int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) {
+    constexpr int NW = WM * WN;               // waves per workgroup
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / 32, FN = TN / 32;
-    constexpr int A_LOADS = BM * 8 / 256, B_LOADS = BN * 8 / 256;
+    // global -> LDS copies of one K stage: every wave instruction moves 1 KiB = 8 rows of 128 B
+    constexpr int A_INST = BM / (8 * NW), B_INST = BN / (8 * NW);
     constexpr int STAGE = (BM + BN) * BK * 2;
-    static_assert(WM * WN == 4, "four waves");
+    static_assert(A_INST * 8 * NW == BM && B_INST * 8 * NW == BN, "copy split");
     static_assert(FM >= 1 && FN >= 1 && (EPI != EPI_SWIGLU || FN % 2 == 0), "tile shape");
-    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
@@ -44,22 +52,22 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     constexpr int COLS = EPI == EPI_SWIGLU ? BN / 2 : BN;  // output columns per tile
     const int n0 = n_tile * COLS;
 
-    const char *Abase = (const char *)a.A;
+    // Lane `lane` of copy instruction i of this wave writes LDS bytes base + 16 * lane, i.e. row
+    // r0 + lane / 8 (r0 = 8 * (NW i + wave)) at physical chunk lane % 8.  The row's logical k chunk
+    // there is (lane % 8) ^ swizzle(row), so that is the 16 bytes the lane fetches.
     const size_t lda_b = (size_t)a.lda * 2, ldb_b = (size_t)a.K * 2;
-    uint32_t a_off[A_LOADS], b_off[B_LOADS];
-    const char *b_src[B_LOADS];
-    int a_lds[A_LOADS], b_lds[B_LOADS];
-    const int ch = tid & 7;
+    const char *a_src[A_INST];
+    const char *b_src[B_INST];
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-        const int row = (tid >> 3) + 32 * i;
-        const int grow = min(m0 + row, a.M - 1);
-        a_off[i] = (uint32_t)(grow * lda_b + ch * 16);
-        a_lds[i] = swz(row, ch);
+    for (int i = 0; i < A_INST; ++i) {
+        const int row = 8 * (NW * i + wave) + (lane >> 3);
+        const int chunk = (lane & 7) ^ ((row >> 1) & 7);
+        a_src[i] = (const char *)a.A + (size_t)min(m0 + row, a.M - 1) * lda_b + chunk * 16;
     }
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i) {
-        const int r = (tid >> 3) + 32 * i;
+    for (int i = 0; i < B_INST; ++i) {
+        const int r = 8 * (NW * i + wave) + (lane >> 3);
+        const int chunk = (lane & 7) ^ (((BM + r) >> 1) & 7);
         int grow;
         const char *src = (const char *)a.B0;
         if (EPI == EPI_SWIGLU) {
@@ -70,29 +78,18 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
         } else {
             grow = n0 + r;
         }
-        grow = min(grow, a.N - 1);
-        b_src[i] = src;
-        b_off[i] = (uint32_t)(grow * ldb_b + ch * 16);
-        b_lds[i] = swz(BM + r, ch);
+        b_src[i] = src + (size_t)min(grow, a.N - 1) * ldb_b + chunk * 16;
     }
-
-    u32x4 ra[A_LOADS], rb[B_LOADS];
-    auto gload = [&](int kt) {
-        const uint32_t kb = (uint32_t)kt * (BK * 2);
+    auto issue = [&](int kt, int buf) {
+        const size_t kb = (size_t)kt * (BK * 2);
+        char *s = smem + buf * STAGE;
 #pragma unroll
-        for (int i = 0; i < A_LOADS; ++i) ra[i] = *(const u32x4 *)(Abase + a_off[i] + kb);
+        for (int i = 0; i < A_INST; ++i)
+            copy16_to_lds(a_src[i] + kb, s + (NW * i + wave) * 1024);
 #pragma unroll
-        for (int i = 0; i < B_LOADS; ++i) rb[i] = *(const u32x4 *)(b_src[i] + b_off[i] + kb);
+        for (int i = 0; i < B_INST; ++i)
+            copy16_to_lds(b_src[i] + kb, s + BM * 128 + (NW * i + wave) * 1024);
     };
-    auto lstore_to = [&](char *s) {
-#pragma unroll
-        for (int i = 0; i < A_LOADS; ++i) *(u32x4 *)(s + a_lds[i]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < B_LOADS; ++i) *(u32x4 *)(s + b_lds[i]) = rb[i];
-    };
-    auto lstore = [&](int buf) { lstore_to(smem + buf * STAGE); };
-    int next_k = 0;
-    auto gload_next = [&]() { gload(next_k); };
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -117,14 +114,19 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
             fb[buf][ni] = *(const bf16x8 *)(s + (brow + ni * 32) * 128 + ((chk ^ bkey) << 4));
     };
 
-    // One K stage per iteration, software-pipelined by hand (the scheduler is told the order):
-    //   LDS fragments of k-step 0, then per k-step its MFMAs interleaved with the LDS reads of the
-    //   next k-step's fragments; the next stage's global loads ride along k-step 0 and its LDS
-    //   stores (other buffer, not read this iteration) along k-step 3.  One barrier per stage.
-    constexpr int NMF = FM * FN, NFR = FM + FN, NLD = A_LOADS + B_LOADS;
-    auto stage = [&](const char *s, char *s_next, bool more) {
+    // One K stage per iteration: wait for this stage's copies, barrier (which also frees the
+    // other buffer), start the next stage's copies, then the MFMAs with the next k-step's
+    // fragments read from LDS under the current k-step's MFMAs (order given to the scheduler).
+    constexpr int NMF = FM * FN, NFR = FM + FN, NLD = A_INST + B_INST;
+    const int nk = a.K / BK;
+    issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        const bool more = kt + 1 < nk;
+        if (more) issue(kt + 1, (kt + 1) & 1);
+        const char *s = smem + (kt & 1) * STAGE;
         lds_frag(s, 0, 0);
-        if (more) gload_next();
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
             if (kk + 1 < BK / 16) lds_frag(s, kk + 1, (kk + 1) & 1);
@@ -134,35 +136,19 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
                 for (int ni = 0; ni < FN; ++ni)
                     acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][mi], fb[kk & 1][ni],
                                                                           acc[mi][ni], 0, 0, 0);
-            if (kk == BK / 16 - 1 && more) lstore_to(s_next);
         }
-        // schedule: DS_READ=0x100, DS_WRITE=0x200, VMEM_READ=0x020, MFMA=0x008
+        // schedule: DS_READ=0x100, MFMA=0x008
         __builtin_amdgcn_sched_group_barrier(0x100, NFR, 0);
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
 #pragma unroll
             for (int i = 0; i < NMF; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                if (kk == 0 && more) {
-                    if (i < NLD) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-                }
                 if (kk + 1 < BK / 16 && i < NFR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                if (kk == BK / 16 - 1 && more && i < NLD) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
             }
         }
-    };
-
-    const int nk = a.K / BK;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    int kt = 0;
-    for (; kt + 1 < nk; ++kt) {
-        next_k = kt + 1;
-        stage(smem + (kt & 1) * STAGE, smem + ((kt + 1) & 1) * STAGE, true);
-        __syncthreads();
     }
-    stage(smem + (kt & 1) * STAGE, nullptr, false);
+    (void)NLD;
 
     // epilogue: lane holds column (lane & 31) of each 32x32 tile, rows 8*(r/4) + 4*(lane/32) + r%4
 #pragma unroll
@@ -255,16 +241,18 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
     const int mt = (a.M + BM - 1) / BM;
     const int cols = EPI == EPI_SWIGLU ? BN / 2 : BN;
     const int nt = (a.N + cols - 1) / cols;
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(mt * nt), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(mt * nt), dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
 }
 
+// Tile choice per shape, from measurements of the step's projections on MI355X: 128x128
+// tiles (64 KiB of LDS, two workgroups per CU, so one hides the other's barrier and copy
+// waits) beat larger tiles on every projection of a 384..2048-token batch; the gate/up pair
+// does slightly better with 192x256.  Very short batches (decode-only LM head) use 64x256.
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
     if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI>(a, s);
-    const long long big = (long long)((a.M + 255) / 256) * ((a.N + (EPI == EPI_SWIGLU ? 127 : 255)) /
-                                                             (EPI == EPI_SWIGLU ? 128 : 256));
-    if (big >= 512) return run_bf16<256, 256, 2, 2, EPI>(a, s);
+    if (EPI == EPI_SWIGLU && a.M > 128) return run_bf16<192, 256, 2, 2, EPI>(a, s);
     return run_bf16<128, 128, 2, 2, EPI>(a, s);
 }
 

@@ -80,28 +80,38 @@ class DeviceModel:
 
 
 class DeviceKV:
-    """Paged KV pools [L][n_pages][n_kv][page][hd] and the int32 block table, on the GPU."""
+    """Paged KV pools and the int32 block table, on the GPU.
+
+    Keys are [L][n_pages][n_kv][page][hd] (position-major inside a page), values
+    [L][n_pages][n_kv][hd][page] (dim-major inside a page), the layouts include/orthrus.h fixes.
+    ``v_by_position`` is a [L][n_pages][n_kv][page][hd] view of the values.
+    """
 
     def __init__(self, cfg, n_pages: int, n_seq: int, max_blocks: int, device="cuda",
                  fill: float = float("nan")):
         self.cfg = cfg
-        shape = (cfg.n_layers, n_pages, cfg.n_kv_heads, cfg.page_size, cfg.head_dim)
+        L, P, kvh, hd = cfg.n_layers, cfg.page_size, cfg.n_kv_heads, cfg.head_dim
         dt = torch_dtype(cfg)
-        self.k = torch.full(shape, fill, dtype=dt, device=device)
-        self.v = torch.full(shape, fill, dtype=dt, device=device)
+        self.k = torch.full((L, n_pages, kvh, P, hd), fill, dtype=dt, device=device)
+        self.v = torch.full((L, n_pages, kvh, hd, P), fill, dtype=dt, device=device)
         self.block_table = torch.full((n_seq, max_blocks), -1, dtype=torch.int32, device=device)
         self.n_pages, self.n_seq, self.max_blocks = n_pages, n_seq, max_blocks
 
     @classmethod
     def from_paged(cls, paged, device="cuda") -> "DeviceKV":
+        """Upload a host image whose pools are both [L][n_pages][n_kv][page][hd]."""
         kv = cls.__new__(cls)
         kv.cfg = paged.cfg
         dt = torch_dtype(paged.cfg)
         kv.k = torch.from_numpy(paged.k).to(device=device, dtype=dt)
-        kv.v = torch.from_numpy(paged.v).to(device=device, dtype=dt)
+        kv.v = torch.from_numpy(paged.v).to(device=device, dtype=dt).transpose(-1, -2).contiguous()
         kv.block_table = torch.from_numpy(paged.block_table).to(device)
         kv.n_pages, kv.n_seq, kv.max_blocks = paged.n_pages, paged.n_seq, paged.max_blocks
         return kv
+
+    @property
+    def v_by_position(self) -> torch.Tensor:
+        return self.v.transpose(-1, -2)
 
     def set_block_table(self, bt: np.ndarray) -> None:
         self.block_table.copy_(torch.from_numpy(np.ascontiguousarray(bt, np.int32)))

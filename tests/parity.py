@@ -89,9 +89,9 @@ class Pair:
         nc, nd = len(batch.chunks), len(batch.rows)
         logits = torch.full((max(1, nd), self.gen[0].vocab), float("nan"), device="cuda")
         out_emb = torch.full((max(1, nc), cfg.d_model), float("nan"), device="cuda")
-        pre = [(_bits(self.dkv_e.k).clone(), _bits(self.dkv_e.v).clone())] if check_kv else None
+        pre = [(_bits(self.dkv_e.k).clone(), _bits(self.dkv_e.v_by_position).clone())] if check_kv else None
         if check_kv and not self.shared_kv:
-            pre.append((_bits(self.dkv_g.k).clone(), _bits(self.dkv_g.v).clone()))
+            pre.append((_bits(self.dkv_g.k).clone(), _bits(self.dkv_g.v_by_position).clone()))
         R.step(self.dm_e, self.dm_g, batch, self.dkv_e, self.dkv_g, self.acc_sum, self.acc_w,
                logits, out_emb, self.ws)
         torch.cuda.synchronize()
@@ -133,7 +133,7 @@ class Pair:
                 pg = torch.tensor([m[0] for m in mine], device="cuda")
                 of = torch.tensor([m[1] for m in mine], device="cuda")
                 mask[pg, :, of] = True
-            for which, now, before in (("k", dkv.k, pre[pi][0]), ("v", dkv.v, pre[pi][1])):
+            for which, now, before in (("k", dkv.k, pre[pi][0]), ("v", dkv.v_by_position, pre[pi][1])):
                 same = _bits(now) == before
                 # slots the step does not own keep their bytes in every layer
                 assert bool(same[:, ~mask].all()), f"{which}: a slot outside the step changed"
