@@ -610,32 +610,37 @@ __global__ __launch_bounds__(256, BF16 ? 2 : 1) void attn_kernel(AttnArgs a) {
     }
 }
 
+// Merge the key-range splits of one (decode row, KV head) for its `group` query heads, in split
+// order: M = max m_s, L = sum l_s 2^(m_s - M), o = sum acc_s 2^(m_s - M) / L.
 template <typename T, int HD, int G>
-__global__ __launch_bounds__(HD) void attn_combine_kernel(AttnArgs a) {
-    const int j = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+__global__ __launch_bounds__(G * HD) void attn_combine_kernel(AttnArgs a) {
+    const int j = blockIdx.x, g = blockIdx.y;
+    const int h = threadIdx.x / HD, d = threadIdx.x % HD;
     const int32_t *row = a.rows + kRowInts * j;
     const int nsplit = row[3], base = row[4], tok = row[2];
     if (nsplit <= 1) return;
-    const int g = h / G, hl = h % G;
+    constexpr int STRIDE = G * (HD + 2);  // floats between consecutive splits of one head
+    const float *pp = a.partials + ((size_t)(base + g * nsplit) * G + h) * (HD + 2);
     float M = -INFINITY;
-    for (int s = 0; s < nsplit; ++s)
-        M = fmaxf(M, a.partials[((size_t)(base + g * nsplit + s) * G + hl) * (HD + 2)]);
+#pragma unroll 8
+    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pp[(size_t)s * STRIDE]);
     float L = 0.f, acc = 0.f;
+#pragma unroll 8
     for (int s = 0; s < nsplit; ++s) {
-        const float *pp = a.partials + ((size_t)(base + g * nsplit + s) * G + hl) * (HD + 2);
-        const float w = (pp[0] == -INFINITY) ? 0.f : exp2f(pp[0] - M);
-        L += pp[1] * w;
-        acc += pp[2 + d] * w;
+        const float *q = pp + (size_t)s * STRIDE;
+        const float w = (q[0] == -INFINITY) ? 0.f : exp2f(q[0] - M);
+        L += q[1] * w;
+        acc += q[2 + d] * w;
     }
-    ((T *)a.o)[((size_t)tok * a.nq + h) * HD + d] = from_f32<T>(L > 0.f ? acc / L : 0.f);
+    ((T *)a.o)[((size_t)tok * a.nq + g * G + h) * HD + d] = from_f32<T>(L > 0.f ? acc / L : 0.f);
 }
 
 template <bool BF16, int HD, int G>
 hipError_t run(const AttnArgs &a, int n_decode, bool combine, hipStream_t s) {
     if (combine) {
         if (n_decode <= 0) return hipSuccess;
-        if (BF16) hipLaunchKernelGGL((attn_combine_kernel<bf16, HD, G>), dim3(n_decode, a.nq), dim3(HD), 0, s, a);
-        else hipLaunchKernelGGL((attn_combine_kernel<float, HD, G>), dim3(n_decode, a.nq), dim3(HD), 0, s, a);
+        if (BF16) hipLaunchKernelGGL((attn_combine_kernel<bf16, HD, G>), dim3(n_decode, a.nkv), dim3(G * HD), 0, s, a);
+        else hipLaunchKernelGGL((attn_combine_kernel<float, HD, G>), dim3(n_decode, a.nkv), dim3(G * HD), 0, s, a);
         return hipGetLastError();
     }
     if (a.n_items <= 0) return hipSuccess;

@@ -107,15 +107,20 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_combine(int dtype, const AttnArgs &a, int n_decode, hipStream_t s);
 
 struct PoolArgs {
-    const float *x;           // fp32 residual rows of the embedding slice [Te][d]
-    const float *gain;        // final norm gain [d]
+    const float *x;           // fp32 residual rows [T][d]
+    const float *gain;        // embedding model's final norm gain [d]
+    const float *gen_gain;    // generator's final norm gain [d] (decode rows)
+    void *act;                // decode rows' normalised LM-head input [T][d], model dtype
     const int32_t *chunks;
-    float *inv_rms;           // [Te] scratch
+    float *inv_rms;           // [Te] scratch: final-norm scale of the embedding rows
     float *acc_sum, *acc_w, *out_emb;
-    int n_chunks, Te, d;
+    int n_chunks, Te, d, row0;
     float eps;
     int *err;
 };
+// final RMSNorm over rows [row0, row0 + rows): 1/rms of embedding rows, normalised decode rows
+hipError_t launch_final_rows(int dtype, const PoolArgs &a, int rows, hipStream_t s);
+// incremental pooler update and finished embeddings (needs launch_final_rows on the emb rows)
 hipError_t launch_pool(const PoolArgs &a, hipStream_t s);
 
 }  // namespace orthrus

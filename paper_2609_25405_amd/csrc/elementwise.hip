@@ -18,28 +18,45 @@ __device__ __forceinline__ float block_sum(float v, float *red) {
     return s;
 }
 
-// y = x / sqrt(mean(x^2) + eps) * gain; gather mode first sets x = table[tok] (fp32 copy kept)
+// 4 consecutive elements of the model dtype <-> float4
+__device__ __forceinline__ float4 load4(const float *p) { return *(const float4 *)p; }
+__device__ __forceinline__ float4 load4(const bf16 *p) {
+    const uint2 u = *(const uint2 *)p;
+    return float4{bf16_lo(u.x), bf16_hi(u.x), bf16_lo(u.y), bf16_hi(u.y)};
+}
+__device__ __forceinline__ void store4(float *p, float4 v) { *(float4 *)p = v; }
+__device__ __forceinline__ void store4(bf16 *p, float4 v) {
+    *(uint2 *)p = uint2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
+}
+
+// y = x / sqrt(mean(x^2) + eps) * gain over one row per block (d a multiple of 4); gather mode
+// first sets x = table[tok] (the fp32 copy is kept as the residual stream)
 template <typename T, bool GATHER>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
     __shared__ float red[4];
     const int r = blockIdx.x;
+    const int nv = a.d / 4;
+    float *xrow = (GATHER ? a.x_out : const_cast<float *>(a.x)) + (size_t)r * a.d;
     float ss = 0.f;
     if (GATHER) {
         const T *src = (const T *)a.table + (size_t)a.tok[r] * a.d;
-        float *dst = a.x_out + (size_t)r * a.d;
-        for (int i = threadIdx.x; i < a.d; i += 256) {
-            const float v = to_f32(src[i]);
-            dst[i] = v;
-            ss += v * v;
+        for (int v = threadIdx.x; v < nv; v += 256) {
+            const float4 x = load4(src + 4 * v);
+            store4(xrow + 4 * v, x);
+            ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
         }
     } else {
-        const float *x = a.x + (size_t)r * a.d;
-        for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
+        for (int v = threadIdx.x; v < nv; v += 256) {
+            const float4 x = load4(xrow + 4 * v);
+            ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+        }
     }
     const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
-    const float *x = GATHER ? a.x_out + (size_t)r * a.d : a.x + (size_t)r * a.d;
     T *y = (T *)a.y + (size_t)r * a.d;
-    for (int i = threadIdx.x; i < a.d; i += 256) y[i] = from_f32<T>(x[i] * inv * a.gain[i]);
+    for (int v = threadIdx.x; v < nv; v += 256) {
+        const float4 x = load4(xrow + 4 * v), g = load4(a.gain + 4 * v);
+        store4(y + 4 * v, float4{x.x * inv * g.x, x.y * inv * g.y, x.z * inv * g.z, x.w * inv * g.w});
+    }
 }
 
 // q, k rotated at their absolute positions (pairs (i, i + hd/2), angle pos * base^(-2i/hd),
@@ -48,7 +65,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
 // [kv head][dim][slot]).
 template <typename T>
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
-    __shared__ float cs[64], sn[64];
+    __shared__ __attribute__((aligned(16))) float cs[64], sn[64];
     const int t = blockIdx.x;
     const int half = a.hd / 2;
     const int pos = a.pos[t];
@@ -68,41 +85,65 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
     const int qkv_dim = (a.nq + 2 * a.nkv) * a.hd;
     const float *src = a.qkv + (size_t)t * qkv_dim;
     const size_t slot = ok ? (((size_t)page * a.nkv) * a.page + pos % a.page) * a.hd : 0;
-    // rotations: (nq + nkv) heads x half pairs
-    for (int w = threadIdx.x; w < (a.nq + a.nkv) * half; w += 256) {
-        const int head = w / half, i = w % half;
-        const float x1 = src[head * a.hd + i], x2 = src[head * a.hd + i + half];
-        const float y1 = x1 * cs[i] - x2 * sn[i];
-        const float y2 = x2 * cs[i] + x1 * sn[i];
+    // rotations: (nq + nkv) heads x (half / 4) quads of pairs (i..i+3, i+half..i+half+3)
+    const int quads = half / 4;
+    for (int w = threadIdx.x; w < (a.nq + a.nkv) * quads; w += 256) {
+        const int head = w / quads, i = 4 * (w % quads);
+        const float4 x1 = *(const float4 *)(src + head * a.hd + i);
+        const float4 x2 = *(const float4 *)(src + head * a.hd + i + half);
+        const float4 c = *(const float4 *)(cs + i), sn4 = *(const float4 *)(sn + i);
+        const float4 y1 = {x1.x * c.x - x2.x * sn4.x, x1.y * c.y - x2.y * sn4.y, x1.z * c.z - x2.z * sn4.z,
+                           x1.w * c.w - x2.w * sn4.w};
+        const float4 y2 = {x2.x * c.x + x1.x * sn4.x, x2.y * c.y + x1.y * sn4.y, x2.z * c.z + x1.z * sn4.z,
+                           x2.w * c.w + x1.w * sn4.w};
+        T *dst;
         if (head < a.nq) {
-            T *q = (T *)a.q_out + ((size_t)t * a.nq + head) * a.hd;
-            q[i] = from_f32<T>(y1);
-            q[i + half] = from_f32<T>(y2);
-        } else if (ok) {
-            const int g = head - a.nq;
-            T *k = (T *)a.k_cache[p] + slot + (size_t)g * a.page * a.hd;
-            k[i] = from_f32<T>(y1);
-            k[i + half] = from_f32<T>(y2);
+            dst = (T *)a.q_out + ((size_t)t * a.nq + head) * a.hd;
+        } else {
+            if (!ok) continue;
+            dst = (T *)a.k_cache[p] + slot + (size_t)(head - a.nq) * a.page * a.hd;
         }
+        store4(dst + i, y1);
+        store4(dst + i + half, y2);
     }
     if (ok) {
         // values are stored dim-major inside a page: [kv head][dim][slot]
         const float *vs = src + (size_t)(a.nq + a.nkv) * a.hd;
         T *v = (T *)a.v_cache[p] + (size_t)page * a.nkv * a.hd * a.page + pos % a.page;
-        for (int w = threadIdx.x; w < a.nkv * a.hd; w += 256) v[(size_t)w * a.page] = from_f32<T>(vs[w]);
+        for (int w = threadIdx.x; w < a.nkv * a.hd / 4; w += 256) {
+            const float4 x = *(const float4 *)(vs + 4 * w);
+            v[(size_t)(4 * w + 0) * a.page] = from_f32<T>(x.x);
+            v[(size_t)(4 * w + 1) * a.page] = from_f32<T>(x.y);
+            v[(size_t)(4 * w + 2) * a.page] = from_f32<T>(x.z);
+            v[(size_t)(4 * w + 3) * a.page] = from_f32<T>(x.w);
+        }
     }
 }
 
 // ---------------------------------------------------------------------- incremental pooler
-// 1/rms of each embedding-slice row (the final RMSNorm's scale)
-__global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
+// Final RMSNorm: for embedding-slice rows only its scale 1/rms is kept (the pooler applies it);
+// decode rows are normalised into the LM head's input.  One row per block.
+template <typename T>
+__global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
     __shared__ float red[4];
-    const int r = blockIdx.x;
+    const int r = a.row0 + blockIdx.x;
+    const int nv = a.d / 4;
     const float *x = a.x + (size_t)r * a.d;
     float ss = 0.f;
-    for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
+    for (int v = threadIdx.x; v < nv; v += 256) {
+        const float4 q = load4(x + 4 * v);
+        ss += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+    }
     const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
-    if (threadIdx.x == 0) a.inv_rms[r] = inv;
+    if (r < a.Te) {
+        if (threadIdx.x == 0) a.inv_rms[r] = inv;
+        return;
+    }
+    T *y = (T *)a.act + (size_t)r * a.d;
+    for (int v = threadIdx.x; v < nv; v += 256) {
+        const float4 q = load4(x + 4 * v), g = load4(a.gen_gain + 4 * v);
+        store4(y + 4 * v, float4{q.x * inv * g.x, q.y * inv * g.y, q.z * inv * g.z, q.w * inv * g.w});
+    }
 }
 
 __device__ __forceinline__ bool chunk_state_ok(const int32_t *ch, const float *acc_w) {
@@ -196,9 +237,15 @@ hipError_t launch_rope_append(int dtype, const RopeArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+hipError_t launch_final_rows(int dtype, const PoolArgs &a, int rows, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    if (dtype == 1) hipLaunchKernelGGL(final_rows_kernel<bf16>, dim3(rows), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(final_rows_kernel<float>, dim3(rows), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_pool(const PoolArgs &a, hipStream_t s) {
     if (a.n_chunks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(pool_rows_kernel, dim3(a.Te), dim3(256), 0, s, a);
     hipLaunchKernelGGL(pool_accum_kernel, dim3(a.n_chunks, a.d / 64), dim3(256), 0, s, a);
     hipLaunchKernelGGL(pool_finish_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
     return hipGetLastError();

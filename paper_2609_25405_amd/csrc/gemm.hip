@@ -251,7 +251,12 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 // does slightly better with 192x256.  Very short batches (decode-only LM head) use 64x256.
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
-    if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI>(a, s);
+    // short batches stream the weights: narrow tiles give every CU a share of the columns
+    if constexpr (EPI != EPI_SWIGLU) {
+        if (a.M <= 64) return run_bf16<64, 128, 1, 4, EPI>(a, s);
+    } else {
+        if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI>(a, s);
+    }
     if (EPI == EPI_SWIGLU && a.M > 128) return run_bf16<192, 256, 2, 2, EPI>(a, s);
     return run_bf16<128, 128, 2, 2, EPI>(a, s);
 }

@@ -386,27 +386,29 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         }
     }
 
-    // incremental pooler on the embedding slice
-    if (p.n_chunks > 0) {
-        PoolArgs pa{};
-        pa.x = x;
-        pa.gain = emb->w.final_norm;
-        pa.chunks = meta + p.off_chunks;
-        pa.inv_rms = (float *)(ws + L.inv_rms);
-        pa.acc_sum = acc_sum;
-        pa.acc_w = acc_w;
-        pa.out_emb = out_emb;
-        pa.n_chunks = p.n_chunks;
-        pa.Te = Te;
-        pa.d = d;
-        pa.eps = c.rms_eps;
-        pa.err = err;
-        RUN("pool", launch_pool(pa, s));
-    }
-    // LM head on the decode slice
+    // final RMSNorm (scale of the embedding rows; LM-head input of the decode rows), then the
+    // incremental pooler on the embedding slice and the LM head on the decode slice
+    PoolArgs pa{};
+    pa.x = x;
+    pa.gain = emb->w.final_norm;
+    pa.gen_gain = gen->w.final_norm;
+    pa.act = act;
+    pa.chunks = meta + p.off_chunks;
+    pa.inv_rms = (float *)(ws + L.inv_rms);
+    pa.acc_sum = acc_sum;
+    pa.acc_w = acc_w;
+    pa.out_emb = out_emb;
+    pa.n_chunks = p.n_chunks;
+    pa.Te = Te;
+    pa.d = d;
+    pa.row0 = 0;
+    pa.eps = c.rms_eps;
+    pa.err = err;
+    // with no layers the gather already normalised the decode rows with the final gain
+    const int final_rows = c.n_layers > 0 ? T : Te;
+    if (final_rows > 0) RUN("final_norm", launch_final_rows(dt, pa, final_rows, s));
+    if (p.n_chunks > 0) RUN("pool", launch_pool(pa, s));
     if (p.D > 0) {
-        const Group gd{gen, Te, T};
-        if (c.n_layers > 0) RUN("rmsnorm", norm(false, gd, gen->w.final_norm));
         GemmArgs ga{};
         ga.A = act + (size_t)Te * d * es;
         ga.B0 = gen->w.lm_head;
