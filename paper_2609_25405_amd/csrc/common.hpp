@@ -63,11 +63,22 @@ struct GemmArgs {
     const void *B1;  // [N][K] up-projection weights (SwiGLU only)
     void *out;       // fp32 [M][N] (store/add) or activation dtype [M][N] (SwiGLU)
     int M, N, K, lda, ldo;
+    // split-K (bf16 path, EPI_ADD_F32 only): with splits > 1 split s writes its fp32 share of
+    // rows [0, M) to partial + s * split_stride (row stride ldo) instead of adding into out
+    int splits;
+    float *partial;
+    size_t split_stride;
 };
 hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
+// split-K factor (<= max_splits, dividing K into whole stages) for a bf16 residual-add
+// projection of this shape; launch_gemm ignores a requested split that does not divide K
+int gemm_add_splits(int M, int N, int K, int max_splits);
 
 struct NormArgs {
     const float *x;         // fp32 residual rows [rows][d]
+    const float *pend;      // pending split-K slabs added to x first (npend of them, or none)
+    size_t pend_stride;     // floats between slabs
+    int npend;
     float *x_out;           // gather mode: fp32 rows written here
     const void *table;      // gather mode: token table [vocab][d] of the model dtype
     const int32_t *tok;     // gather mode: token per row
@@ -114,6 +125,9 @@ struct PoolArgs {
     const int32_t *chunks;
     float *inv_rms;           // [Te] scratch: final-norm scale of the embedding rows
     float *acc_sum, *acc_w, *out_emb;
+    const float *pend;        // pending split-K slabs added to x first (npend of them, or none)
+    size_t pend_stride;
+    int npend;
     int n_chunks, Te, d, row0;
     float eps;
     int *err;

@@ -47,7 +47,15 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
         }
     } else {
         for (int v = threadIdx.x; v < nv; v += 256) {
-            const float4 x = load4(xrow + 4 * v);
+            float4 x = load4(xrow + 4 * v);
+            if (a.npend > 0) {
+                // finish a split-K residual add: x += slab 0 + slab 1 + ... in order
+                for (int sp = 0; sp < a.npend; ++sp) {
+                    const float4 p = load4(a.pend + sp * a.pend_stride + (size_t)r * a.d + 4 * v);
+                    x = float4{x.x + p.x, x.y + p.y, x.z + p.z, x.w + p.w};
+                }
+                store4(xrow + 4 * v, x);
+            }
             ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
         }
     }
@@ -128,10 +136,18 @@ __global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
     __shared__ float red[4];
     const int r = a.row0 + blockIdx.x;
     const int nv = a.d / 4;
-    const float *x = a.x + (size_t)r * a.d;
+    float *x = const_cast<float *>(a.x) + (size_t)r * a.d;
     float ss = 0.f;
     for (int v = threadIdx.x; v < nv; v += 256) {
-        const float4 q = load4(x + 4 * v);
+        float4 q = load4(x + 4 * v);
+        if (a.npend > 0) {
+            // finish the last layer's split-K residual add (slabs in order)
+            for (int sp = 0; sp < a.npend; ++sp) {
+                const float4 p = load4(a.pend + sp * a.pend_stride + (size_t)r * a.d + 4 * v);
+                q = float4{q.x + p.x, q.y + p.y, q.z + p.z, q.w + p.w};
+            }
+            store4(x + 4 * v, q);
+        }
         ss += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
     }
     const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);

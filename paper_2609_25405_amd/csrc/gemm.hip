@@ -44,9 +44,12 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
     const int mt = (a.M + BM - 1) / BM;
-    const int total = gridDim.x;
-    const int b = blockIdx.x;
-    const int t = (total % 8 == 0) ? (b % 8) * (total / 8) + b / 8 : b;
+    constexpr int COLS_ = EPI == EPI_SWIGLU ? BN / 2 : BN;
+    const int tiles = mt * ((a.N + COLS_ - 1) / COLS_);
+    const int splits = gridDim.x / tiles;          // split-K factor (1 = whole K per tile)
+    const int split = blockIdx.x / tiles;
+    const int b = blockIdx.x % tiles;
+    const int t = (tiles % 8 == 0) ? (b % 8) * (tiles / 8) + b / 8 : b;
     const int n_tile = t / mt, m_tile = t % mt;
     const int m0 = m_tile * BM;
     constexpr int COLS = EPI == EPI_SWIGLU ? BN / 2 : BN;  // output columns per tile
@@ -118,13 +121,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     // other buffer), start the next stage's copies, then the MFMAs with the next k-step's
     // fragments read from LDS under the current k-step's MFMAs (order given to the scheduler).
     constexpr int NMF = FM * FN, NFR = FM + FN, NLD = A_INST + B_INST;
-    const int nk = a.K / BK;
-    issue(0, 0);
+    const int nk = a.K / BK / splits;
+    const int kt0 = split * nk;
+    issue(kt0, 0);
     for (int kt = 0; kt < nk; ++kt) {
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         const bool more = kt + 1 < nk;
-        if (more) issue(kt + 1, (kt + 1) & 1);
+        if (more) issue(kt0 + kt + 1, (kt + 1) & 1);
         const char *s = smem + (kt & 1) * STAGE;
         lds_frag(s, 0, 0);
 #pragma unroll
@@ -163,6 +167,15 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
                 for (int ni = 0; ni < FN / 2; ++ni) {
                     const int col = n0 + wn * (TN / 2) + ni * 32 + (lane & 31);
                     if (col < a.N) o[col] = from_f32<bf16>(silu(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+                }
+            } else if (splits > 1) {
+                // split-K: this split's share goes to its own fp32 slab; the row's consumer adds
+                // the slabs to the residual stream in split order
+                float *o = a.partial + (size_t)split * a.split_stride + (size_t)row * a.ldo;
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni) {
+                    const int col = n0 + wn * TN + ni * 32 + (lane & 31);
+                    if (col < a.N) o[col] = acc[mi][ni][r];
                 }
             } else {
                 float *o = (float *)a.out + (size_t)row * a.ldo;
@@ -241,17 +254,18 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
     const int mt = (a.M + BM - 1) / BM;
     const int cols = EPI == EPI_SWIGLU ? BN / 2 : BN;
     const int nt = (a.N + cols - 1) / cols;
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(mt * nt), dim3(64 * WM * WN), 0, s, a);
+    const int splits =
+        (EPI == EPI_ADD_F32 && a.partial && a.splits > 1 && a.K % (a.splits * BK) == 0) ? a.splits : 1;
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(mt * nt * splits), dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
 }
 
 // Tile choice per shape, from measurements of the step's projections on MI355X: 128x128
 // tiles (64 KiB of LDS, two workgroups per CU, so one hides the other's barrier and copy
 // waits) beat larger tiles on every projection of a 384..2048-token batch; the gate/up pair
-// does slightly better with 192x256.  Very short batches (decode-only LM head) use 64x256.
+// does slightly better with 192x256.  Very short batches (decode-only LM head) use narrow tiles.
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
-    // short batches stream the weights: narrow tiles give every CU a share of the columns
     if constexpr (EPI != EPI_SWIGLU) {
         if (a.M <= 64) return run_bf16<64, 128, 1, 4, EPI>(a, s);
     } else {
@@ -262,6 +276,22 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
 }
 
 }  // namespace
+
+// Split-K factor for a residual-add projection on the bf16 path: enough work units for two per
+// CU (a few hundred tiles over 256 CUs otherwise leaves most CUs idle in the last round), each
+// split a whole number of 64-deep stages and at least 512 deep.  1 = no split.
+int gemm_add_splits(int M, int N, int K, int max_splits) {
+    const int BM = M <= 64 ? 64 : 128, BN = 128;
+    const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    if (tiles >= 384) return 1;
+    int best = 1;
+    for (int s = 2; s <= max_splits; ++s) {
+        if (K % (s * BK) || K / s < 512) continue;
+        best = s;
+        if (tiles * s >= 512) break;
+    }
+    return best;
+}
 
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, hipStream_t s) {
     if (a.M <= 0) return hipSuccess;

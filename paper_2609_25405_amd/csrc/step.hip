@@ -36,8 +36,10 @@ constexpr size_t kAlign = 256;
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, total;
+    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, split_slabs, total;
 };
+// split-K slabs of one residual-add projection: at most kMaxSplits fp32 [T][d] slabs
+constexpr int kMaxSplits = 4;
 
 Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials) {
     const size_t es = m.cfg.dtype == ORTHRUS_BF16 ? 2 : 4;
@@ -54,6 +56,7 @@ Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials
     L.u = o; o += up(T * (size_t)m.cfg.d_ff * es);
     L.inv_rms = o; o += up(T * 4);
     L.partials = o; o += up(n_partials * (size_t)m.group() * (m.cfg.head_dim + 2) * 4);
+    L.split_slabs = o; o += m.cfg.dtype == ORTHRUS_BF16 ? up((size_t)kMaxSplits * T * d * 4) : 0;
     L.total = o;
     return L;
 }
@@ -275,8 +278,15 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         if (T > Te) groups[n_groups++] = {gen, Te, T};
     }
 
+    // split-K slabs of the last residual-add projection, not yet added to x
+    float *slabs = dt == ORTHRUS_BF16 ? (float *)(ws + L.split_slabs) : nullptr;
+    const size_t slab_stride = (size_t)T * d;
+    int pending = 0;
     auto norm = [&](bool gather, const Group &g, const float *gain) -> hipError_t {
         NormArgs n{};
+        n.pend = slabs ? slabs + (size_t)g.r0 * d : nullptr;
+        n.pend_stride = slab_stride;
+        n.npend = gather ? 0 : pending;
         n.x = x + (size_t)g.r0 * d;
         n.x_out = x + (size_t)g.r0 * d;
         n.table = g.m->w.tok_emb;
@@ -300,7 +310,26 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.K = K;
         ga.lda = lda;
         ga.ldo = ldo;
+        ga.splits = 1;
         return launch_gemm(dt, epi, ga, s);
+    };
+    // residual-add projection into x; one model and bf16: split K when the tile count is low and
+    // leave the slabs for the next row-wise kernel (returns the split count)
+    auto add_proj = [&](const Group &g, const char *A, int lda, const void *B, int K, int &splits) -> hipError_t {
+        GemmArgs ga{};
+        ga.A = A + (size_t)g.r0 * lda * es;
+        ga.B0 = B;
+        ga.out = x + (size_t)g.r0 * d;
+        ga.M = g.r1 - g.r0;
+        ga.N = d;
+        ga.K = K;
+        ga.lda = lda;
+        ga.ldo = d;
+        splits = (slabs && n_groups == 1) ? gemm_add_splits(ga.M, d, K, kMaxSplits) : 1;
+        ga.splits = splits;
+        ga.partial = slabs;
+        ga.split_stride = slab_stride;
+        return launch_gemm(dt, EPI_ADD_F32, ga, s);
     };
 
     // token gather fused with the first RMSNorm (the final norm when there are no layers)
@@ -354,8 +383,10 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     const int qd = M.q_dim(), qkvd = M.qkv_dim(), F = c.d_ff;
 
     for (int l = 0; l < c.n_layers; ++l) {
-        if (l > 0)
+        if (l > 0) {
             for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].attn_norm));
+            pending = 0;
+        }
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d));
@@ -371,19 +402,23 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         }
         RUN("attention", launch_attention(dt, aa, s));
         if (p.n_split_rows > 0) RUN("attn_combine", launch_attn_combine(dt, aa, p.D, s));
+        int splits = 1;
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-            RUN("gemm_o", gemm(EPI_ADD_F32, groups[gi], ob, qd, lw.w_o, nullptr, x, d, 4, d, qd));
+            RUN("gemm_o", add_proj(groups[gi], ob, qd, lw.w_o, qd, splits));
         }
+        pending = splits > 1 ? splits : 0;
         for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].mlp_norm));
+        pending = 0;
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             RUN("gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d));
         }
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-            RUN("gemm_down", gemm(EPI_ADD_F32, groups[gi], ub, F, lw.w_down, nullptr, x, d, 4, d, F));
+            RUN("gemm_down", add_proj(groups[gi], ub, F, lw.w_down, F, splits));
         }
+        pending = splits > 1 ? splits : 0;  // added by the next layer's norm or the final norm
     }
 
     // final RMSNorm (scale of the embedding rows; LM-head input of the decode rows), then the
@@ -399,6 +434,9 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     pa.acc_w = acc_w;
     pa.out_emb = out_emb;
     pa.n_chunks = p.n_chunks;
+    pa.pend = slabs;
+    pa.pend_stride = slab_stride;
+    pa.npend = pending;
     pa.Te = Te;
     pa.d = d;
     pa.row0 = 0;
@@ -418,6 +456,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.K = d;
         ga.lda = d;
         ga.ldo = gen->cfg.vocab;
+        ga.splits = 1;
         RUN("lm_head", launch_gemm(dt, EPI_STORE_F32, ga, s));
     }
     return ORTHRUS_OK;
