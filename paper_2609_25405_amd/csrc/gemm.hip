@@ -29,17 +29,38 @@ __device__ __forceinline__ void copy16_to_lds(const void *src, char *lds) {
     __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds, 16, 0, 0);
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+// s_waitcnt immediate that waits until at most n vector-memory operations are outstanding
+// (gfx9 encoding: vmcnt[3:0] in bits 3:0 and vmcnt[5:4] in bits 15:14; expcnt and lgkmcnt at
+// their maxima so they impose no wait)
+template <int N>
+constexpr int vmcnt_imm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    return (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+
+// workgroup barrier for the LDS ring: the LDS reads issued before it have completed and no
+// memory access moves across it; unlike __syncthreads it does not drain the outstanding
+// global->LDS copies of later stages (their completion is awaited explicitly with vmcnt)
+__device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int BM, int BN, int WM, int WN, int EPI, int BKS, int STAGES>
 __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) {
     constexpr int NW = WM * WN;               // waves per workgroup
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / 32, FN = TN / 32;
-    // global -> LDS copies of one K stage: every wave instruction moves 1 KiB = 8 rows of 128 B
-    constexpr int A_INST = BM / (8 * NW), B_INST = BN / (8 * NW);
-    constexpr int STAGE = (BM + BN) * BK * 2;
-    static_assert(A_INST * 8 * NW == BM && B_INST * 8 * NW == BN, "copy split");
+    constexpr int ROWB = BKS * 2;             // bytes of one LDS row (BKS bf16 of K)
+    constexpr int CHUNKS = ROWB / 16;         // 16-byte chunks per row
+    constexpr int RPI = 1024 / ROWB;          // rows moved by one wave copy instruction (1 KiB)
+    constexpr int RP256 = 256 / ROWB;         // rows per 256 bytes (one pass of the 64 LDS banks)
+    // global -> LDS copies of one K stage
+    constexpr int A_INST = BM / (RPI * NW), B_INST = BN / (RPI * NW);
+    constexpr int INST = A_INST + B_INST;     // copy instructions per wave per stage
+    constexpr int STAGE = (BM + BN) * ROWB;
+    constexpr int KSTEPS = BKS / 16;
+    static_assert(A_INST * RPI * NW == BM && B_INST * RPI * NW == BN, "copy split");
     static_assert(FM >= 1 && FN >= 1 && (EPI != EPI_SWIGLU || FN % 2 == 0), "tile shape");
-    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+    static_assert(STAGES >= 2 && (STAGES - 2) * INST < 64, "pipeline depth");
+    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
@@ -55,22 +76,25 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     constexpr int COLS = EPI == EPI_SWIGLU ? BN / 2 : BN;  // output columns per tile
     const int n0 = n_tile * COLS;
 
-    // Lane `lane` of copy instruction i of this wave writes LDS bytes base + 16 * lane, i.e. row
-    // r0 + lane / 8 (r0 = 8 * (NW i + wave)) at physical chunk lane % 8.  The row's logical k chunk
-    // there is (lane % 8) ^ swizzle(row), so that is the 16 bytes the lane fetches.
+    // LDS row r holds 16-byte chunk c at physical position c ^ key(r), key(r) = (r / RP256) %
+    // CHUNKS, so the 16 lanes of one pass of a fragment read (16 consecutive rows, same chunk)
+    // hit 16 distinct 16-byte bank groups.  Lane `lane` of copy instruction i of this wave
+    // writes LDS bytes base + 16 * lane, i.e. row r0 + lane / CHUNKS at physical chunk
+    // lane % CHUNKS (r0 = RPI * (NW i + wave)); it fetches the logical chunk stored there.
+    auto key_of = [](int row) { return (row / RP256) % CHUNKS; };
     const size_t lda_b = (size_t)a.lda * 2, ldb_b = (size_t)a.K * 2;
     const char *a_src[A_INST];
     const char *b_src[B_INST];
 #pragma unroll
     for (int i = 0; i < A_INST; ++i) {
-        const int row = 8 * (NW * i + wave) + (lane >> 3);
-        const int chunk = (lane & 7) ^ ((row >> 1) & 7);
+        const int row = RPI * (NW * i + wave) + lane / CHUNKS;
+        const int chunk = (lane % CHUNKS) ^ key_of(row);
         a_src[i] = (const char *)a.A + (size_t)min(m0 + row, a.M - 1) * lda_b + chunk * 16;
     }
 #pragma unroll
     for (int i = 0; i < B_INST; ++i) {
-        const int r = 8 * (NW * i + wave) + (lane >> 3);
-        const int chunk = (lane & 7) ^ (((BM + r) >> 1) & 7);
+        const int r = RPI * (NW * i + wave) + lane / CHUNKS;
+        const int chunk = (lane % CHUNKS) ^ key_of(BM + r);
         int grow;
         const char *src = (const char *)a.B0;
         if (EPI == EPI_SWIGLU) {
@@ -83,15 +107,12 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
         }
         b_src[i] = src + (size_t)min(grow, a.N - 1) * ldb_b + chunk * 16;
     }
-    auto issue = [&](int kt, int buf) {
-        const size_t kb = (size_t)kt * (BK * 2);
+    // copy j (< INST) of K stage kt into LDS buffer buf: A rows first, then B rows
+    auto copy = [&](int j, int kt, int buf) {
+        const size_t kb = (size_t)kt * ROWB;
         char *s = smem + buf * STAGE;
-#pragma unroll
-        for (int i = 0; i < A_INST; ++i)
-            copy16_to_lds(a_src[i] + kb, s + (NW * i + wave) * 1024);
-#pragma unroll
-        for (int i = 0; i < B_INST; ++i)
-            copy16_to_lds(b_src[i] + kb, s + BM * 128 + (NW * i + wave) * 1024);
+        if (j < A_INST) copy16_to_lds(a_src[j] + kb, s + (NW * j + wave) * 1024);
+        else copy16_to_lds(b_src[j - A_INST] + kb, s + BM * ROWB + (NW * (j - A_INST) + wave) * 1024);
     };
 
     f32x16 acc[FM][FN];
@@ -102,38 +123,49 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // fragment rows of this lane; the swizzle key (row >> 1) & 7 is the same for every
-    // 32-row fragment of the lane, so the LDS offsets differ only by constants
+    // fragment rows of this lane; the swizzle key is the same for every 32-row fragment of the
+    // lane (32 rows span a whole number of 256-byte passes), so offsets differ by constants
     const int arow = wm * TM + (lane & 31), brow = BM + wn * TN + (lane & 31);
-    const int akey = (arow >> 1) & 7, bkey = (brow >> 1) & 7;
+    const int akey = key_of(arow), bkey = key_of(brow);
     bf16x8 fa[2][FM], fb[2][FN];
     auto lds_frag = [&](const char *s, int kk, int buf) {
         const int chk = kk * 2 + (lane >> 5);
 #pragma unroll
         for (int mi = 0; mi < FM; ++mi)
-            fa[buf][mi] = *(const bf16x8 *)(s + (arow + mi * 32) * 128 + ((chk ^ akey) << 4));
+            fa[buf][mi] = *(const bf16x8 *)(s + (arow + mi * 32) * ROWB + ((chk ^ akey) << 4));
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni)
-            fb[buf][ni] = *(const bf16x8 *)(s + (brow + ni * 32) * 128 + ((chk ^ bkey) << 4));
+            fb[buf][ni] = *(const bf16x8 *)(s + (brow + ni * 32) * ROWB + ((chk ^ bkey) << 4));
     };
 
-    // One K stage per iteration: wait for this stage's copies, barrier (which also frees the
-    // other buffer), start the next stage's copies, then the MFMAs with the next k-step's
-    // fragments read from LDS under the current k-step's MFMAs (order given to the scheduler).
-    constexpr int NMF = FM * FN, NFR = FM + FN, NLD = A_INST + B_INST;
-    const int nk = a.K / BK / splits;
+    // STAGES-deep ring of LDS stages: the copies of stage kt + STAGES - 1 are issued while stage
+    // kt is computed.  Iteration kt: wait for this wave's copies of stage kt (later stages stay
+    // in flight), barrier (everyone's copies landed; everyone finished reading the buffer about
+    // to be refilled), issue the next stage's copies, then the MFMAs of stage kt with the next
+    // k-step's fragments read under the current k-step's.  (Spreading the copies between the
+    // MFMAs, or adding L2 prefetches a few stages ahead, measured slower on MI355X.)
+    constexpr int NMF = FM * FN, NFR = FM + FN;
+    const int nk = a.K / BKS / splits;
     const int kt0 = split * nk;
-    issue(kt0, 0);
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+        if (p < nk) {
+#pragma unroll
+            for (int j = 0; j < INST; ++j) copy(j, kt0 + p, p);
+        }
     for (int kt = 0; kt < nk; ++kt) {
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        const bool more = kt + 1 < nk;
-        if (more) issue(kt0 + kt + 1, (kt + 1) & 1);
-        const char *s = smem + (kt & 1) * STAGE;
+        if (kt + STAGES - 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm<(STAGES - 2) * INST>());
+        else __builtin_amdgcn_s_waitcnt(0);
+        ring_barrier();
+        if (kt + STAGES - 1 < nk) {
+#pragma unroll
+            for (int j = 0; j < INST; ++j) copy(j, kt0 + kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+        }
+        const char *s = smem + (kt % STAGES) * STAGE;
         lds_frag(s, 0, 0);
 #pragma unroll
-        for (int kk = 0; kk < BK / 16; ++kk) {
-            if (kk + 1 < BK / 16) lds_frag(s, kk + 1, (kk + 1) & 1);
+        for (int kk = 0; kk < KSTEPS; ++kk) {
+            if (kk + 1 < KSTEPS) lds_frag(s, kk + 1, (kk + 1) & 1);
 #pragma unroll
             for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
@@ -144,15 +176,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
         // schedule: DS_READ=0x100, MFMA=0x008
         __builtin_amdgcn_sched_group_barrier(0x100, NFR, 0);
 #pragma unroll
-        for (int kk = 0; kk < BK / 16; ++kk) {
+        for (int kk = 0; kk < KSTEPS; ++kk) {
 #pragma unroll
             for (int i = 0; i < NMF; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                if (kk + 1 < BK / 16 && i < NFR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                if (kk + 1 < KSTEPS && i < NFR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
         }
     }
-    (void)NLD;
 
     // epilogue: lane holds column (lane & 31) of each 32x32 tile, rows 8*(r/4) + 4*(lane/32) + r%4
 #pragma unroll
@@ -249,46 +280,57 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int EPI, int BKS = 64, int STAGES = 2>
 hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
     const int mt = (a.M + BM - 1) / BM;
     const int cols = EPI == EPI_SWIGLU ? BN / 2 : BN;
     const int nt = (a.N + cols - 1) / cols;
     const int splits =
         (EPI == EPI_ADD_F32 && a.partial && a.splits > 1 && a.K % (a.splits * BK) == 0) ? a.splits : 1;
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(mt * nt * splits), dim3(64 * WM * WN), 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, BKS, STAGES>), dim3(mt * nt * splits),
+                       dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
 }
 
-// Tile choice per shape, from measurements of the step's projections on MI355X: 128x128
-// tiles (64 KiB of LDS, two workgroups per CU, so one hides the other's barrier and copy
-// waits) beat larger tiles on every projection of a 384..2048-token batch; the gate/up pair
-// does slightly better with 192x256.  Very short batches (decode-only LM head) use narrow tiles.
+// Tile choice per shape, from measurements of the step's projections on MI355X (M = 1088
+// tokens of a 7B-class layer).  Copy latency, not LDS or MFMA issue, bounds these GEMMs, so
+// the choice trades tile reuse against filling the CUs:
+//  - M <= 64 (decode-only batches, the LM head): weight streaming; a 3-deep copy ring keeps
+//    enough bytes in flight per CU (70 -> 43 us for a 64 x 32000 x 4096 LM head);
+//  - gate/up: 192x256 tiles over 8 waves;
+//  - residual-add projections with split-K slabs: 192x256 over 8 waves, split 2 (o 58 -> 46 us,
+//    down 177 -> 135 us against 128x128 tiles);
+//  - otherwise 128x128 (64 KiB of LDS, two workgroups per CU hide each other's waits).
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
-    if constexpr (EPI != EPI_SWIGLU) {
-        if (a.M <= 64) return run_bf16<64, 128, 1, 4, EPI>(a, s);
+    if constexpr (EPI == EPI_SWIGLU) {
+        if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI, 64, 3>(a, s);
+        if (a.M > 128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else {
-        if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI>(a, s);
+        if (a.M <= 64) return run_bf16<64, 128, 1, 4, EPI, 64, 3>(a, s);
+        if (EPI == EPI_ADD_F32 && a.partial && a.splits > 1) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        if (EPI == EPI_ADD_F32) return run_bf16<128, 128, 4, 2, EPI>(a, s);
+        return run_bf16<128, 128, 2, 2, EPI>(a, s);
     }
-    if (EPI == EPI_SWIGLU && a.M > 128) return run_bf16<192, 256, 2, 2, EPI>(a, s);
-    return run_bf16<128, 128, 2, 2, EPI>(a, s);
 }
 
 }  // namespace
 
-// Split-K factor for a residual-add projection on the bf16 path: enough work units for two per
-// CU (a few hundred tiles over 256 CUs otherwise leaves most CUs idle in the last round), each
-// split a whole number of 64-deep stages and at least 512 deep.  1 = no split.
+// Split-K factor for a residual-add projection on the bf16 path, for the tiles dispatch_bf16
+// uses with it (64x128 for M <= 64, else 192x256, one workgroup per CU): the factor whose
+// workgroups fill the last round over 256 CUs best, the smaller one on a tie, each split a whole
+// number of 64-deep stages and at least 512 deep.  1 = no split.
 int gemm_add_splits(int M, int N, int K, int max_splits) {
-    const int BM = M <= 64 ? 64 : 128, BN = 128;
-    const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    if (tiles >= 384) return 1;
+    const int bm = M <= 64 ? 64 : 192, bn = M <= 64 ? 128 : 256;
+    const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    auto fill = [](long w) { const long rounds = (w + 255) / 256; return (double)w / (double)(rounds * 256); };
     int best = 1;
+    double best_fill = M <= 64 ? fill(tiles) : 0.0;   // M > 64 without a split uses other tiles
     for (int s = 2; s <= max_splits; ++s) {
         if (K % (s * BK) || K / s < 512) continue;
-        best = s;
-        if (tiles * s >= 512) break;
+        const double f = fill(tiles * s);
+        if (f > best_fill + 1e-9) { best = s; best_fill = f; }
     }
     return best;
 }
