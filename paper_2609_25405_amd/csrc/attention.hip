@@ -13,12 +13,12 @@
 //     the cache (L2-resident, shared by the group's waves) one block ahead of the MFMAs, an
 //     online softmax in fp32 (exp2 domain) and causal masking on the diagonal blocks.  Waves
 //     never synchronise, so each stops at its own causal bound.
-//   * decode items: one (decode row, KV head, <= 256-key split).  Each wave owns up to four of
-//     the split's pages and issues all their K and V loads at once (128 KiB in flight per item),
-//     scores with v_dot2_f32_bf16 for all `group` query heads at once, takes the softmax over the
-//     split through LDS, then accumulates P V from registers.  Rows with several splits write
-//     (max, sum, unnormalised output) partials merged by attn_combine in split order, so results
-//     do not depend on scheduling.
+//   * decode items: one (decode row, KV head, key-range split), walked in 128-key chunks.  Each
+//     wave owns two pages of a chunk, scores with v_dot2_f32_bf16 for all `group` query heads
+//     at once, keeps an online softmax, and accumulates P V from registers; the next chunk's K
+//     and V loads (64 KiB per item) are in flight while a chunk is computed.  Rows with
+//     several splits write (max, sum, unnormalised output) partials merged by attn_combine in
+//     split order, so results do not depend on scheduling.
 // Page ids read from the block table are range-checked; a bad id sets the sticky device error
 // word and its keys are skipped (never dereferenced).
 #include "common.hpp"
@@ -31,6 +31,7 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kPage = 16;
 constexpr int kPrefillPageWindow = 512;  // page ids staged in LDS at a time (even)
+constexpr int kDecodeChunkPages = 8;     // pages per step of a bf16 decode item (4 waves x 2)
 
 struct PoolView {
     const char *k, *v;
@@ -54,24 +55,33 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
 }
 
 // ------------------------------------------------------------------ decode split, bf16 path
-// Loads are issued branch-free and before any use: every page id of the wave first, then every
-// K and V line of those pages; invalid or absent pages read page 0 and are masked afterwards.
+// A split is walked in chunks of kDecodeChunkPages pages (128 keys); each wave owns two pages of
+// a chunk.  Loads are branch-free (invalid or absent pages read page 0 and are masked) and
+// software-pipelined across chunks: the next chunk's K lines go out as soon as this chunk's
+// scores are taken, its V lines as soon as this chunk's P V is done, and page ids two chunks
+// ahead, so the memory pipe stays busy while the wave computes.  Each wave keeps an online
+// softmax (max, sum, output) over its keys of all chunks; the four waves merge once at the end.
 template <int HD, int G>
 __device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *smem) {
     constexpr int KL = HD / 32;     // 16-byte loads per lane per page, for K and for V
     constexpr int QD = HD / 4;      // head dims per lane in the score pass (4 lanes per key)
     constexpr int VD = HD / 64;     // head dims per lane in the value pass
-    constexpr int PPW = kSplitPages / 4;
-    constexpr int KPW = PPW * kPage;                       // keys per wave
+    constexpr int CP = kDecodeChunkPages;
+    constexpr int PPW = CP / 4;                            // pages per wave per chunk
+    constexpr int KPW = PPW * kPage;                       // keys per wave per chunk
+    constexpr int CHUNK = CP * kPage;                      // keys per chunk
     uint32_t *pk_all = (uint32_t *)smem;                   // [4 waves][KPW / 2][G] bf16 weight pairs
     float *mw = (float *)(pk_all + 4 * (KPW / 2) * G);     // [4][G] wave maxima
     float *lw = mw + 4 * G;                                // [4][G] wave sums
     float *part = lw + 4 * G;                              // [4][G][HD] wave outputs
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    uint32_t *qs = (uint32_t *)(part + 4 * G * HD) + wave * (G * HD / 2);  // wave's copy of q
     const int j = it[IT_INDEX], g = it[IT_KVHEAD];
     const int k0 = it[IT_KEY_BEGIN], k1 = it[IT_KEY_END], pslot = it[IT_PARTIAL];
     const int nk = k1 - k0;
     const int n_pg = (nk + kPage - 1) / kPage;
+    const int n_ch = (n_pg + CP - 1) / CP;
     const int32_t *row = a.rows + kRowInts * j;
     const int seq = row[0], tok = row[2];
     const PoolView pv = pool_view(a, 1);
@@ -79,118 +89,171 @@ __device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *sme
     const size_t page_bytes = (size_t)a.nkv * kPage * HD * 2;
     const int kin = lane >> 2, qtr = lane & 3;
 
-    int page[PPW];
-    bool pok[PPW];
+    // page ids of chunk c for this wave (pages c * CP + wave + 4 i), raw
+    auto load_pages = [&](int c, int (&pg)[PPW]) {
 #pragma unroll
-    for (int i = 0; i < PPW; ++i) page[i] = bt[min(wave + 4 * i, n_pg - 1)];
-#pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        const bool present = wave + 4 * i < n_pg;
-        pok[i] = present && page[i] >= 0 && page[i] < pv.n_pages;
-        if (present && !pok[i] && lane == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
-        page[i] = pok[i] ? page[i] : 0;
-    }
-    // query heads g*G .. g*G+G-1, this lane's quarter of the head dims, as bf16 pairs; loaded
-    // first so the score pass waits only for them and its own page's keys (loads retire in order)
-    uint32_t qp[G][QD / 2];
-    const char *qrow = (const char *)a.q + ((size_t)tok * a.nq + g * G) * HD * 2 + qtr * QD * 2;
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int c = 0; c < QD / 8; ++c) {
-            const u32x4 v = *(const u32x4 *)(qrow + h * HD * 2 + 16 * c);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) qp[h][4 * c + e] = v[e];
-        }
-    u32x4 kr[PPW][KL], vr[PPW][KL];
-#pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        const char *kp = pv.k + page[i] * page_bytes + (size_t)((g * kPage + kin) * HD + qtr * QD) * 2;
-#pragma unroll
-        for (int c = 0; c < KL; ++c) kr[i][c] = *(const u32x4 *)(kp + 16 * c);
-    }
-#pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        const char *vp = pv.v + page[i] * page_bytes + (size_t)((g * HD + lane * VD) * kPage) * 2;
-#pragma unroll
-        for (int c = 0; c < KL; ++c) vr[i][c] = *(const u32x4 *)(vp + 16 * c);
-    }
-
-    // ---- scores of this wave's keys (4 lanes per key), softmax statistics inside the wave
-    const float scale = kLog2e / sqrtf((float)HD);
-    float s[PPW][G];
-    float mloc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) mloc[h] = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        const bool vis = pok[i] && (wave + 4 * i) * kPage + kin < nk;
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-            float acc = 0.f;
-#pragma unroll
-            for (int c = 0; c < KL; ++c)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) acc = dot2(qp[h][4 * c + e], kr[i][c][e], acc);
-            acc += __shfl_xor(acc, 1, 64);
-            acc += __shfl_xor(acc, 2, 64);
-            s[i][h] = vis ? acc * scale : -INFINITY;
-            mloc[h] = fmaxf(mloc[h], s[i][h]);
-        }
-    }
-    float l[G];
-    uint16_t *pk16 = (uint16_t *)(pk_all + wave * (KPW / 2) * G);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        float mh = mloc[h];
-#pragma unroll
-        for (int o = 4; o <= 32; o <<= 1) mh = fmaxf(mh, __shfl_xor(mh, o, 64));
-        mloc[h] = mh;
-        float ls = 0.f;
+        for (int i = 0; i < PPW; ++i) pg[i] = bt[min(c * CP + wave + 4 * i, n_pg - 1)];
+    };
+    // range check: absent pages (past the split) and bad ids read page 0 and are masked later
+    auto check_pages = [&](int c, int (&pg)[PPW], bool (&ok)[PPW]) {
 #pragma unroll
         for (int i = 0; i < PPW; ++i) {
-            const float p = mh == -INFINITY ? 0.f : exp2f(s[i][h] - mh);
-            ls += p;
-            // key i*16 + kin of this wave; adjacent keys share one 32-bit word
-            const int key = i * kPage + kin;
-            if (qtr == 0) pk16[((key >> 1) * G + h) * 2 + (key & 1)] = (uint16_t)f2bf_bits(p);
+            const bool present = c * CP + wave + 4 * i < n_pg;
+            ok[i] = present && pg[i] >= 0 && pg[i] < pv.n_pages;
+            if (present && !ok[i] && lane == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+            pg[i] = ok[i] ? pg[i] : 0;
         }
+    };
+    u32x4 kr[PPW][KL], vr[PPW][KL];
+    auto issue_k = [&](const int (&pg)[PPW]) {
 #pragma unroll
-        for (int o = 4; o <= 32; o <<= 1) ls += __shfl_xor(ls, o, 64);
-        l[h] = ls;
+        for (int i = 0; i < PPW; ++i) {
+            const char *kp = pv.k + pg[i] * page_bytes + (size_t)((g * kPage + kin) * HD + qtr * QD) * 2;
+#pragma unroll
+            for (int c = 0; c < KL; ++c) kr[i][c] = *(const u32x4 *)(kp + 16 * c);
+        }
+    };
+    auto issue_v = [&](const int (&pg)[PPW]) {
+#pragma unroll
+        for (int i = 0; i < PPW; ++i) {
+            const char *vp = pv.v + pg[i] * page_bytes + (size_t)((g * HD + lane * VD) * kPage) * 2;
+#pragma unroll
+            for (int c = 0; c < KL; ++c) vr[i][c] = *(const u32x4 *)(vp + 16 * c);
+        }
+    };
+
+    int pg_cur[PPW], pg_nxt[PPW];
+    bool ok_cur[PPW], ok_nxt[PPW];
+    load_pages(0, pg_cur);
+    // query heads g*G .. g*G+G-1 (G*HD bf16, contiguous) into the wave's LDS copy, 16 bytes a lane;
+    // the score pass reads one head's quarter at a time from there
+    {
+        const char *qrow = (const char *)a.q + ((size_t)tok * a.nq + g * G) * HD * 2;
+#pragma unroll
+        for (int c = 0; c < (G * HD * 2 + 1023) / 1024; ++c) {
+            const int byte = (c * 64 + lane) * 16;
+            if (byte < G * HD * 2) *(u32x4 *)((char *)qs + byte) = *(const u32x4 *)(qrow + byte);
+        }
     }
+    check_pages(0, pg_cur, ok_cur);
+    issue_k(pg_cur);
+    load_pages(1, pg_nxt);
+    issue_v(pg_cur);
+
+    const float scale = kLog2e / sqrtf((float)HD);
+    float m[G], l[G], acc[G][VD];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        m[h] = -INFINITY;
+        l[h] = 0.f;
+#pragma unroll
+        for (int d = 0; d < VD; ++d) acc[h][d] = 0.f;
+    }
+    uint16_t *pk16 = (uint16_t *)(pk_all + wave * (KPW / 2) * G);
+    const uint32_t *pkw = pk_all + wave * (KPW / 2) * G;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int c = 0; c < n_ch; ++c) {
+        const int cbase = c * CHUNK;   // first key of the chunk inside the split
+        // ---- scores of this wave's keys of the chunk (4 lanes per key)
+        float s[PPW][G];
+        float mloc[G];
+#pragma unroll
+        for (int h = 0; h < G; ++h) mloc[h] = -INFINITY;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            u32x4 qh[QD / 8];
+#pragma unroll
+            for (int cc = 0; cc < QD / 8; ++cc) qh[cc] = *(const u32x4 *)(qs + h * (HD / 2) + qtr * (QD / 2) + 4 * cc);
+#pragma unroll
+            for (int i = 0; i < PPW; ++i) {
+                const bool vis = ok_cur[i] && cbase + (wave + 4 * i) * kPage + kin < nk;
+                float d2 = 0.f;
+#pragma unroll
+                for (int cc = 0; cc < KL; ++cc)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) d2 = dot2(qh[cc][e], kr[i][cc][e], d2);
+                d2 += __shfl_xor(d2, 1, 64);
+                d2 += __shfl_xor(d2, 2, 64);
+                s[i][h] = vis ? d2 * scale : -INFINITY;
+                mloc[h] = fmaxf(mloc[h], s[i][h]);
+            }
+            __builtin_amdgcn_sched_barrier(0);   // one head's q in registers at a time
+        }
+        // the next chunk's keys go out now (kr is free); its page ids were loaded a chunk ago.
+        // The scheduling barrier keeps the loads below the dot products, so the next chunk's
+        // keys reuse this chunk's registers instead of needing a second set.
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 1 < n_ch) {
+            check_pages(c + 1, pg_nxt, ok_nxt);
+            issue_k(pg_nxt);
+        }
+        // ---- online softmax over the wave's keys so far
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            float mh = mloc[h];
+#pragma unroll
+            for (int o = 4; o <= 32; o <<= 1) mh = fmaxf(mh, __shfl_xor(mh, o, 64));
+            const float mn = fmaxf(m[h], mh);
+            const float alpha = m[h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[h] - mn);
+            m[h] = mn;
+            float ls = 0.f;
+#pragma unroll
+            for (int i = 0; i < PPW; ++i) {
+                const float pr = mn == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[i][h] - mn);
+                ls += pr;
+                // key i*16 + kin of this wave; adjacent keys share one 32-bit word
+                const int key = i * kPage + kin;
+                if (qtr == 0) pk16[((key >> 1) * G + h) * 2 + (key & 1)] = (uint16_t)f2bf_bits(pr);
+            }
+#pragma unroll
+            for (int o = 4; o <= 32; o <<= 1) ls += __shfl_xor(ls, o, 64);
+            l[h] = l[h] * alpha + ls;
+#pragma unroll
+            for (int d = 0; d < VD; ++d) acc[h][d] *= alpha;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // ---- P V from registers: this lane owns head dims lane*VD .. lane*VD+VD-1 of its pages
-    const uint32_t *pkw = pk_all + wave * (KPW / 2) * G;
-    float acc[G][VD];
+        // ---- P V from registers: this lane owns head dims lane*VD .. lane*VD+VD-1 of its pages
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+        for (int i = 0; i < PPW; ++i) {
+            // positions of page i inside the split (0 when the page is absent or invalid)
+            const int valid = ok_cur[i] ? min(kPage, nk - cbase - (wave + 4 * i) * kPage) : 0;
 #pragma unroll
-        for (int d = 0; d < VD; ++d) acc[h][d] = 0.f;
+            for (int d = 0; d < VD; ++d) {
 #pragma unroll
-    for (int i = 0; i < PPW; ++i) {
-        // positions of page i inside the split (0 when the page is absent or invalid)
-        const int valid = pok[i] ? min(kPage, nk - (wave + 4 * i) * kPage) : 0;
+                for (int jp = 0; jp < 8; ++jp) {
+                    uint32_t vv = vr[i][(d * 8 + jp) >> 2][(d * 8 + jp) & 3];
+                    // positions past the split hold other data (or NaN poison): zero them
+                    vv = (2 * jp + 1 < valid) ? vv : ((2 * jp < valid) ? (vv & 0xffffu) : 0u);
+                    const uint32_t *pw = pkw + (i * 8 + jp) * G;
 #pragma unroll
-        for (int d = 0; d < VD; ++d) {
-#pragma unroll
-            for (int jp = 0; jp < 8; ++jp) {
-                uint32_t vv = vr[i][(d * 8 + jp) >> 2][(d * 8 + jp) & 3];
-                // positions past the split hold other data (or NaN poison): zero them
-                vv = (2 * jp + 1 < valid) ? vv : ((2 * jp < valid) ? (vv & 0xffffu) : 0u);
-                const uint32_t *pw = pkw + (i * 8 + jp) * G;
-#pragma unroll
-                for (int h = 0; h < G; ++h) acc[h][d] = dot2(pw[h], vv, acc[h][d]);
+                    for (int h = 0; h < G; ++h) acc[h][d] = dot2(pw[h], vv, acc[h][d]);
+                }
             }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 1 < n_ch) {
+            issue_v(pg_nxt);
+#pragma unroll
+            for (int i = 0; i < PPW; ++i) {
+                pg_cur[i] = pg_nxt[i];
+                ok_cur[i] = ok_nxt[i];
+            }
+            if (c + 2 < n_ch) load_pages(c + 2, pg_nxt);
+        }
+        // the next chunk's weights overwrite this wave's LDS slots only after these reads
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
     if (lane == 0) {
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            mw[wave * G + h] = mloc[h];
+            mw[wave * G + h] = m[h];
             lw[wave * G + h] = l[h];
         }
     }
@@ -208,7 +271,7 @@ __device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *sme
         float L = 0.f, sum = 0.f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            const float sc_w = mw[w * G + h] == -INFINITY ? 0.f : exp2f(mw[w * G + h] - M);
+            const float sc_w = mw[w * G + h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[w * G + h] - M);
             L += lw[w * G + h] * sc_w;
             sum += part[(w * G + h) * HD + d] * sc_w;
         }
@@ -411,53 +474,67 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         return int2{pg_lds[p0 - w0], pg_lds[p1 - w0]};
     };
 
-    // chunk assignment of this thread: PER_THREAD chunks c = tid + 256 * i over [K | V]; two
-    // register stages keep the loads of the next two blocks in flight
+    // chunk assignment of this thread: PER_THREAD chunks c = tid + 256 * i over [K | V] (the
+    // first KI of them key chunks); two register stages keep the next two blocks' loads in
+    // flight.  Source and LDS offsets do not depend on the block, only the two page ids do.
+    constexpr int KI = St::KCH / 256;
+    static_assert(St::KCH % 256 == 0, "key chunks per thread");
+    uint32_t src_off[St::PER_THREAD], lds_off[St::PER_THREAD];
+    int lo_key[St::PER_THREAD];       // K: key within the block; V: first key of the 8-key run
+    bool hi_page[St::PER_THREAD];     // chunk reads the block's second page
+#pragma unroll
+    for (int i = 0; i < St::PER_THREAD; ++i) {
+        const int c = tid + 256 * i;
+        if (i < KI) {
+            const int key = c / (HD / 8), part = c % (HD / 8);
+            hi_page[i] = key >= kPage;
+            lo_key[i] = key;
+            src_off[i] = ((g * kPage + (key & 15)) * HD + part * 8) * 2;
+            lds_off[i] = key * St::KROW + part * 16;
+        } else {
+            const int v = c - St::KCH;
+            const int p2 = v / (HD * 2), rem = v % (HD * 2);
+            const int d = rem >> 1, h2 = rem & 1;
+            hi_page[i] = p2 != 0;
+            lo_key[i] = p2 * kPage + h2 * 8;
+            src_off[i] = (g * HD + d) * kPage * 2 + h2 * 16;
+            lds_off[i] = 32 * St::KROW + d * St::VROW + p2 * 32 + h2 * 16;
+        }
+    }
     u32x4 stg0[St::PER_THREAD], stg1[St::PER_THREAD];
     auto issue = [&](u32x4 (&stg)[St::PER_THREAD], int2 pg) {
-        const int sp0 = pg.x >= 0 ? pg.x : 0, sp1 = pg.y >= 0 ? pg.y : 0;
+        const char *k0 = pv.k + (size_t)max(pg.x, 0) * page_bytes, *k1 = pv.k + (size_t)max(pg.y, 0) * page_bytes;
+        const char *v0 = pv.v + (size_t)max(pg.x, 0) * page_bytes, *v1 = pv.v + (size_t)max(pg.y, 0) * page_bytes;
 #pragma unroll
         for (int i = 0; i < St::PER_THREAD; ++i) {
-            const int c = tid + 256 * i;
-            const char *src;
-            if (c < St::KCH) {
-                const int key = c / (HD / 8), part = c % (HD / 8);
-                const int pgid = key < kPage ? sp0 : sp1;
-                src = pv.k + pgid * page_bytes + (size_t)((g * kPage + (key & 15)) * HD + part * 8) * 2;
-            } else {
-                const int v = c - St::KCH;
-                const int p2 = v / (HD * 2), rem = v % (HD * 2);
-                const int d = rem >> 1, h2 = rem & 1;
-                const int pgid = p2 ? sp1 : sp0;
-                src = pv.v + pgid * page_bytes + (size_t)((g * HD + d) * kPage) * 2 + h2 * 16;
-            }
-            stg[i] = *(const u32x4 *)src;
+            const char *base = i < KI ? (hi_page[i] ? k1 : k0) : (hi_page[i] ? v1 : v0);
+            stg[i] = *(const u32x4 *)(base + src_off[i]);
         }
     };
+    // keys at or past the tile's causal bound, or on a bad page, are stored as zeros (their
+    // slots may hold other data or NaN poison); blocks clear of both are stored as loaded
     auto stash = [&](const u32x4 (&stg)[St::PER_THREAD], char *buf, int blk, int2 pg) {
         const bool ok0 = pg.x >= 0, ok1 = pg.y >= 0;
+        if (ok0 && ok1 && (blk + 1) * 32 <= kend) {
+#pragma unroll
+            for (int i = 0; i < St::PER_THREAD; ++i) *(u32x4 *)(buf + lds_off[i]) = stg[i];
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < St::PER_THREAD; ++i) {
-            const int c = tid + 256 * i;
             u32x4 v = stg[i];
-            if (c < St::KCH) {
-                const int key = c / (HD / 8), part = c % (HD / 8);
-                const bool keep = (key < kPage ? ok0 : ok1) && blk * 32 + key < kend;
-                if (!keep) v = u32x4{0u, 0u, 0u, 0u};
-                *(u32x4 *)(buf + key * St::KROW + part * 16) = v;
+            const bool ok = hi_page[i] ? ok1 : ok0;
+            if (i < KI) {
+                if (!ok || blk * 32 + lo_key[i] >= kend) v = u32x4{0u, 0u, 0u, 0u};
             } else {
-                const int vi = c - St::KCH;
-                const int p2 = vi / (HD * 2), rem = vi % (HD * 2);
-                const int d = rem >> 1, h2 = rem & 1;
-                // zero positions at or past the causal bound (other data or NaN poison)
-                const int nvalid = (p2 ? ok1 : ok0) ? kend - (blk * 32 + p2 * kPage + h2 * 8) : 0;
+                const int nvalid = ok ? kend - (blk * 32 + lo_key[i]) : 0;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const uint32_t m = (2 * e + 1 < nvalid) ? 0xffffffffu : ((2 * e < nvalid) ? 0xffffu : 0u);
                     v[e] &= m;
                 }
-                *(u32x4 *)(buf + 32 * St::KROW + d * St::VROW + p2 * 32 + h2 * 16) = v;
             }
+            *(u32x4 *)(buf + lds_off[i]) = v;
         }
     };
 
@@ -471,6 +548,10 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     for (int d = 0; d < DB; ++d)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[d][e] = 0.f;
+    // running maximum m (log2 domain, scores times `scale`) and sum l of this lane's query.  m
+    // is raised only when a block's maximum exceeds it by more than 2^8 (any lane of the wave),
+    // so the rescale of the accumulators is rare; probabilities stay below 2^8 in between and
+    // the final division by l is unaffected.
     float m = -INFINITY, l = 0.f;
     const float scale = kLog2e / sqrtf((float)HD);
     const int wave_first = off + qb + sb * 32;    // first query position of this wave
@@ -499,33 +580,44 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
                 s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
             }
             // lane's query = col; register e holds key 8*(e/4) + 4*half + e%4 of the block
-            const bool diag = (kb + 1) * 32 > wave_first;
-            float mloc = -INFINITY;
+            if ((kb + 1) * 32 > wave_first) {   // block reaches this wave's first query: mask
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int kpos = kb * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                const bool vis = !diag || kpos <= qpos;
-                s[e] = vis ? s[e] * scale : -INFINITY;
-                mloc = fmaxf(mloc, s[e]);
+                for (int e = 0; e < 16; ++e) {
+                    const int kpos = kb * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                    if (kpos > qpos) s[e] = -INFINITY;
+                }
             }
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-            const float mn = fmaxf(m, mloc);
-            const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mn);
-            float psum = 0.f;
-            bf16x8 pf[2];
+            float mloc = s[0];
+#pragma unroll
+            for (int e = 1; e < 16; ++e) mloc = fmaxf(mloc, s[e]);
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale;
+            if (__ballot(mloc > m + 8.f) != 0) {
+                const float mn = fmaxf(m, mloc);
+                const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+                l *= alpha;
+#pragma unroll
+                for (int d = 0; d < DB; ++d)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[d][e] *= alpha;
+                m = mn;
+            }
+            const float neg_m = (m == -INFINITY) ? 0.f : -m;
+            float p[16], psum = 0.f;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const float p = (mn == -INFINITY) ? 0.f : exp2f(s[e] - mn);
-                psum += p;
-                pf[e >> 3][e & 7] = from_f32<bf16>(p);
+                p[e] = __builtin_amdgcn_exp2f(fmaf(s[e], scale, neg_m));
+                psum += p[e];
             }
             psum += __shfl_xor(psum, 32, 64);
-            l = l * alpha + psum;
-            m = mn;
+            l += psum;
+            bf16x8 pf[2];
 #pragma unroll
-            for (int d = 0; d < DB; ++d)
+            for (int k2 = 0; k2 < 2; ++k2) {
+                u32x4 w;
 #pragma unroll
-                for (int e = 0; e < 16; ++e) acc[d][e] *= alpha;
+                for (int q = 0; q < 4; ++q) w[q] = pack_bf16x2(p[k2 * 8 + 2 * q], p[k2 * 8 + 2 * q + 1]);
+                pf[k2] = __builtin_bit_cast(bf16x8, w);
+            }
             // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; lane half `half` holds keys
             // 16*k2 + 4*half .. +3 and 16*k2 + 8 + 4*half .. +3 of the block
 #pragma unroll
@@ -591,7 +683,8 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
 template <bool BF16, int HD, int G>
 constexpr size_t attn_smem() {
     constexpr int MAXK = kSplitPages * kPage;
-    constexpr size_t dec = BF16 ? (4 * (MAXK / 4 / 2) * G + 8 * G + 4 * G * HD) * 4
+    constexpr int DK = kDecodeChunkPages * kPage;   // keys of one bf16 decode chunk
+    constexpr size_t dec = BF16 ? (4 * (DK / 4 / 2) * G + 8 * G + 4 * G * HD + 4 * G * HD / 2) * 4
                                 : (MAXK * G + 8 * G + 4 * G * HD) * 4;
     constexpr size_t pre = BF16 ? 2 * PrefillStage<HD>::BYTES + 4 * kPrefillPageWindow : 0;
     return dec > pre ? dec : pre;
@@ -628,7 +721,7 @@ __global__ __launch_bounds__(G * HD) void attn_combine_kernel(AttnArgs a) {
 #pragma unroll 8
     for (int s = 0; s < nsplit; ++s) {
         const float *q = pp + (size_t)s * STRIDE;
-        const float w = (q[0] == -INFINITY) ? 0.f : exp2f(q[0] - M);
+        const float w = (q[0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(q[0] - M);
         L += q[1] * w;
         acc += q[2 + d] * w;
     }

@@ -17,14 +17,15 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
-// round-to-nearest-even float -> bf16 bits (inputs here are finite)
+// float -> bf16, round to nearest even: gfx950's v_cvt_pk_bf16_f32 (two values per instruction)
 __device__ __forceinline__ uint32_t f2bf_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
+    return __builtin_bit_cast(uint16_t, (bf16)f);
 }
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f2bf_bits(lo) | (f2bf_bits(hi) << 16);
+    bf16x2 v;
+    v[0] = (bf16)lo;
+    v[1] = (bf16)hi;
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 template <typename T> __device__ __forceinline__ float to_f32(T v);
@@ -34,9 +35,7 @@ template <> __device__ __forceinline__ float to_f32<bf16>(bf16 v) {
 }
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
-template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) {
-    return __builtin_bit_cast(bf16, (uint16_t)f2bf_bits(v));
-}
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -8,6 +8,9 @@
 #include "plan.hpp"
 
 #include <algorithm>
+#include <array>
+
+#include <algorithm>
 #include <numeric>
 #include <set>
 #include <utility>
@@ -104,12 +107,17 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         it[IT_KEY_END] = pre[k].kend;
         it[IT_PARTIAL] = -1;
     }
+    // decode splits: whole chunks of kSplitPages pages, up to `cps` chunks per split, the
+    // row's chunks dealt out evenly over its splits
+    const int cps = gen.cfg.dtype == ORTHRUS_BF16 ? kDecodeChunksBf16 : 1;
+    std::vector<std::array<int32_t, kItemInts>> dec;
     int partial = 0;
     for (int j = 0; j < p.D; ++j) {
         const orthrus_decode_row &r = b.rows[j];
         const int n_keys = r.ctx_len + 1;
         const int n_pages = (n_keys + P - 1) / P;
-        const int n_splits = (n_pages + kSplitPages - 1) / kSplitPages;
+        const int n_chunk = (n_pages + kSplitPages - 1) / kSplitPages;
+        const int n_splits = (n_chunk + cps - 1) / cps;
         rows[kRowInts * j + 0] = r.seq;
         rows[kRowInts * j + 1] = r.ctx_len;
         rows[kRowInts * j + 2] = p.Te + j;
@@ -118,21 +126,29 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         if (n_splits > 1) p.n_split_rows++;
         for (int g = 0; g < nkv; ++g) {
             for (int s = 0; s < n_splits; ++s) {
-                int32_t it[kItemInts];
+                const int c0 = (int)((int64_t)s * n_chunk / n_splits);
+                const int c1 = (int)((int64_t)(s + 1) * n_chunk / n_splits);
+                std::array<int32_t, kItemInts> it{};
                 it[IT_KIND] = 1;
                 it[IT_INDEX] = j;
                 it[IT_KVHEAD] = g;
                 it[IT_A] = s;
                 it[IT_B] = n_splits;
-                it[IT_KEY_BEGIN] = s * kSplitPages * P;
-                it[IT_KEY_END] = std::min(n_keys, (s + 1) * kSplitPages * P);
+                it[IT_KEY_BEGIN] = c0 * kSplitPages * P;
+                it[IT_KEY_END] = std::min(n_keys, c1 * kSplitPages * P);
                 // partial slots: [first slot of row][kv head][split], each holding `group` heads
                 it[IT_PARTIAL] = n_splits > 1 ? partial + g * n_splits + s : -1;
-                items.insert(items.end(), it, it + kItemInts);
+                dec.push_back(it);
             }
         }
         if (n_splits > 1) partial += nkv * n_splits;
     }
+    // longest key ranges first, so the last round of the launch is short
+    std::stable_sort(dec.begin(), dec.end(), [](const std::array<int32_t, kItemInts> &x,
+                                                const std::array<int32_t, kItemInts> &y) {
+        return x[IT_KEY_END] - x[IT_KEY_BEGIN] > y[IT_KEY_END] - y[IT_KEY_BEGIN];
+    });
+    for (const auto &it : dec) items.insert(items.end(), it.begin(), it.end());
     p.n_decode_items = (int)(items.size() / kItemInts) - p.n_prefill;
     p.n_partials = partial;
 

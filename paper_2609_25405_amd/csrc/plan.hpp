@@ -12,8 +12,12 @@ namespace orthrus {
 // Query-head rows per prefill work item; a work item covers (128 / group) tokens of one
 // chunk times the `group` query heads that share one KV head.
 constexpr int kPrefillRows = 128;
-// Pages of one decode key-range split (16 pages = 256 keys of a 16-token page).
+// Pages of one decode chunk (16 pages = 256 keys of a 16-token page): the unit a decode work
+// item walks its key range in, and the whole split on the fp32 path.
 constexpr int kSplitPages = 16;
+// Chunks per decode split on the bf16 path (its items pipeline one chunk's loads under the
+// previous chunk's arithmetic, so longer splits keep the memory pipe busier).
+constexpr int kDecodeChunksBf16 = 4;
 
 struct Model {
     orthrus_config cfg;

@@ -148,12 +148,18 @@ def _check_coverage(batch, cfg, npre, ndec, items):
     assert work == sorted(work, reverse=True)  # heaviest first
     seen_k = {}
     slots = set()
+    # decode splits: whole 256-key chunks (the last one cut at the row's end), up to four
+    # chunks per split on the bf16 path and one on the fp32 path, longest first
+    max_split = 1024 if cfg.dtype == "bf16" else 256
+    lengths = []
     for it in items[npre:npre + ndec]:
         kind, j, g, s, ns, kb, ke, ps = it
         assert kind == 1
         r = batch.rows[j]
-        assert 0 <= s < ns and kb % P_ == 0 and kb < ke <= r.ctx_len + 1
-        assert ke - kb <= 256
+        assert 0 <= s < ns and kb % 256 == 0 and kb < ke <= r.ctx_len + 1
+        assert ke == r.ctx_len + 1 or ke % 256 == 0
+        assert ke - kb <= max_split
+        lengths.append(ke - kb)
         for k in range(kb, ke):
             assert (j, g, k) not in seen_k
             seen_k[(j, g, k)] = True
@@ -163,6 +169,7 @@ def _check_coverage(batch, cfg, npre, ndec, items):
             assert ps not in slots
             slots.add(ps)
     assert len(seen_k) == sum(r.ctx_len + 1 for r in batch.rows) * cfg.n_kv_heads
+    assert lengths == sorted(lengths, reverse=True)
     if slots:
         assert slots == set(range(len(slots)))
 
