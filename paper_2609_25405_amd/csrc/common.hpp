@@ -133,7 +133,9 @@ struct PoolArgs {
 };
 // final RMSNorm over rows [row0, row0 + rows): 1/rms of embedding rows, normalised decode rows
 hipError_t launch_final_rows(int dtype, const PoolArgs &a, int rows, hipStream_t s);
-// incremental pooler update and finished embeddings (needs launch_final_rows on the emb rows)
-hipError_t launch_pool(const PoolArgs &a, hipStream_t s);
+// incremental pooler update and finished embeddings.  Single-row heads (last token, CLS) take
+// their row's final norm themselves (adding npend slabs); with any_mean, mean-pooled chunks
+// are accumulated too and need launch_final_rows over their rows first.
+hipError_t launch_pool(const PoolArgs &a, bool any_mean, hipStream_t s);
 
 }  // namespace orthrus

@@ -167,16 +167,15 @@ __device__ __forceinline__ bool chunk_state_ok(const int32_t *ch, const float *a
     return off == 0 || acc_w[seq] == (float)off;
 }
 
-// S update of Eq. (1) for mean (w = 1), positional heads keep their one row.
-// Block = 64 columns x 4 row slices; grid = (chunks, d / 64).
+// S update of Eq. (1) for mean pooling (w = 1).  Block = 64 columns x 4 row slices; grid =
+// (chunks, d / 64).  Needs the final-norm scales of the chunk's rows (final_rows_kernel).
 __global__ __launch_bounds__(256) void pool_accum_kernel(PoolArgs a) {
     __shared__ float part[4][64];
     const int ci = blockIdx.x;
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3], t0 = ch[4];
     const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
-    const bool last = flags & ORTHRUS_CHUNK_LAST;
-    if (pool == ORTHRUS_POOL_NONE) return;
+    if (pool != ORTHRUS_POOL_MEAN) return;   // single-row heads are done by pool_rows_kernel
     if (!chunk_state_ok(ch, a.acc_w)) {
         if (blockIdx.y == 0 && threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_ACC);
         return;
@@ -184,34 +183,24 @@ __global__ __launch_bounds__(256) void pool_accum_kernel(PoolArgs a) {
     const int c = blockIdx.y * 64 + (threadIdx.x & 63), slice = threadIdx.x >> 6;
     const float gc = a.gain[c];
     float *S = a.acc_sum + (size_t)seq * a.d + c;
-    if (pool == ORTHRUS_POOL_MEAN) {
-        float s = 0.f;
-        for (int r = slice; r < len; r += 4) s += a.x[(size_t)(t0 + r) * a.d + c] * a.inv_rms[t0 + r];
-        part[slice][threadIdx.x & 63] = s;
-        __syncthreads();
-        if (slice == 0) {
-            const float tot = ((part[0][c & 63] + part[1][c & 63]) + part[2][c & 63]) + part[3][c & 63];
-            *S = (off == 0 ? 0.f : *S) + tot * gc;
-        }
-        return;
-    }
-    if (slice != 0) return;
-    if (pool == ORTHRUS_POOL_LAST) {
-        if (last) *S = a.x[(size_t)(t0 + len - 1) * a.d + c] * a.inv_rms[t0 + len - 1] * gc;
-        else if (off == 0) *S = 0.f;
-    } else {  // CLS
-        if (off == 0) *S = a.x[(size_t)t0 * a.d + c] * a.inv_rms[t0] * gc;
+    float s = 0.f;
+    for (int r = slice; r < len; r += 4) s += a.x[(size_t)(t0 + r) * a.d + c] * a.inv_rms[t0 + r];
+    part[slice][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (slice == 0) {
+        const float tot = ((part[0][c & 63] + part[1][c & 63]) + part[2][c & 63]) + part[3][c & 63];
+        *S = (off == 0 ? 0.f : *S) + tot * gc;
     }
 }
 
-// W update of Eq. (2) and, for a request's final chunk, v / max(||v||, 1e-12)
+// W update of Eq. (2) and, for a request's final chunk, v / max(||v||, 1e-12), mean pooling
 __global__ __launch_bounds__(256) void pool_finish_kernel(PoolArgs a) {
     __shared__ float red[4];
     const int ci = blockIdx.x;
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3];
     const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
-    if (pool == ORTHRUS_POOL_NONE) return;
+    if (pool != ORTHRUS_POOL_MEAN) return;
     const bool ok = chunk_state_ok(ch, a.acc_w);
     __syncthreads();
     if (!ok) return;
@@ -220,7 +209,7 @@ __global__ __launch_bounds__(256) void pool_finish_kernel(PoolArgs a) {
     if (threadIdx.x == 0) a.acc_w[seq] = W;
     if (!(flags & ORTHRUS_CHUNK_LAST)) return;
     const float *S = a.acc_sum + (size_t)seq * a.d;
-    const float div = pool == ORTHRUS_POOL_MEAN ? W : 1.f;
+    const float div = W;
     float ss = 0.f;
     for (int i = threadIdx.x; i < a.d; i += 256) {
         const float v = S[i] / div;
@@ -230,6 +219,66 @@ __global__ __launch_bounds__(256) void pool_finish_kernel(PoolArgs a) {
     const float inv = 1.f / fmaxf(nrm, 1e-12f);
     float *out = a.out_emb + (size_t)ci * a.d;
     for (int i = threadIdx.x; i < a.d; i += 256) out[i] = (S[i] / div) * inv;
+}
+
+// Single-row heads (last token, CLS): one block per chunk does the whole update.  The pooled
+// row (the chunk's last row on its request's final chunk; row 0 of a request's first chunk)
+// gets its final RMSNorm here (after the pending split-K slabs, if any), S of Eq. (1) takes
+// that row (last: an offset-0 chunk without it clears S), W of Eq. (2) grows by the chunk
+// length, and a final chunk writes S / max(||S||, 1e-12).
+__global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
+    __shared__ float red[4];
+    const int ci = blockIdx.x;
+    const int32_t *ch = a.chunks + kChunkInts * ci;
+    const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3], t0 = ch[4];
+    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
+    const bool last = flags & ORTHRUS_CHUNK_LAST;
+    if (pool == ORTHRUS_POOL_NONE || pool == ORTHRUS_POOL_MEAN) return;
+    const float w_old = a.acc_w[seq];
+    if (!(off == 0 || w_old == (float)off)) {
+        if (threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_ACC);
+        return;
+    }
+    const int r = pool == ORTHRUS_POOL_LAST ? (last ? t0 + len - 1 : -1) : (off == 0 ? t0 : -1);
+    float *S = a.acc_sum + (size_t)seq * a.d;
+    const int nv = a.d / 4;
+    if (r >= 0) {
+        const float *xr = a.x + (size_t)r * a.d;
+        auto row = [&](int v) {
+            float4 q = load4(xr + 4 * v);
+            for (int sp = 0; sp < a.npend; ++sp) {
+                const float4 p = load4(a.pend + sp * a.pend_stride + (size_t)r * a.d + 4 * v);
+                q = float4{q.x + p.x, q.y + p.y, q.z + p.z, q.w + p.w};
+            }
+            return q;
+        };
+        float ss = 0.f;
+        for (int v = threadIdx.x; v < nv; v += 256) {
+            const float4 q = row(v);
+            ss += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+        }
+        const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
+        for (int v = threadIdx.x; v < nv; v += 256) {
+            const float4 q = row(v), g = load4(a.gain + 4 * v);
+            store4(S + 4 * v, float4{q.x * inv * g.x, q.y * inv * g.y, q.z * inv * g.z, q.w * inv * g.w});
+        }
+    } else if (pool == ORTHRUS_POOL_LAST && off == 0) {
+        for (int v = threadIdx.x; v < nv; v += 256) store4(S + 4 * v, float4{0.f, 0.f, 0.f, 0.f});
+    }
+    __syncthreads();  // S complete; every thread has read the old W
+    if (threadIdx.x == 0) a.acc_w[seq] = (off == 0 ? 0.f : w_old) + (float)len;
+    if (!last) return;
+    float nn = 0.f;
+    for (int v = threadIdx.x; v < nv; v += 256) {
+        const float4 q = load4(S + 4 * v);
+        nn += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+    }
+    const float sc = 1.f / fmaxf(sqrtf(block_sum(nn, red)), 1e-12f);
+    float *out = a.out_emb + (size_t)ci * a.d;
+    for (int v = threadIdx.x; v < nv; v += 256) {
+        const float4 q = load4(S + 4 * v);
+        store4(out + 4 * v, float4{q.x * sc, q.y * sc, q.z * sc, q.w * sc});
+    }
 }
 
 }  // namespace
@@ -260,10 +309,13 @@ hipError_t launch_final_rows(int dtype, const PoolArgs &a, int rows, hipStream_t
     return hipGetLastError();
 }
 
-hipError_t launch_pool(const PoolArgs &a, hipStream_t s) {
+hipError_t launch_pool(const PoolArgs &a, bool any_mean, hipStream_t s) {
     if (a.n_chunks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(pool_accum_kernel, dim3(a.n_chunks, a.d / 64), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(pool_finish_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(pool_rows_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
+    if (any_mean) {
+        hipLaunchKernelGGL(pool_accum_kernel, dim3(a.n_chunks, a.d / 64), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(pool_finish_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 

@@ -442,10 +442,22 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     pa.row0 = 0;
     pa.eps = c.rms_eps;
     pa.err = err;
-    // with no layers the gather already normalised the decode rows with the final gain
-    const int final_rows = c.n_layers > 0 ? T : Te;
-    if (final_rows > 0) RUN("final_norm", launch_final_rows(dt, pa, final_rows, s));
-    if (p.n_chunks > 0) RUN("pool", launch_pool(pa, s));
+    // Only mean pooling needs the final norm of every embedding row; single-row heads normalise
+    // their one row inside the pooler.  With no layers the gather already normalised the
+    // decode rows with the final gain.
+    bool any_mean = false;
+    for (int i = 0; i < batch->n_chunks; ++i)
+        any_mean |= ((batch->chunks[i].flags >> ORTHRUS_POOL_SHIFT) & 3) == ORTHRUS_POOL_MEAN;
+    const int row_first = any_mean ? 0 : Te;
+    const int row_end = c.n_layers > 0 ? T : (any_mean ? Te : 0);
+    if (row_end > row_first) {
+        pa.row0 = row_first;
+        RUN("final_norm", launch_final_rows(dt, pa, row_end - row_first, s));
+    }
+    // the embedding rows' pending slabs were added by the final norm when it covered them
+    pa.row0 = 0;
+    if (any_mean) pa.npend = 0;
+    if (p.n_chunks > 0) RUN("pool", launch_pool(pa, any_mean, s));
     if (p.D > 0) {
         GemmArgs ga{};
         ga.A = act + (size_t)Te * d * es;

@@ -77,6 +77,10 @@ def test_gqa_long_context_splits(dtype):
     rows = [DecodeRow(3 + i, c) for i, c in enumerate(ctx)]
     ids = draw_tokens(7, 1, 200 + 133 + 97 + len(rows), cfg.vocab)
     pair.step(Batch(chunks, rows, ids))
+    # no mean-pooled chunk: the single-row heads take their own final norm (and any pending
+    # split-K slabs) inside the pooler; requests 0 and 2 restart at offset 0
+    chunks2 = [EmbChunk(0, 0, 64, False, "cls"), EmbChunk(2, 0, 80, True, "last")]
+    pair.step(Batch(chunks2, [], draw_tokens(7, 2, 144, cfg.vocab)))
     print(pair.report, flush=True)
 
 
