@@ -54,7 +54,22 @@ __device__ __forceinline__ void flag_error(int *err, int bit) { atomicOr(err, bi
 // ---------------------------------------------------------------------------------------
 // launchers (host functions defined next to their kernels)
 // ---------------------------------------------------------------------------------------
-enum GemmEpilogue { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+enum GemmEpilogue { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3 };
+
+// QKV projection epilogue (bf16 path): rotate q and k at each token's position, store q for
+// attention and append rotated k and raw v to the paged cache (Section 3.2's cache writes)
+struct QkvRope {
+    const float2 *cs;          // [T][hd/2] (cos, sin) of each token's position
+    const int32_t *pos, *seq;  // per token (global token index)
+    void *q_out;               // [T][nq][hd]
+    void *k_cache[2], *v_cache[2];          // layer base per pool
+    const int32_t *block_table[2];
+    int n_pages[2], max_blocks[2];
+    int row0;                  // global token index of the launch's row 0
+    int Te;                    // tokens < Te use pool 0, others pool 1
+    int nq, nkv, hd, page;
+    int *err;
+};
 
 struct GemmArgs {
     const void *A;   // [M][K] activations, row stride lda (elements)
@@ -67,6 +82,7 @@ struct GemmArgs {
     int splits;
     float *partial;
     size_t split_stride;
+    QkvRope rope;    // EPI_QKV_ROPE only
 };
 hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
 // split-K factor (<= max_splits, dividing K into whole stages) for a bf16 residual-add
@@ -85,6 +101,11 @@ struct NormArgs {
     void *y;                // normalised rows [rows][d], model dtype
     int rows, d;
     float eps;
+    // gather mode, optional: per row (cos, sin) of pos * base^(-2i/hd), i < hd/2, into cs
+    float2 *cs;
+    const int32_t *pos;
+    int hd;
+    float rope_base;
 };
 hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t s);
 

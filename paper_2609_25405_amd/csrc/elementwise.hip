@@ -38,6 +38,13 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
     const int nv = a.d / 4;
     float *xrow = (GATHER ? a.x_out : const_cast<float *>(a.x)) + (size_t)r * a.d;
     float ss = 0.f;
+    if (GATHER && a.cs && threadIdx.x < a.hd / 2) {
+        // rotation table of this token for the QKV epilogue (angle evaluated in double)
+        const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
+        double sv, cv;
+        sincos((double)a.pos[r] * inv_freq, &sv, &cv);
+        a.cs[(size_t)r * (a.hd / 2) + threadIdx.x] = float2{(float)cv, (float)sv};
+    }
     if (GATHER) {
         const T *src = (const T *)a.table + (size_t)a.tok[r] * a.d;
         for (int v = threadIdx.x; v < nv; v += 256) {

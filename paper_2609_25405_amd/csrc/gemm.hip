@@ -11,6 +11,7 @@
 // weight tile inside one L2.
 // fp32 path: plain LDS-tiled FMA kernel (64x64 tile, 4x4 per thread) for exact checks.
 #include "common.hpp"
+#include "orthrus.h"
 
 namespace orthrus {
 
@@ -60,7 +61,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     static_assert(A_INST * RPI * NW == BM && B_INST * RPI * NW == BN, "copy split");
     static_assert(FM >= 1 && FN >= 1 && (EPI != EPI_SWIGLU || FN % 2 == 0), "tile shape");
     static_assert(STAGES >= 2 && (STAGES - 2) * INST < 64, "pipeline depth");
-    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+    // the QKV epilogue stages the fp32 tile (rows padded to 136 floats) and per-row metadata
+    constexpr int CROW = 136;
+    constexpr int EPI_BYTES = EPI == EPI_QKV_ROPE ? BM * CROW * 4 + BM * 16 : 0;
+    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE > EPI_BYTES ? STAGES * STAGE : EPI_BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
@@ -185,6 +189,130 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
         }
     }
 
+    if constexpr (EPI == EPI_QKV_ROPE) {
+        // Rotation of q and k at each token's position (pairs (i, i + hd/2)), q stored for
+        // attention, rotated k and raw v appended to the paged cache.  The fp32 tile goes
+        // through LDS so every store is a 16-byte piece: 8 dims of a q or k row, or (values,
+        // dim-major pages) 8 consecutive slots of one dim when 8 rows fill them.
+        static_assert(BN == 128, "tiles of whole heads");
+        const QkvRope &q = a.rope;
+        float *ct = (float *)smem;                       // [BM][CROW] fp32 tile
+        int4 *meta = (int4 *)(smem + BM * CROW * 4);     // per row {token, slot, page or -1, pool}
+        __syncthreads();                                 // every wave is done with the stage buffers
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < FN; ++ni)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = wm * TM + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                    ct[row * CROW + wn * TN + ni * 32 + (lane & 31)] = acc[mi][ni][r];
+                }
+        for (int rr = tid; rr < BM; rr += 64 * NW) {
+            const int lr = m0 + rr;
+            int4 md{-1, 0, -1, 0};
+            if (lr < a.M) {
+                const int t = q.row0 + lr;
+                const int pos = q.pos[t], sq = q.seq[t], pl = t < q.Te ? 0 : 1;
+                const int page = q.block_table[pl][(size_t)sq * q.max_blocks[pl] + pos / q.page];
+                const bool ok = page >= 0 && page < q.n_pages[pl];
+                // flagged once per row: by the tile holding the first key head
+                if (!ok && n0 == q.nq * q.hd) flag_error(q.err, ORTHRUS_DEVERR_PAGE);
+                md = int4{t, pos % q.page, ok ? page : -1, pl};
+            }
+            meta[rr] = md;
+        }
+        __syncthreads();
+        const int hd = q.hd, half = hd / 2, G8 = half / 8;
+        for (int h2 = 0; h2 < 128 / hd; ++h2) {
+            const int head = (n0 + h2 * hd) / hd;
+            if (head < q.nq + q.nkv) {
+                // q or k: items (row, group of 8 pairs)
+                const bool is_q = head < q.nq;
+                const int kvh = head - q.nq;
+                for (int it = tid; it < BM * G8; it += 64 * NW) {
+                    const int row = it / G8, g = it % G8;
+                    const int4 md = meta[row];
+                    if (md.x < 0 || (!is_q && md.z < 0)) continue;
+                    const float *lo = ct + row * CROW + h2 * hd + g * 8, *hi = lo + half;
+                    const float4 *csp = (const float4 *)(q.cs + (size_t)md.x * half + g * 8);
+                    u32x4 w1, w2;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float4 cs = csp[e];   // (cos, sin) of pairs 2e and 2e + 1
+                        const float a0 = lo[2 * e], a1 = lo[2 * e + 1], b0 = hi[2 * e], b1 = hi[2 * e + 1];
+                        w1[e] = pack_bf16x2(a0 * cs.x - b0 * cs.y, a1 * cs.z - b1 * cs.w);
+                        w2[e] = pack_bf16x2(b0 * cs.x + a0 * cs.y, b1 * cs.z + a1 * cs.w);
+                    }
+                    bf16 *dst = is_q ? (bf16 *)q.q_out + ((size_t)md.x * q.nq + head) * hd
+                                     : (bf16 *)q.k_cache[md.w] + (((size_t)md.z * q.nkv + kvh) * q.page + md.y) * hd;
+                    *(u32x4 *)(dst + g * 8) = w1;
+                    *(u32x4 *)(dst + half + g * 8) = w2;
+                }
+            } else {
+                // v: items (dim, group of 8 rows); a dim of one page holds `page` slots contiguously
+                const int kvh = head - q.nq - q.nkv;
+                for (int it = tid; it < hd * (BM / 8); it += 64 * NW) {
+                    const int d = it % hd, r0 = (it / hd) * 8;
+                    const int4 m0d = meta[r0];
+                    bool run = m0d.x >= 0 && m0d.z >= 0 && (m0d.y & 7) == 0;
+#pragma unroll
+                    for (int k = 1; k < 8; ++k) {
+                        const int4 mk = meta[r0 + k];
+                        run = run && mk.z == m0d.z && mk.w == m0d.w && mk.y == m0d.y + k;
+                    }
+                    const float *col = ct + r0 * CROW + h2 * hd + d;
+                    if (run) {
+                        u32x4 w;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(col[(2 * e) * CROW], col[(2 * e + 1) * CROW]);
+                        bf16 *vc = (bf16 *)q.v_cache[m0d.w] + (((size_t)m0d.z * q.nkv + kvh) * hd + d) * q.page + m0d.y;
+                        *(u32x4 *)vc = w;
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const int4 mk = meta[r0 + k];
+                            if (mk.x < 0 || mk.z < 0) continue;
+                            bf16 *vc = (bf16 *)q.v_cache[mk.w] + (((size_t)mk.z * q.nkv + kvh) * hd + d) * q.page + mk.y;
+                            *vc = (bf16)col[k * CROW];
+                        }
+                    }
+                }
+            }
+        }
+        return;
+    }
+
+    if constexpr (EPI == EPI_SWIGLU) {
+        // The MFMA layout leaves each lane one column of 16 rows per fragment, i.e. 2-byte
+        // stores per output.  Instead the BM x BN/2 bf16 output tile is staged through the
+        // idle stage buffers and written back as whole 16-byte pieces of its rows.
+        constexpr int OC = BN / 2;                 // output columns of the tile
+        constexpr int OROW = OC * 2 + 16;          // padded LDS row: rows 4 apart differ by 16 banks
+        static_assert(BM * OROW <= STAGES * STAGE, "output tile fits the stage buffers");
+        __syncthreads();                           // every wave is done with the stage buffers
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = wm * TM + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+#pragma unroll
+                for (int ni = 0; ni < FN / 2; ++ni) {
+                    const int col = wn * (TN / 2) + ni * 32 + (lane & 31);
+                    *(bf16 *)(smem + row * OROW + col * 2) = (bf16)(silu(acc[mi][ni][r]) * acc[mi][ni + FN / 2][r]);
+                }
+            }
+        __syncthreads();
+        constexpr int PPR = OC / 8;                // 16-byte pieces per row
+        for (int c = tid; c < BM * PPR; c += 64 * NW) {
+            const int row = c / PPR, part = c % PPR;
+            const int grow = m0 + row, gcol = n0 + part * 8;
+            if (grow < a.M && gcol < a.N)
+                *(u32x4 *)((bf16 *)a.out + (size_t)grow * a.ldo + gcol) = *(const u32x4 *)(smem + row * OROW + part * 16);
+        }
+        return;
+    }
+
     // epilogue: lane holds column (lane & 31) of each 32x32 tile, rows 8*(r/4) + 4*(lane/32) + r%4
 #pragma unroll
     for (int mi = 0; mi < FM; ++mi) {
@@ -295,20 +423,24 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 // Tile choice per shape, from measurements of the step's projections on MI355X (M = 1088
 // tokens of a 7B-class layer).  Copy latency, not LDS or MFMA issue, bounds these GEMMs, so
 // the choice trades tile reuse against filling the CUs:
-//  - M <= 64 (decode-only batches, the LM head): weight streaming; a 3-deep copy ring keeps
-//    enough bytes in flight per CU (70 -> 43 us for a 64 x 32000 x 4096 LM head);
+//  - M <= 64 (decode-only batches, the LM head): weight streaming; 64x64 tiles (more
+//    workgroups) with a 4-deep copy ring keep enough bytes in flight per CU (LM head
+//    64 x 32000 x 4096: 70 -> 43 us with warm caches; decode-batch QKV 35 -> 25 us);
 //  - gate/up: 192x256 tiles over 8 waves;
 //  - residual-add projections with split-K slabs: 192x256 over 8 waves, split 2 (o 58 -> 46 us,
 //    down 177 -> 135 us against 128x128 tiles);
 //  - otherwise 128x128 (64 KiB of LDS, two workgroups per CU hide each other's waits).
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
-    if constexpr (EPI == EPI_SWIGLU) {
+    if constexpr (EPI == EPI_QKV_ROPE) {
+        if (a.M <= 64) return run_bf16<64, 128, 2, 2, EPI, 64, 4>(a, s);
+        return run_bf16<128, 128, 2, 2, EPI>(a, s);
+    } else if constexpr (EPI == EPI_SWIGLU) {
         if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI, 64, 3>(a, s);
         if (a.M > 128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else {
-        if (a.M <= 64) return run_bf16<64, 128, 1, 4, EPI, 64, 3>(a, s);
+        if (a.M <= 64) return run_bf16<64, 64, 2, 2, EPI, 64, 4>(a, s);
         if (EPI == EPI_ADD_F32 && a.partial && a.splits > 1) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         if (EPI == EPI_ADD_F32) return run_bf16<128, 128, 4, 2, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
@@ -318,11 +450,11 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 // Split-K factor for a residual-add projection on the bf16 path, for the tiles dispatch_bf16
-// uses with it (64x128 for M <= 64, else 192x256, one workgroup per CU): the factor whose
+// uses with it (64x64 for M <= 64, else 192x256, one workgroup per CU): the factor whose
 // workgroups fill the last round over 256 CUs best, the smaller one on a tie, each split a whole
 // number of 64-deep stages and at least 512 deep.  1 = no split.
 int gemm_add_splits(int M, int N, int K, int max_splits) {
-    const int bm = M <= 64 ? 64 : 192, bn = M <= 64 ? 128 : 256;
+    const int bm = M <= 64 ? 64 : 192, bn = M <= 64 ? 64 : 256;
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     auto fill = [](long w) { const long rounds = (w + 255) / 256; return (double)w / (double)(rounds * 256); };
     int best = 1;
@@ -341,9 +473,13 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, hipStream_t s) {
         switch (epi) {
             case EPI_STORE_F32: return dispatch_bf16<EPI_STORE_F32>(a, s);
             case EPI_ADD_F32: return dispatch_bf16<EPI_ADD_F32>(a, s);
+            case EPI_QKV_ROPE:
+                if (a.rope.hd != 64 && a.rope.hd != 128) return hipErrorInvalidValue;
+                return dispatch_bf16<EPI_QKV_ROPE>(a, s);
             default: return dispatch_bf16<EPI_SWIGLU>(a, s);
         }
     }
+    if (epi == EPI_QKV_ROPE) return hipErrorInvalidValue;   // fp32 path: GEMM, then rope_append
     dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
     switch (epi) {
         case EPI_STORE_F32: hipLaunchKernelGGL(gemm_f32_kernel<EPI_STORE_F32>, grid, dim3(256), 0, s, a); break;

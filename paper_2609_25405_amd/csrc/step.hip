@@ -36,7 +36,7 @@ constexpr size_t kAlign = 256;
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, split_slabs, total;
+    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, split_slabs, rope_cs, total;
 };
 // split-K slabs of one residual-add projection: at most kMaxSplits fp32 [T][d] slabs
 constexpr int kMaxSplits = 4;
@@ -50,13 +50,15 @@ Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials
     L.meta = o; o += up(meta_ints * 4);
     L.x = o; o += up(T * d * 4);
     L.act = o; o += up(T * d * es);
-    L.qkv = o; o += up(T * (size_t)m.qkv_dim() * 4);
+    // fp32 QKV rows for the separate rotation kernel (fp32 path; bf16 rotates in the GEMM)
+    L.qkv = o; o += m.cfg.dtype == ORTHRUS_BF16 ? 0 : up(T * (size_t)m.qkv_dim() * 4);
     L.q = o; o += up(T * (size_t)m.q_dim() * es);
     L.o = o; o += up(T * (size_t)m.q_dim() * es);
     L.u = o; o += up(T * (size_t)m.cfg.d_ff * es);
     L.inv_rms = o; o += up(T * 4);
     L.partials = o; o += up(n_partials * (size_t)m.group() * (m.cfg.head_dim + 2) * 4);
     L.split_slabs = o; o += m.cfg.dtype == ORTHRUS_BF16 ? up((size_t)kMaxSplits * T * d * 4) : 0;
+    L.rope_cs = o; o += m.cfg.dtype == ORTHRUS_BF16 ? up(T * (size_t)(m.cfg.head_dim / 2) * 8) : 0;
     L.total = o;
     return L;
 }
@@ -280,6 +282,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 
     // split-K slabs of the last residual-add projection, not yet added to x
     float *slabs = dt == ORTHRUS_BF16 ? (float *)(ws + L.split_slabs) : nullptr;
+    float2 *rope_cs = dt == ORTHRUS_BF16 ? (float2 *)(ws + L.rope_cs) : nullptr;
     const size_t slab_stride = (size_t)T * d;
     int pending = 0;
     auto norm = [&](bool gather, const Group &g, const float *gain) -> hipError_t {
@@ -296,6 +299,12 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         n.rows = g.r1 - g.r0;
         n.d = d;
         n.eps = c.rms_eps;
+        if (gather && rope_cs) {
+            n.cs = rope_cs + (size_t)g.r0 * (c.head_dim / 2);
+            n.pos = meta + p.off_pos + g.r0;
+            n.hd = c.head_dim;
+            n.rope_base = c.rope_base;
+        }
         return launch_rmsnorm(dt, gather, n, s);
     };
     auto gemm = [&](int epi, const Group &g, const char *A, int lda, const void *B0, const void *B1,
@@ -387,15 +396,50 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
             for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].attn_norm));
             pending = 0;
         }
-        for (int gi = 0; gi < n_groups; ++gi) {
-            const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-            RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d));
-        }
         ra.k_cache[0] = (char *)emb_kv->k_cache + l * e_stride;
         ra.v_cache[0] = (char *)emb_kv->v_cache + l * e_stride;
         ra.k_cache[1] = (char *)gen_kv->k_cache + l * g_stride;
         ra.v_cache[1] = (char *)gen_kv->v_cache + l * g_stride;
-        RUN("rope_append", launch_rope_append(dt, ra, s));
+        if (dt == ORTHRUS_BF16) {
+            // QKV projection with rotation and cache append in its epilogue
+            for (int gi = 0; gi < n_groups; ++gi) {
+                const Group &g = groups[gi];
+                GemmArgs ga{};
+                ga.A = act + (size_t)g.r0 * d * es;
+                ga.B0 = g.m->layers[l].w_qkv;
+                ga.M = g.r1 - g.r0;
+                ga.N = qkvd;
+                ga.K = d;
+                ga.lda = d;
+                ga.splits = 1;
+                QkvRope &q = ga.rope;
+                q.cs = rope_cs;
+                q.pos = ra.pos;
+                q.seq = ra.seq;
+                q.q_out = qb;
+                for (int i = 0; i < 2; ++i) {
+                    q.k_cache[i] = ra.k_cache[i];
+                    q.v_cache[i] = ra.v_cache[i];
+                    q.block_table[i] = ra.block_table[i];
+                    q.n_pages[i] = ra.n_pages[i];
+                    q.max_blocks[i] = ra.max_blocks[i];
+                }
+                q.row0 = g.r0;
+                q.Te = Te;
+                q.nq = c.n_q_heads;
+                q.nkv = c.n_kv_heads;
+                q.hd = c.head_dim;
+                q.page = c.page_size;
+                q.err = err;
+                RUN("gemm_qkv_rope", launch_gemm(dt, EPI_QKV_ROPE, ga, s));
+            }
+        } else {
+            for (int gi = 0; gi < n_groups; ++gi) {
+                const orthrus_layer_weights &lw = groups[gi].m->layers[l];
+                RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d));
+            }
+            RUN("rope_append", launch_rope_append(dt, ra, s));
+        }
         for (int i = 0; i < 2; ++i) {
             aa.k_cache[i] = ra.k_cache[i];
             aa.v_cache[i] = ra.v_cache[i];
