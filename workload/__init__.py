@@ -361,3 +361,169 @@ def tiny_mixed_scenario(seed: int = 1001, dtype: str = "f32", qk_std: Optional[f
         steps.append(Batch(chunks=chunks, rows=rows, token_ids=ids))
         ctx = [c + 1 for c in ctx]
     return cfg, weights, n_seq, steps
+
+
+# ---------------------------------------------------------------------------
+# larger-shape scenarios at reduced depth (7B-shape layers)
+# ---------------------------------------------------------------------------
+def _lognormal_lengths(rng, mean: float, n: int, sigma: float = 0.8, lo: int = 1, hi: int = 1 << 30):
+    """Integer lengths from a lognormal with the given mean, clipped to [lo, hi]."""
+    mu = np.log(mean) - 0.5 * sigma * sigma
+    return np.clip(np.rint(rng.lognormal(mu, sigma, size=n)), lo, hi).astype(np.int64)
+
+
+def retrieval_mix_scenario(seed: int = 1003, n_layers: int = 1, budget: int = 2048,
+                           fractions=(0.0, 0.25, 0.5, 0.75, 1.0), max_decode: int = 256):
+    """Two 7B-shape models (embedding: mean pooling, no LM head; generator: vocab 32000) and
+    one step per embedding fraction f of the token budget.
+
+    Each step brings fresh query requests (single final chunks, lengths lognormal with mean
+    64, the last one cut to fill f * budget exactly) and decode rows of the generation
+    requests: D = min(budget - T_e, max_decode) of them, the same requests step after step
+    (context + 1 per step they decode in), first contexts lognormal with mean 512.  Cached
+    generator keys/values are N(0, 1) in bf16.  Returns (cfg_e, W_e, cfg_g, W_g, paged_e,
+    paged_g, steps).
+    """
+    cfg_e = llm7b_config(n_layers=n_layers, has_lm_head=False)
+    cfg_g = llm7b_config(n_layers=n_layers)
+    W_e = make_weights(cfg_e, seed, model_tag=1)
+    W_g = make_weights(cfg_g, seed, model_tag=2)
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(92,)))
+    P = cfg_g.page_size
+    n_gen = max_decode
+    ctx0 = _lognormal_lengths(rng, 512, n_gen, lo=16, hi=4096 - len(fractions) - 1)
+    # queries of every step, and the decode participation
+    plan = []
+    q_total = 0
+    for f in fractions:
+        te = int(round(f * budget))
+        lens = []
+        while sum(lens) < te:
+            lens.append(int(_lognormal_lengths(rng, 64, 1, lo=1, hi=budget)[0]))
+        if lens:
+            lens[-1] -= sum(lens) - te
+            lens = [x for x in lens if x > 0]
+        plan.append((lens, min(budget - te, max_decode)))
+        q_total += len(lens)
+    n_seq_e = max(1, q_total)
+    pages_e = sum(-(-x // P) for lens, _ in plan for x in lens) + 8
+    max_blocks_e = budget // P + 1
+    paged_e = PagedKV(cfg_e, pages_e, n_seq_e, max_blocks_e, seed)
+    steps_total = len(fractions)
+    pages_g = int(sum(-(-(int(c) + steps_total + 1) // P) for c in ctx0)) + 8
+    max_blocks_g = 4096 // P + 1
+    paged_g = PagedKV(cfg_g, pages_g, n_gen, max_blocks_g, seed + 1)
+    for s, c in enumerate(ctx0):
+        paged_g.fill_random(s, int(c), seed)
+        paged_g.reserve(s, int(c) + steps_total + 1)
+    ctx = ctx0.copy()
+    steps: List[Batch] = []
+    q_seq = 0
+    for k, (lens, D) in enumerate(plan):
+        chunks = []
+        for x in lens:
+            paged_e.reserve(q_seq, x)
+            chunks.append(EmbChunk(seq=q_seq, offset=0, len=x, last=True, pool=POOL_MEAN))
+            q_seq += 1
+        rows = [DecodeRow(seq=s, ctx_len=int(ctx[s])) for s in range(D)]
+        ids = draw_tokens(seed, 100 + k, sum(lens) + D, cfg_e.vocab)
+        steps.append(Batch(chunks=chunks, rows=rows, token_ids=ids))
+        ctx[:D] += 1
+    return cfg_e, W_e, cfg_g, W_g, paged_e, paged_g, steps
+
+
+def long_document_scenario(seed: int = 1004, n_layers: int = 1, n_docs: int = 3, doc_len: int = 2048,
+                           chunk: int = 512, per_step: int = 3, n_dec: int = 32, ctx0: int = 2048):
+    """Long-document embedding on one 7B-shape model (mean pooling, vocab 32000 LM head).
+
+    ``n_docs`` documents of ``doc_len`` tokens are chunked by ``chunk`` and fed
+    ``per_step`` chunks per step (at most one per document: a request appears once per
+    batch), round-robin over the documents, next to ``n_dec``
+    decode rows starting at context ``ctx0`` (+1 per step).  Document keys/values are
+    written by the steps themselves; the decode requests' first ``ctx0`` positions are
+    N(0, 1) bf16.  Returns (cfg, W, paged, steps).
+    """
+    if per_step > n_docs:
+        raise ValueError("more chunks per step than documents")
+    cfg = llm7b_config(n_layers=n_layers)
+    W = make_weights(cfg, seed)
+    P = cfg.page_size
+    n_chunks = -(-doc_len // chunk)
+    order = [(d, c) for c in range(n_chunks) for d in range(n_docs)]   # round-robin
+    n_steps = -(-len(order) // per_step)
+    n_seq = n_docs + n_dec
+    pages = n_docs * (-(-doc_len // P)) + n_dec * (-(-(ctx0 + n_steps + 1) // P)) + 8
+    max_blocks = max(doc_len, ctx0 + n_steps + 1) // P + 1
+    paged = PagedKV(cfg, pages, n_seq, max_blocks, seed)
+    for d in range(n_docs):
+        paged.reserve(d, doc_len)
+    for j in range(n_dec):
+        paged.fill_random(n_docs + j, ctx0, seed)
+        paged.reserve(n_docs + j, ctx0 + n_steps + 1)
+    doc_tok = [draw_tokens(seed, 200 + d, doc_len, cfg.vocab) for d in range(n_docs)]
+    dec_tok = draw_tokens(seed, 300, n_steps * n_dec, cfg.vocab).reshape(n_steps, n_dec)
+    steps: List[Batch] = []
+    for k in range(n_steps):
+        part = order[k * per_step:(k + 1) * per_step]
+        chunks, ids = [], []
+        for d, c in part:
+            off = c * chunk
+            ln = min(chunk, doc_len - off)
+            chunks.append(EmbChunk(seq=d, offset=off, len=ln, last=off + ln == doc_len, pool=POOL_MEAN))
+            ids.append(doc_tok[d][off:off + ln])
+        rows = [DecodeRow(seq=n_docs + j, ctx_len=ctx0 + k) for j in range(n_dec)]
+        ids.append(dec_tok[k])
+        steps.append(Batch(chunks=chunks, rows=rows, token_ids=np.concatenate(ids).astype(np.int32)))
+    return cfg, W, paged, steps
+
+
+@dataclass
+class DeviceKVRecipe:
+    """Block table of a cache whose contents are drawn on the device (too large for a host image)."""
+    n_pages: int
+    n_seq: int
+    max_blocks: int
+    block_table: np.ndarray
+    seed: int
+
+
+def decode_heavy_scenario(seed: int = 1005, n_layers: int = 1, n_dec: int = 256, ctx_lo: int = 4096,
+                          ctx_hi: int = 8192, n_queries: int = 8, q_len: int = 16):
+    """Decode-heavy step on one 7B-shape generator (vocab 32000): ``n_dec`` decode rows with
+    contexts uniform in [ctx_lo, ctx_hi] plus ``n_queries`` short final chunks (mean
+    pooling).  Keys/values are N(0, 1) bf16 drawn on the device (``fill_device_pools``);
+    physical pages are a seeded permutation.  Returns (cfg, W, batch, recipe).
+    """
+    cfg = llm7b_config(n_layers=n_layers)
+    W = make_weights(cfg, seed)
+    P = cfg.page_size
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(93,)))
+    ctx = rng.integers(ctx_lo, ctx_hi, size=n_dec, endpoint=True)
+    n_seq = n_queries + n_dec
+    need = [-(-q_len // P)] * n_queries + [-(-(int(c) + 1) // P) for c in ctx]
+    n_pages = int(sum(need))
+    max_blocks = max(need)
+    perm = rng.permutation(n_pages).astype(np.int32)
+    bt = np.full((n_seq, max_blocks), -1, np.int32)
+    o = 0
+    for s, n in enumerate(need):
+        bt[s, :n] = perm[o:o + n]
+        o += n
+    chunks = [EmbChunk(seq=i, offset=0, len=q_len, last=True, pool=POOL_MEAN) for i in range(n_queries)]
+    rows = [DecodeRow(seq=n_queries + j, ctx_len=int(c)) for j, c in enumerate(ctx)]
+    ids = draw_tokens(seed, 400, n_queries * q_len + n_dec, cfg.vocab)
+    return cfg, W, Batch(chunks=chunks, rows=rows, token_ids=ids), DeviceKVRecipe(n_pages, n_seq, max_blocks, bt, seed)
+
+
+def fill_device_pools(k, v, seed: int) -> None:
+    """Fill device key/value pools with N(0, 1) values of their dtype from a seeded device
+    generator (torch tensors; values, not a method step)."""
+    import torch
+    g = torch.Generator(device=k.device)
+    g.manual_seed(seed)
+    for t in (k, v):
+        flat = t.view(-1)
+        step = 1 << 26
+        for i in range(0, flat.numel(), step):
+            part = flat[i:i + step]
+            part.copy_(torch.randn(part.numel(), generator=g, device=k.device, dtype=torch.float32).to(t.dtype))
