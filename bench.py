@@ -69,6 +69,7 @@ def algorithmic_work(cfg, batch):
     es = 2 if cfg.dtype == "bf16" else 4
     work = {
         "gemm_qkv": ("flop", 2.0 * T * d * qkv, L),
+        "gemm_qkv_rope": ("flop", 2.0 * T * d * qkv, L),   # bf16: rotation and cache append fused
         "gemm_o": ("flop", 2.0 * T * qd * d, L),
         "gemm_gate_up": ("flop", 2.0 * T * d * 2 * F, L),
         "gemm_down": ("flop", 2.0 * T * F * d, L),
@@ -90,7 +91,19 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="BLAS threads for the oracle (0 = all)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run three plain 1 GiB device copies (the reference kernel for scaling "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        x = torch.ones(256 * 1024 * 1024, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print("copied 1 GiB x3", flush=True)
+        return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the mixed step runs whole on a single MI355X "
               "(independent replicas per GPU; no collective in the method). Use --gpus 1.",
@@ -170,8 +183,8 @@ def main() -> int:
         roof = {"kernel": dom, "bound": "hbm", "achieved": dk.get("gbs"), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": dk.get("frac_hbm"), "traffic": None,
                 "algorithmic_per_launch": per_launch, "avg_launch_ms": dk["avg_ms"]}
-    gemm_names = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "lm_head"]
-    gemm_flop = sum(work[k][1] * work[k][2] for k in gemm_names)
+    gemm_names = ["gemm_qkv", "gemm_qkv_rope", "gemm_o", "gemm_gate_up", "gemm_down", "lm_head"]
+    gemm_flop = sum(work[k][1] * work[k][2] for k in gemm_names if k in prof)
     gemm_ms = sum(prof[k][1] for k in gemm_names if k in prof) / args.steps
     attn_ms = prof.get("attention", (0, 0.0))[1] / args.steps
     Te, T = batch.n_emb_tokens, batch.n_tokens
