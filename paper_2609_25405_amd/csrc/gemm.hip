@@ -44,7 +44,7 @@ constexpr int vmcnt_imm() {
 // global->LDS copies of later stages (their completion is awaited explicitly with vmcnt)
 __device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int BM, int BN, int WM, int WN, int EPI, int BKS, int STAGES>
+template <int BM, int BN, int WM, int WN, int EPI, int BKS, int STAGES, int BSTAGES>
 __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) {
     constexpr int NW = WM * WN;               // waves per workgroup
     constexpr int TM = BM / WM, TN = BN / WN;
@@ -56,15 +56,24 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     // global -> LDS copies of one K stage
     constexpr int A_INST = BM / (RPI * NW), B_INST = BN / (RPI * NW);
     constexpr int INST = A_INST + B_INST;     // copy instructions per wave per stage
-    constexpr int STAGE = (BM + BN) * ROWB;
     constexpr int KSTEPS = BKS / 16;
+    // separate rings for A (STAGES buffers of BM rows) and B (BSTAGES buffers of BN rows): the
+    // weight operand may prefetch deeper than the activations within the same LDS budget
+    constexpr int RING_BYTES = STAGES * BM * ROWB + BSTAGES * BN * ROWB;
+    // the shallower ring's copies are issued first in every iteration; vector-memory operations
+    // complete in order, so iteration kt may leave these many copies of this wave in flight when
+    // it waits for its stage kt (the deeper ring's copies issued after the shallower's stage kt)
+    constexpr int SD = STAGES < BSTAGES ? STAGES : BSTAGES, SDD = STAGES < BSTAGES ? BSTAGES : STAGES;
+    constexpr int DEEP_INST = STAGES < BSTAGES ? B_INST : A_INST;
+    constexpr int IN_FLIGHT = (SD - 2) * INST + (SDD > SD ? DEEP_INST : 0);
     static_assert(A_INST * RPI * NW == BM && B_INST * RPI * NW == BN, "copy split");
     static_assert(FM >= 1 && FN >= 1 && (EPI != EPI_SWIGLU || FN % 2 == 0), "tile shape");
-    static_assert(STAGES >= 2 && (STAGES - 2) * INST < 64, "pipeline depth");
+    static_assert(SD >= 2 && IN_FLIGHT < 64, "pipeline depth");
     // the QKV epilogue stages the fp32 tile (rows padded to 136 floats) and per-row metadata
     constexpr int CROW = 136;
     constexpr int EPI_BYTES = EPI == EPI_QKV_ROPE ? BM * CROW * 4 + BM * 16 : 0;
-    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE > EPI_BYTES ? STAGES * STAGE : EPI_BYTES];
+    __shared__ __attribute__((aligned(1024))) char smem[RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES];
+    char *const smem_b = smem + STAGES * BM * ROWB;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
@@ -111,12 +120,31 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
         }
         b_src[i] = src + (size_t)min(grow, a.N - 1) * ldb_b + chunk * 16;
     }
-    // copy j (< INST) of K stage kt into LDS buffer buf: A rows first, then B rows
-    auto copy = [&](int j, int kt, int buf) {
+    // this wave's copies of K stage kt of A (into A buffer buf) and of B (into B buffer buf)
+    auto copy_a = [&](int kt, int buf) {
         const size_t kb = (size_t)kt * ROWB;
-        char *s = smem + buf * STAGE;
-        if (j < A_INST) copy16_to_lds(a_src[j] + kb, s + (NW * j + wave) * 1024);
-        else copy16_to_lds(b_src[j - A_INST] + kb, s + BM * ROWB + (NW * (j - A_INST) + wave) * 1024);
+#pragma unroll
+        for (int j = 0; j < A_INST; ++j)
+            copy16_to_lds(a_src[j] + kb, smem + buf * BM * ROWB + (NW * j + wave) * 1024);
+    };
+    auto copy_b = [&](int kt, int buf) {
+        const size_t kb = (size_t)kt * ROWB;
+#pragma unroll
+        for (int j = 0; j < B_INST; ++j)
+            copy16_to_lds(b_src[j] + kb, smem_b + buf * BN * ROWB + (NW * j + wave) * 1024);
+    };
+    // iteration i's copies: A stage i + STAGES - 1 and B stage i + BSTAGES - 1 (the shallower
+    // ring first).  Past the last stage they repeat it into the buffer just freed, which nobody
+    // reads, so every iteration issues the same count and the wait bound stays exact.
+    auto issue = [&](int i, int kt0, int nk) {
+        const int sa = i + STAGES - 1, sb = i + BSTAGES - 1;
+        if (STAGES <= BSTAGES) {
+            if (sa >= 0) copy_a(kt0 + min(sa, nk - 1), sa % STAGES);
+            if (sb >= 0) copy_b(kt0 + min(sb, nk - 1), sb % BSTAGES);
+        } else {
+            if (sb >= 0) copy_b(kt0 + min(sb, nk - 1), sb % BSTAGES);
+            if (sa >= 0) copy_a(kt0 + min(sa, nk - 1), sa % STAGES);
+        }
     };
 
     f32x16 acc[FM][FN];
@@ -129,47 +157,39 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
 
     // fragment rows of this lane; the swizzle key is the same for every 32-row fragment of the
     // lane (32 rows span a whole number of 256-byte passes), so offsets differ by constants
-    const int arow = wm * TM + (lane & 31), brow = BM + wn * TN + (lane & 31);
-    const int akey = key_of(arow), bkey = key_of(brow);
+    // (B rows keep the swizzle key of row BM + r, as the copies above write them)
+    const int arow = wm * TM + (lane & 31), brow = wn * TN + (lane & 31);
+    const int akey = key_of(arow), bkey = key_of(BM + brow);
     bf16x8 fa[2][FM], fb[2][FN];
-    auto lds_frag = [&](const char *s, int kk, int buf) {
+    auto lds_frag = [&](const char *sa, const char *sb, int kk, int buf) {
         const int chk = kk * 2 + (lane >> 5);
 #pragma unroll
         for (int mi = 0; mi < FM; ++mi)
-            fa[buf][mi] = *(const bf16x8 *)(s + (arow + mi * 32) * ROWB + ((chk ^ akey) << 4));
+            fa[buf][mi] = *(const bf16x8 *)(sa + (arow + mi * 32) * ROWB + ((chk ^ akey) << 4));
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni)
-            fb[buf][ni] = *(const bf16x8 *)(s + (brow + ni * 32) * ROWB + ((chk ^ bkey) << 4));
+            fb[buf][ni] = *(const bf16x8 *)(sb + (brow + ni * 32) * ROWB + ((chk ^ bkey) << 4));
     };
 
-    // STAGES-deep ring of LDS stages: the copies of stage kt + STAGES - 1 are issued while stage
-    // kt is computed.  Iteration kt: wait for this wave's copies of stage kt (later stages stay
-    // in flight), barrier (everyone's copies landed; everyone finished reading the buffer about
-    // to be refilled), issue the next stage's copies, then the MFMAs of stage kt with the next
-    // k-step's fragments read under the current k-step's.  (Spreading the copies between the
-    // MFMAs, or adding L2 prefetches a few stages ahead, measured slower on MI355X.)
+    // Rings of LDS stages: the copies of A stage kt + STAGES - 1 and B stage kt + BSTAGES - 1
+    // are issued while stage kt is computed.  Iteration kt: wait for this wave's copies of
+    // stage kt (later ones stay in flight), barrier (everyone's copies landed; everyone
+    // finished reading the buffers about to be refilled), issue, then the MFMAs of stage kt
+    // with the next k-step's fragments read under the current k-step's.  (Spreading the copies
+    // between the MFMAs, or L2 prefetches further ahead, measured slower on MI355X.)
     constexpr int NMF = FM * FN, NFR = FM + FN;
     const int nk = a.K / BKS / splits;
     const int kt0 = split * nk;
-#pragma unroll
-    for (int p = 0; p < STAGES - 1; ++p)
-        if (p < nk) {
-#pragma unroll
-            for (int j = 0; j < INST; ++j) copy(j, kt0 + p, p);
-        }
+    for (int i = -(SDD - 1); i < 0; ++i) issue(i, kt0, nk);
     for (int kt = 0; kt < nk; ++kt) {
-        if (kt + STAGES - 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm<(STAGES - 2) * INST>());
-        else __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm<IN_FLIGHT>());
         ring_barrier();
-        if (kt + STAGES - 1 < nk) {
-#pragma unroll
-            for (int j = 0; j < INST; ++j) copy(j, kt0 + kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-        }
-        const char *s = smem + (kt % STAGES) * STAGE;
-        lds_frag(s, 0, 0);
+        issue(kt, kt0, nk);
+        const char *sa = smem + (kt % STAGES) * BM * ROWB, *sb = smem_b + (kt % BSTAGES) * BN * ROWB;
+        lds_frag(sa, sb, 0, 0);
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) {
-            if (kk + 1 < KSTEPS) lds_frag(s, kk + 1, (kk + 1) & 1);
+            if (kk + 1 < KSTEPS) lds_frag(sa, sb, kk + 1, (kk + 1) & 1);
 #pragma unroll
             for (int mi = 0; mi < FM; ++mi)
 #pragma unroll
@@ -188,6 +208,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
             }
         }
     }
+    // the repeated copies of the last iterations still write LDS: drain them before the
+    // epilogues reuse the stage buffers
+    __builtin_amdgcn_s_waitcnt(0);
 
     if constexpr (EPI == EPI_QKV_ROPE) {
         // Rotation of q and k at each token's position (pairs (i, i + hd/2)), q stored for
@@ -289,7 +312,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
         // idle stage buffers and written back as whole 16-byte pieces of its rows.
         constexpr int OC = BN / 2;                 // output columns of the tile
         constexpr int OROW = OC * 2 + 16;          // padded LDS row: rows 4 apart differ by 16 banks
-        static_assert(BM * OROW <= STAGES * STAGE, "output tile fits the stage buffers");
+        static_assert(BM * OROW <= RING_BYTES, "output tile fits the stage buffers");
         __syncthreads();                           // every wave is done with the stage buffers
 #pragma unroll
         for (int mi = 0; mi < FM; ++mi)
@@ -408,14 +431,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, int BKS = 64, int STAGES = 2>
+template <int BM, int BN, int WM, int WN, int EPI, int BKS = 64, int STAGES = 2, int BSTAGES = STAGES>
 hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
     const int mt = (a.M + BM - 1) / BM;
     const int cols = EPI == EPI_SWIGLU ? BN / 2 : BN;
     const int nt = (a.N + cols - 1) / cols;
     const int splits =
         (EPI == EPI_ADD_F32 && a.partial && a.splits > 1 && a.K % (a.splits * BK) == 0) ? a.splits : 1;
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, BKS, STAGES>), dim3(mt * nt * splits),
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, BKS, STAGES, BSTAGES>), dim3(mt * nt * splits),
                        dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
 }
