@@ -10,10 +10,11 @@ baseline leg of the benchmark; the product path never imports it.
   for every request type), single-pass pooling heads (Section 3.3) and the
   next-token logits of a generation request recomputed from its whole prefix.
 * ``oracle.step`` -- the same arithmetic under the step's contract: a
-  type-sorted batch of embedding chunks and decode tokens (Section 3.2) that
-  reads and appends a paged KV cache, updates the per-request pooling state by
-  Eq. (1)-(2) and the positional heads, and finishes embeddings after a
-  request's final chunk.
+  type-sorted batch of embedding chunks, generation prefill chunks and decode
+  tokens (Section 3.2) that reads and appends a paged KV cache, updates the
+  per-request pooling state by Eq. (1)-(2) and the positional heads, finishes
+  embeddings after a request's final chunk, and emits next-token logits for
+  the last row of a prompt's final chunk and for every decode token.
 
 Where the paper leaves a detail open (the model family's normalisation, RoPE
 variant, grouping of query heads, the L2 normalisation of finished embeddings,
@@ -24,9 +25,9 @@ generators in ``workload`` feed both.
 """
 from .model import (rmsnorm, rope_rotate, causal_gqa_attention, silu, forward_full,
                     pool_single_pass, l2_normalize, embed_single_pass, decode_full_recompute,
-                    lm_logits)
+                    lm_logits, greedy_token)
 from .step import OracleKV, StepError, step_oracle
 
 __all__ = ["rmsnorm", "rope_rotate", "causal_gqa_attention", "silu", "forward_full",
            "pool_single_pass", "l2_normalize", "embed_single_pass", "decode_full_recompute",
-           "lm_logits", "OracleKV", "StepError", "step_oracle"]
+           "lm_logits", "greedy_token", "OracleKV", "StepError", "step_oracle"]

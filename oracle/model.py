@@ -151,3 +151,10 @@ def decode_full_recompute(cfg, weights, ids) -> np.ndarray:
     """Next-token logits after tokens ids, recomputed from the whole prefix without a cache."""
     H = forward_full(cfg, weights, ids)
     return lm_logits(weights, H[-1])
+
+
+def greedy_token(logits: np.ndarray) -> np.ndarray:
+    """Greedy sampling (the sampler of Algorithm 1 at temperature 0): the index of each row's
+    largest logit, the lowest index among equal maxima (the paper fixes no tie-break)."""
+    logits = np.asarray(logits, F64)
+    return np.argmax(logits, axis=-1).astype(np.int64)

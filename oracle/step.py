@@ -2,9 +2,10 @@
 
 One call is the body of the paper's heterogeneous-batching loop (Algorithm 1)
 without the scheduler and the sampler: a forward over a type-sorted batch of
-embedding chunks and decode tokens (Section 3.2), then the incremental pooler
-on the embedding slice (Section 3.3, Eq. (1)-(2) and the positional heads) and
-the LM head on the decode slice.
+embedding chunks, generation prefill chunks and decode tokens (Section 3.2),
+then the incremental pooler on the embedding slice (Section 3.3, Eq. (1)-(2) and
+the positional heads) and the LM head on the last row of every prompt's final
+chunk and on every decode token (the rows the sampler reads).
 
 Requests never attend to each other, so the oracle runs them one at a time, in
 batch order, each through every layer: for a chunk the rows are the positions
@@ -27,7 +28,12 @@ Readings taken where the paper is silent (also listed in the design notes):
   final chunk stores its last row.  CLS: the offset-0 chunk stores its first
   row.  Every pooled chunk adds len to W so the offset check holds for all heads;
 * a finished embedding (chunk flagged last) is v / max(||v||_2, 1e-12);
-* pooling kind "none" writes keys/values only (a cache-filling prefill chunk).
+* pooling kind "none" writes keys/values only (a cache-filling prefill chunk);
+* a generation prefill chunk (seq, offset, len, last) runs through the generator
+  and its cache like a decode row of ``len`` tokens at positions offset ..
+  offset+len-1; only the final chunk of a prompt (last) emits logits, for its
+  last row.  Logits rows are those rows in chunk order, then the decode rows;
+  prompt chunks and decode rows share the generator's sequence namespace.
 """
 from __future__ import annotations
 
@@ -103,8 +109,10 @@ def _forward_cached(cfg, weights, kv: OracleKV, seq: int, ids: np.ndarray,
 def validate(emb, gen, batch, emb_kv: OracleKV, gen_kv: OracleKV) -> None:
     """Host-side contract checks: raise StepError(desc | dupseq | capacity)."""
     emb_cfg, gen_cfg = emb[0], gen[0]
+    gen_chunks = list(getattr(batch, "gen_chunks", []) or [])
     n_emb = sum(int(c.len) for c in batch.chunks)
-    T = n_emb + len(batch.rows)
+    n_gen = sum(int(c.len) for c in gen_chunks)
+    T = n_emb + n_gen + len(batch.rows)
     ids = np.asarray(batch.token_ids)
     if ids.shape != (T,):
         raise StepError("desc", f"token_ids has {ids.size} entries, batch needs {T}")
@@ -120,6 +128,15 @@ def validate(emb, gen, batch, emb_kv: OracleKV, gen_kv: OracleKV) -> None:
         if ("e", c.seq) in seen:
             raise StepError("dupseq", f"seq {c.seq} twice")
         seen.add(("e", c.seq))
+    for c in gen_chunks:
+        if not (0 <= c.seq < gen_kv.n_seq) or c.offset < 0 or c.len < 1:
+            raise StepError("desc", f"bad prompt chunk {c}")
+        if c.offset + c.len > gen_kv.max_blocks * gen_kv.page:
+            raise StepError("capacity", f"prompt chunk {c} exceeds the block table")
+        key = ("e" if shared else "g", c.seq)
+        if key in seen:
+            raise StepError("dupseq", f"seq {c.seq} twice")
+        seen.add(key)
     for r in batch.rows:
         if not (0 <= r.seq < gen_kv.n_seq) or r.ctx_len < 0:
             raise StepError("desc", f"bad decode row {r}")
@@ -129,12 +146,12 @@ def validate(emb, gen, batch, emb_kv: OracleKV, gen_kv: OracleKV) -> None:
         if key in seen:
             raise StepError("dupseq", f"seq {r.seq} twice")
         seen.add(key)
-    if batch.rows and gen[1].get("lm_head") is None:
-        raise StepError("desc", "decode rows need a model with an LM head")
+    if (batch.rows or any(c.last for c in gen_chunks)) and gen[1].get("lm_head") is None:
+        raise StepError("desc", "logits need a model with an LM head")
     if n_emb and ((ids[:n_emb] < 0).any() or (ids[:n_emb] >= emb_cfg.vocab).any()):
         raise StepError("desc", "chunk token id out of range")
-    if batch.rows and ((ids[n_emb:] < 0).any() or (ids[n_emb:] >= gen_cfg.vocab).any()):
-        raise StepError("desc", "decode token id out of range")
+    if T > n_emb and ((ids[n_emb:] < 0).any() or (ids[n_emb:] >= gen_cfg.vocab).any()):
+        raise StepError("desc", "generation token id out of range")
 
 
 def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleKV,
@@ -142,8 +159,8 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
     """Run one mixed step.  ``emb`` and ``gen`` are (cfg, weights); they may be the same model.
 
     ``emb_kv`` / ``gen_kv`` are updated in place (the step appends keys and values).
-    Returns float64 ``logits``[n_decode, vocab], ``out_emb``[n_chunks, d] (NaN rows for
-    chunks not flagged last) and the updated ``acc_sum``[n_seq, d], ``acc_w``[n_seq].
+    Returns float64 ``logits``[n_last_prompt_chunks + n_decode, vocab], ``out_emb``[n_chunks, d]
+    (NaN rows for chunks not flagged last) and the updated ``acc_sum``[n_seq, d], ``acc_w``[n_seq].
     """
     validate(emb, gen, batch, emb_kv, gen_kv)
     emb_cfg, emb_w = emb
@@ -176,9 +193,20 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
         if c.last:
             v = S[c.seq] / W[c.seq] if c.pool == "mean" else S[c.seq]
             out_emb[i] = l2_normalize(v)
-    logits = np.zeros((len(batch.rows), gen_cfg.vocab if batch.rows else 0), F64)
-    for j, r in enumerate(batch.rows):
+    gen_chunks = list(getattr(batch, "gen_chunks", []) or [])
+    n_logits = sum(1 for c in gen_chunks if c.last) + len(batch.rows)
+    logits = np.zeros((n_logits, gen_cfg.vocab if n_logits else 0), F64)
+    j = 0
+    for c in gen_chunks:
+        pos = np.arange(c.offset, c.offset + c.len)
+        H = _forward_cached(gen_cfg, gen_w, gen_kv, c.seq, ids[t:t + c.len], pos)
+        t += c.len
+        if c.last:
+            logits[j] = lm_logits(gen_w, H[-1])
+            j += 1
+    for r in batch.rows:
         H = _forward_cached(gen_cfg, gen_w, gen_kv, r.seq, ids[t:t + 1], np.array([r.ctx_len]))
         t += 1
         logits[j] = lm_logits(gen_w, H[0])
+        j += 1
     return {"logits": logits, "out_emb": out_emb, "acc_sum": S, "acc_w": W}

@@ -167,3 +167,27 @@ def test_device_errors_are_flagged_not_faulted():
     kv.set_block_table(bt)
     R.step(dm, dm, Batch([], [DecodeRow(1, 3)], ids[:1]), kv, kv, S, Wc, lg, None, ws)
     assert ws.device_error() == 1
+
+
+def test_step_is_bitwise_deterministic():
+    """Two runs of the same 7B-layer step on the same inputs give identical bits (split-K slabs,
+    decode partials and pooling all reduce in a fixed order; no float atomics)."""
+    wl = layer7b_mixed_workload()
+    cfg, b = wl.cfg, wl.batch
+    dm = R.DeviceModel(cfg, wl.weights)
+    kv = R.DeviceKV.from_paged(wl.kv)
+    ws = R.Workspace(dm, dm, b.n_tokens, len(b.chunks), len(b.rows), 4096)
+    outs = []
+    for _ in range(2):
+        S = torch.tensor(wl.acc_sum, device="cuda")
+        Wc = torch.tensor(wl.acc_w, device="cuda")
+        logits = torch.empty((len(b.rows), cfg.vocab), device="cuda")
+        emb = torch.full((len(b.chunks), cfg.d_model), float("nan"), device="cuda")
+        R.step(dm, dm, b, kv, kv, S, Wc, logits, emb, ws)
+        torch.cuda.synchronize()
+        assert ws.device_error() == 0
+        outs.append((logits.cpu(), emb.cpu(), S.cpu(), Wc.cpu(), kv.k.view(torch.int16).clone(),
+                     kv.v.view(torch.int16).clone()))
+    for a, c in zip(*outs):
+        assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
+                           c.view(torch.int32) if c.dtype == torch.float32 else c)

@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 from oracle import OracleKV, StepError, step_oracle
-from workload import (Batch, DecodeRow, EmbChunk, ModelConfig, PagedKV, draw_tokens,
+from workload import (Batch, DecodeRow, EmbChunk, GenChunk, ModelConfig, PagedKV, draw_tokens,
                       make_weights, tiny_config)
 from tests import bruteforce
 
@@ -390,3 +390,112 @@ def test_contract_errors():
     bad = ids.copy()
     bad[0] = cfg.vocab
     assert kind(Batch([EmbChunk(0, 0, 8, False)], [], bad)) == "desc"
+
+
+# ---------------------------------------------------------------------------
+# generation prefill chunks (the batch unit's third item type) and greedy sampling
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("C", [1, 7, 16, 21])
+@pytest.mark.parametrize("nkv", [4, 2])
+def test_prompt_chunks_then_greedy_decode_equal_recompute(C, nkv):
+    """A prompt fed as generation prefill chunks of C tokens gives, on its final chunk, the
+    next-token logits of the whole prompt recomputed without a cache; greedy decoding through
+    the cache then matches full recompute of prompt + generated tokens at every step."""
+    cfg = micro_config(n_kv_heads=nkv)
+    W = sharp_weights(cfg, 61)
+    prompt = draw_tokens(9, 0, 21, cfg.vocab)
+    pk = _fresh_kv(cfg, 2, 40, 3)
+    pk.reserve(1, 40)
+    kv = OracleKV.from_paged(pk)
+    S, Wc = np.zeros((2, cfg.d_model)), np.zeros(2)
+    for off in range(0, len(prompt), C):
+        ln = min(C, len(prompt) - off)
+        last = off + ln == len(prompt)
+        b = Batch(token_ids=prompt[off:off + ln], gen_chunks=[GenChunk(1, off, ln, last)])
+        r = step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        assert r["logits"].shape == ((1, cfg.vocab) if last else (0, 0))
+        np.testing.assert_array_equal(r["acc_w"], Wc)   # prompts touch no pooling state
+    seqs = list(prompt)
+    np.testing.assert_allclose(r["logits"][0], oracle.decode_full_recompute(cfg, W, np.array(seqs)),
+                               rtol=1e-11, atol=1e-13)
+    tok = int(oracle.greedy_token(r["logits"])[0])
+    for _ in range(3):
+        b = Batch(rows=[DecodeRow(1, len(seqs))], token_ids=np.array([tok], np.int32))
+        r = step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        seqs.append(tok)
+        np.testing.assert_allclose(r["logits"][0], oracle.decode_full_recompute(cfg, W, np.array(seqs)),
+                                   rtol=1e-11, atol=1e-13)
+        tok = int(oracle.greedy_token(r["logits"])[0])
+
+
+def test_three_item_types_equal_each_request_alone():
+    """Embedding chunks, prompt chunks and decode rows in one batch give the outputs each
+    request gives alone; logits rows are the final prompt chunks' last rows (in order), then
+    the decode rows."""
+    cfg = micro_config()
+    W = sharp_weights(cfg, 71)
+    toks = {s: draw_tokens(10, s, 30, cfg.vocab) for s in range(6)}
+
+    def setup():
+        pk = _fresh_kv(cfg, 6, 64, 4)
+        for s in range(6):
+            pk.reserve(s, 40)
+        kv = OracleKV.from_paged(pk)
+        for s in (4, 5):     # generation requests with a cached prompt, now decoding
+            b = Batch([EmbChunk(s, 0, 12, False, "none")], [], toks[s][:12])
+            step_oracle((cfg, W), (cfg, W), b, kv, kv, np.zeros((6, cfg.d_model)), np.zeros(6))
+        return kv, np.zeros((6, cfg.d_model)), np.zeros(6)
+
+    chunks = [EmbChunk(0, 0, 8, True, "mean")]
+    gens = [GenChunk(2, 0, 9, True), GenChunk(3, 0, 6, False)]
+    rows = [DecodeRow(4, 12), DecodeRow(5, 12)]
+    ids = [toks[0][:8], toks[2][:9], toks[3][:6], toks[4][12:13], toks[5][12:13]]
+    kv, S, Wc = setup()
+    mixed = step_oracle((cfg, W), (cfg, W), Batch(chunks, rows, np.concatenate(ids), gens),
+                        kv, kv, S, Wc)
+    assert mixed["logits"].shape == (3, cfg.vocab)
+    kv1, S1, W1 = setup()
+    alone = [step_oracle((cfg, W), (cfg, W), Batch(chunks, [], ids[0]), kv1, kv1, S1, W1),
+             step_oracle((cfg, W), (cfg, W), Batch(token_ids=ids[1], gen_chunks=[gens[0]]), kv1, kv1, S1, W1),
+             step_oracle((cfg, W), (cfg, W), Batch(token_ids=ids[2], gen_chunks=[gens[1]]), kv1, kv1, S1, W1),
+             step_oracle((cfg, W), (cfg, W), Batch([], [rows[0]], ids[3]), kv1, kv1, S1, W1),
+             step_oracle((cfg, W), (cfg, W), Batch([], [rows[1]], ids[4]), kv1, kv1, S1, W1)]
+    np.testing.assert_allclose(mixed["out_emb"][0], alone[0]["out_emb"][0], rtol=1e-13)
+    assert alone[2]["logits"].shape[0] == 0
+    for j, k in enumerate((1, 3, 4)):
+        np.testing.assert_allclose(mixed["logits"][j], alone[k]["logits"][0], rtol=1e-12)
+    np.testing.assert_array_equal(kv.k, kv1.k)
+
+
+def test_prompt_chunk_contract_errors():
+    cfg = micro_config()
+    W = sharp_weights(cfg, 81)
+    pk = _fresh_kv(cfg, 4, 32, 5)
+    for s in range(4):
+        pk.reserve(s, 32)
+    kv = OracleKV.from_paged(pk)
+    z = (np.zeros((4, cfg.d_model)), np.zeros(4))
+    ids = draw_tokens(11, 0, 40, cfg.vocab)
+    bad = [
+        (Batch([], [DecodeRow(1, 3)], ids[:5], [GenChunk(1, 0, 4, False)]), "dupseq"),   # prompt + decode, one seq
+        (Batch([EmbChunk(2, 0, 4, False)], [], ids[:8], [GenChunk(2, 0, 4, False)]), "dupseq"),  # shared cache
+        (Batch(token_ids=ids[:4], gen_chunks=[GenChunk(1, 30, 4, True)]), "capacity"),
+        (Batch(token_ids=ids[:4], gen_chunks=[GenChunk(4, 0, 4, True)]), "desc"),      # seq out of range
+        (Batch(token_ids=ids[:0], gen_chunks=[GenChunk(1, 0, 0, True)]), "desc"),      # empty chunk
+        (Batch(token_ids=ids[:3], gen_chunks=[GenChunk(1, 0, 4, True)]), "desc"),      # token count
+    ]
+    for b, kind in bad:
+        with pytest.raises(StepError) as e:
+            step_oracle((cfg, W), (cfg, W), b, kv, kv, *z)
+        assert e.value.kind == kind, (b, e.value.kind)
+    nohead = cfg.replace(has_lm_head=False)
+    Wn = make_weights(nohead, 81)
+    with pytest.raises(StepError) as e:
+        step_oracle((nohead, Wn), (nohead, Wn), Batch(token_ids=ids[:4], gen_chunks=[GenChunk(1, 0, 4, True)]),
+                    kv, kv, *z)
+    assert e.value.kind == "desc"
+
+
+def test_greedy_token_takes_the_lowest_index_on_ties():
+    logits = np.array([[0.5, 2.0, 2.0, -1.0], [3.0, 3.0, 3.0, 3.0], [-np.inf, -5.0, -7.0, -5.0]])
+    np.testing.assert_array_equal(oracle.greedy_token(logits), [1, 0, 1])

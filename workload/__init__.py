@@ -180,23 +180,41 @@ class DecodeRow:
 
 
 @dataclass
-class Batch:
-    """One step: embedding chunks first, then decode rows (type-sorted batch unit).
+class GenChunk:
+    """A segment of a generation request's prompt; the final one (last) yields logits."""
+    seq: int
+    offset: int
+    len: int
+    last: bool
 
-    ``token_ids`` holds every chunk's tokens in chunk order, then one input token
-    per decode row.
+
+@dataclass
+class Batch:
+    """One step, type-sorted: embedding chunks, generation prefill chunks, decode rows.
+
+    ``token_ids`` holds every embedding chunk's tokens in chunk order, then every prompt
+    chunk's tokens, then one input token per decode row.
     """
     chunks: List[EmbChunk] = field(default_factory=list)
     rows: List[DecodeRow] = field(default_factory=list)
     token_ids: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int32))
+    gen_chunks: List[GenChunk] = field(default_factory=list)
 
     @property
     def n_emb_tokens(self) -> int:
         return int(sum(c.len for c in self.chunks))
 
     @property
+    def n_gen_tokens(self) -> int:
+        return int(sum(c.len for c in self.gen_chunks))
+
+    @property
+    def n_logit_rows(self) -> int:
+        return int(sum(1 for c in self.gen_chunks if c.last)) + len(self.rows)
+
+    @property
     def n_tokens(self) -> int:
-        return self.n_emb_tokens + len(self.rows)
+        return self.n_emb_tokens + self.n_gen_tokens + len(self.rows)
 
 
 # ---------------------------------------------------------------------------
@@ -366,8 +384,9 @@ def tiny_mixed_scenario(seed: int = 1001, dtype: str = "f32", qk_std: Optional[f
 # ---------------------------------------------------------------------------
 # larger-shape scenarios at reduced depth (7B-shape layers)
 # ---------------------------------------------------------------------------
-def _lognormal_lengths(rng, mean: float, n: int, sigma: float = 0.8, lo: int = 1, hi: int = 1 << 30):
-    """Integer lengths from a lognormal with the given mean, clipped to [lo, hi]."""
+def _lognormal_lengths(rng, mean: float, n: int, sigma: float = 0.6, lo: int = 1, hi: int = 1 << 30):
+    """Integer lengths from a lognormal with the given mean (sigma in log space, mu = ln(mean) -
+    sigma^2 / 2), rounded and clipped to [lo, hi]."""
     mu = np.log(mean) - 0.5 * sigma * sigma
     return np.clip(np.rint(rng.lognormal(mu, sigma, size=n)), lo, hi).astype(np.int64)
 
@@ -391,7 +410,7 @@ def retrieval_mix_scenario(seed: int = 1003, n_layers: int = 1, budget: int = 20
     rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(92,)))
     P = cfg_g.page_size
     n_gen = max_decode
-    ctx0 = _lognormal_lengths(rng, 512, n_gen, lo=16, hi=4096 - len(fractions) - 1)
+    ctx0 = _lognormal_lengths(rng, 512, n_gen, lo=16, hi=4096 - len(fractions) - 1)   # documents
     # queries of every step, and the decode participation
     plan = []
     q_total = 0
@@ -399,7 +418,7 @@ def retrieval_mix_scenario(seed: int = 1003, n_layers: int = 1, budget: int = 20
         te = int(round(f * budget))
         lens = []
         while sum(lens) < te:
-            lens.append(int(_lognormal_lengths(rng, 64, 1, lo=1, hi=budget)[0]))
+            lens.append(int(_lognormal_lengths(rng, 64, 1, lo=1, hi=budget)[0]))        # queries
         if lens:
             lens[-1] -= sum(lens) - te
             lens = [x for x in lens if x > 0]
