@@ -1,11 +1,12 @@
 /*
- * orthrus.h -- C ABI of the mixed embedding-chunk + decode step on one MI355X (gfx950).
+ * orthrus.h -- C ABI of the mixed embedding + generation step on one MI355X (gfx950).
  *
  * One call of orthrus_step() is the body of the heterogeneous-batching inference loop
  * (Algorithm 1) minus scheduling and sampling: a single forward pass over a type-sorted
- * batch holding embedding chunks and generation decode tokens (Section 3.2, "Batch
- * Unit"), followed by the incremental pooler on the embedding slice (Section 3.3,
- * Eq. (1)-(2) and the positional heads) and the LM head on the decode slice.  Every
+ * batch holding embedding chunks, generation prefill chunks and generation decode tokens
+ * (Section 3.2, "Batch Unit"), followed by the incremental pooler on the embedding slice
+ * (Section 3.3, Eq. (1)-(2) and the positional heads) and the LM head on the rows that need
+ * next-token logits.  orthrus_sample_greedy() is the sampler on those logits.  Every
  * request type shares the same attention and feed-forward layers (Section 3.1).
  *
  * Model family: pre-norm decoder with RMSNorm, rotary position embedding (half-split
@@ -105,13 +106,24 @@ typedef struct orthrus_decode_row {
     int32_t seq, ctx_len;
 } orthrus_decode_row;
 
-/* The batch (HOST memory).  token_ids holds sum(len) chunk tokens in chunk order, then one
- * input token per decode row: the type-sorted layout of Section 3.2. */
+/* One generation prefill chunk: prompt tokens at positions [offset, offset + len) of generation
+ * request `seq`, run through the generator and appended to its cache like `len` decode tokens
+ * (the prompt-processing item of the Section 3.2 batch unit).  flags: ORTHRUS_CHUNK_LAST marks
+ * the prompt's final chunk, whose last row gets next-token logits; no other bit may be set. */
+typedef struct orthrus_gen_chunk {
+    int32_t seq, offset, len, flags;
+} orthrus_gen_chunk;
+
+/* The batch (HOST memory), type-sorted as in Section 3.2: token_ids holds the embedding chunks'
+ * tokens in chunk order, then the generation prefill chunks' tokens in chunk order, then one
+ * input token per decode row.  n_gen_chunks / gen_chunks may be 0 / NULL. */
 typedef struct orthrus_batch {
     int32_t n_chunks, n_decode;
     const orthrus_emb_chunk *chunks;
     const orthrus_decode_row *rows;
     const int32_t *token_ids;
+    int32_t n_gen_chunks;
+    const orthrus_gen_chunk *gen_chunks;
 } orthrus_batch;
 
 /* A paged KV cache (device), model dtype.  k_cache: [n_layers][n_pages][n_kv_heads][page][hd]
@@ -131,21 +143,26 @@ typedef struct orthrus_kv {
 int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, orthrus_model **out);
 void orthrus_model_destroy(orthrus_model *m);
 
-/* Device workspace bytes for steps of at most max_tokens tokens (chunks + decode rows), at
- * most max_chunks chunks, at most max_decode decode rows, and decode contexts of at most
- * max_ctx tokens.  `gen` may equal `emb`.  Returns 0 for invalid arguments. */
+/* Device workspace bytes for steps of at most max_tokens tokens (all chunk tokens + decode
+ * rows), at most max_chunks chunks (embedding plus generation prefill), at most max_decode
+ * decode rows, and decode contexts of at most max_ctx tokens.  `gen` may equal `emb`.  Returns 0
+ * for invalid arguments. */
 size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *gen, int32_t max_tokens,
                                int32_t max_chunks, int32_t max_decode, int32_t max_ctx);
 
 /* One mixed step, enqueued on `stream` (a hipStream_t; NULL = default stream); returns after
- * enqueueing.  Embedding chunks run through `emb` and read/append `emb_kv`; decode rows run
- * through `gen` (needs an LM head) and read/append `gen_kv`.  `gen` may equal `emb` (shared
- * backbone) and `gen_kv` may equal `emb_kv`; two distinct models must have equal configs.
+ * enqueueing.  Embedding chunks run through `emb` and read/append `emb_kv`; generation prefill
+ * chunks and decode rows run through `gen` (needs an LM head when any row gets logits) and
+ * read/append `gen_kv`.  `gen` may equal `emb` (shared backbone) and `gen_kv` may equal
+ * `emb_kv` (then all three item types share one sequence namespace); two distinct models must
+ * have equal configs.
  *   acc_sum  [emb_kv->n_seq][d] fp32 device, acc_w [emb_kv->n_seq] fp32 device: pooling state S,
  *            W of Eq. (1)-(2) per embedding request, updated in place.  A chunk at offset 0
  *            resets its request's state; a later chunk requires W == offset (else device error
  *            ORTHRUS_DEVERR_ACC and the chunk's pooling update is skipped).
- *   out_logits [n_decode][vocab] fp32 device: next-token logits of each decode row.
+ *   out_logits [n_logit_rows][vocab] fp32 device, n_logit_rows = (generation chunks flagged
+ *            LAST) + n_decode: next-token logits of the last row of each final prompt chunk, in
+ *            chunk order, then of each decode row.  May be NULL when n_logit_rows is 0.
  *   out_emb  [n_chunks][d] fp32 device: row i is written only if chunk i has ORTHRUS_CHUNK_LAST;
  *            it holds v / max(||v||_2, 1e-12) with v = S / W (mean) or S (last, CLS).
  *   workspace: device buffer of ws_bytes >= orthrus_workspace_bytes(...) for this batch.
@@ -154,6 +171,15 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
 int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
                  float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream);
+
+/* Greedy sampling (the sampler of Algorithm 1): out_tokens[r] = argmax over v of
+ * logits[r * vocab + v] for r < rows, enqueued on `stream`.  Ties go to the lowest index; a NaN
+ * counts as larger than every number (the first NaN wins), so the result equals a first-maximum
+ * argmax in which NaN compares greatest.  logits: fp32 device [rows][vocab]; out_tokens: int32
+ * device [rows].  EINVAL for rows < 0, vocab < 1, or a null pointer with rows > 0; rows == 0
+ * is otherwise a no-op.  Launch failures return EHIP. */
+int orthrus_sample_greedy(const float *logits, int32_t rows, int32_t vocab, int32_t *out_tokens,
+                          void *stream);
 
 /* Zeroes the device error word at the start of `workspace` (enqueued on `stream`).  Call once
  * on a freshly allocated workspace before its first step. */
@@ -164,11 +190,12 @@ int orthrus_workspace_init(void *workspace, void *stream);
 int orthrus_device_error(void *workspace, void *stream, int32_t *bits);
 
 /* Host-side plan of a batch without touching the GPU (for inspection and tests).  Counts the
- * attention work items the step would launch: n_prefill_items (query tiles of embedding
- * chunks), n_decode_items (key-range splits of decode rows, one per KV head and split).  If
- * `items` is non-NULL it receives up to `cap` items of 8 int32 each:
+ * attention work items the step would launch: n_prefill_items (query tiles of embedding and
+ * generation prefill chunks), n_decode_items (key-range splits of decode rows, one per KV head
+ * and split).  If `items` is non-NULL it receives up to `cap` items of 8 int32 each:
  *   {kind (0 prefill, 1 decode), chunk or row index, kv head, q_begin or split index,
- *    q_count or n_splits, key_begin, key_end (exclusive), partial slot or -1}. */
+ *    q_count or n_splits, key_begin, key_end (exclusive), partial slot or -1}.
+ * Chunk indices count the embedding chunks first, then the generation prefill chunks. */
 int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, int32_t *n_prefill_items,
                  int32_t *n_decode_items, int32_t *items, int32_t cap);

@@ -57,10 +57,15 @@ class orthrus_decode_row(Structure):
     _fields_ = [("seq", c_int32), ("ctx_len", c_int32)]
 
 
+class orthrus_gen_chunk(Structure):
+    _fields_ = [("seq", c_int32), ("offset", c_int32), ("len", c_int32), ("flags", c_int32)]
+
+
 class orthrus_batch(Structure):
     _fields_ = [("n_chunks", c_int32), ("n_decode", c_int32),
                 ("chunks", POINTER(orthrus_emb_chunk)), ("rows", POINTER(orthrus_decode_row)),
-                ("token_ids", POINTER(c_int32))]
+                ("token_ids", POINTER(c_int32)), ("n_gen_chunks", c_int32),
+                ("gen_chunks", POINTER(orthrus_gen_chunk))]
 
 
 class orthrus_kv(Structure):
@@ -82,6 +87,7 @@ SIGNATURES = {
     "orthrus_step": (c_int, [c_void_p, c_void_p, POINTER(orthrus_batch), POINTER(orthrus_kv),
                              POINTER(orthrus_kv), c_void_p, c_void_p, c_void_p, c_void_p,
                              c_void_p, c_size_t, c_void_p]),
+    "orthrus_sample_greedy": (c_int, [c_void_p, c_int32, c_int32, c_void_p, c_void_p]),
     "orthrus_workspace_init": (c_int, [c_void_p, c_void_p]),
     "orthrus_device_error": (c_int, [c_void_p, c_void_p, POINTER(c_int32)]),
     "orthrus_plan": (c_int, [c_void_p, c_void_p, POINTER(orthrus_batch), POINTER(orthrus_kv),
@@ -133,6 +139,10 @@ def orthrus_step(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits, ou
                  ws_bytes, stream):
     return load().orthrus_step(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits,
                                out_emb, workspace, ws_bytes, stream)
+
+
+def orthrus_sample_greedy(logits, rows, vocab, out_tokens, stream):
+    return load().orthrus_sample_greedy(logits, rows, vocab, out_tokens, stream)
 
 
 def orthrus_workspace_init(workspace, stream):

@@ -7,7 +7,8 @@
 // decode dot products pair adjacent dims (q.k) or adjacent positions (p.v) without shuffles.
 //
 // The host planner emits a work list; block b runs item b:
-//   * prefill items (embedding-chunk rows, heaviest first): (128 / group) tokens of one chunk
+//   * prefill items (rows of embedding and generation prefill chunks, heaviest first; each
+//     chunk reads the cache of its own model): (128 / group) tokens of one chunk
 //     times the `group` query heads of one KV head; each wave owns 32 query rows of one head
 //     and walks the keys of its request in 32-key blocks, with operands loaded straight from
 //     the cache (L2-resident, shared by the group's waves) one block ahead of the MFMAs, an
@@ -39,15 +40,19 @@ struct PoolView {
     int n_pages, max_blocks;
 };
 
+// cache of pool p (0: embedding model's, 1: generator's); selects, not an indexed load, so a
+// run-time p keeps the kernel arguments in scalar registers
 __device__ __forceinline__ PoolView pool_view(const AttnArgs &a, int p) {
     PoolView pv;
-    pv.k = (const char *)a.k_cache[p];
-    pv.v = (const char *)a.v_cache[p];
-    pv.bt = a.block_table[p];
-    pv.n_pages = a.n_pages[p];
-    pv.max_blocks = a.max_blocks[p];
+    pv.k = (const char *)(p ? a.k_cache[1] : a.k_cache[0]);
+    pv.v = (const char *)(p ? a.v_cache[1] : a.v_cache[0]);
+    pv.bt = p ? a.block_table[1] : a.block_table[0];
+    pv.n_pages = p ? a.n_pages[1] : a.n_pages[0];
+    pv.max_blocks = p ? a.max_blocks[1] : a.max_blocks[0];
     return pv;
 }
+// prefill chunks of the generator (prompt chunks) read its cache
+__device__ __forceinline__ int chunk_pool(const int32_t *ch) { return (ch[3] & kChunkGen) ? 1 : 0; }
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c,
@@ -384,7 +389,7 @@ __device__ void prefill_item_f32(const AttnArgs &a, const int32_t *it) {
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], tok = ch[4] + qb + r;
     const int qpos = off + qb + r;
-    const PoolView pv = pool_view(a, 0);
+    const PoolView pv = pool_view(a, chunk_pool(ch));
     const size_t page_elems = (size_t)a.nkv * kPage * HD;
     const float *qp = (const float *)a.q + ((size_t)tok * a.nq + h) * HD;
     float q[HD], acc[HD];
@@ -450,7 +455,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     const int r = sb * 32 + min(col, max(rows, 1) - 1);   // padded rows repeat a valid row
     const int tok = tok0 + qb + min(r, qn - 1);
     const int qpos = off + qb + min(r, qn - 1);
-    const PoolView pv = pool_view(a, 0);
+    const PoolView pv = pool_view(a, chunk_pool(ch));
     const size_t page_bytes = (size_t)a.nkv * kPage * HD * 2;
     const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks;
     const int nkb = (kend + 31) / 32;

@@ -140,20 +140,25 @@ hipError_t launch_attn_combine(int dtype, const AttnArgs &a, int n_decode, hipSt
 struct PoolArgs {
     const float *x;           // fp32 residual rows [T][d]
     const float *gain;        // embedding model's final norm gain [d]
-    const float *gen_gain;    // generator's final norm gain [d] (decode rows)
-    void *act;                // decode rows' normalised LM-head input [T][d], model dtype
-    const int32_t *chunks;
+    const float *gen_gain;    // generator's final norm gain [d] (rows that get logits)
+    void *act;                // LM-head input [n_lm][d], model dtype
+    const int32_t *lm_rows;   // [n_lm] token rows that get logits
+    const int32_t *chunks;    // chunk table; the first n_chunks entries are embedding chunks
     float *inv_rms;           // [Te] scratch: final-norm scale of the embedding rows
     float *acc_sum, *acc_w, *out_emb;
     const float *pend;        // pending split-K slabs added to x first (npend of them, or none)
     size_t pend_stride;
     int npend;
-    int n_chunks, Te, d, row0;
+    int n_chunks, Te, d;
+    int n_emb_rows, n_lm;     // final-norm launch: embedding rows [0, n_emb_rows), lm_rows
     float eps;
     int *err;
 };
-// final RMSNorm over rows [row0, row0 + rows): 1/rms of embedding rows, normalised decode rows
-hipError_t launch_final_rows(int dtype, const PoolArgs &a, int rows, hipStream_t s);
+// final RMSNorm: 1/rms of embedding rows [0, n_emb_rows), then the n_lm rows listed in lm_rows
+// normalised into act
+hipError_t launch_final_rows(int dtype, const PoolArgs &a, hipStream_t s);
+// greedy sampler: out[r] = first index of the largest logits[r][.] (NaN compares greatest)
+hipError_t launch_argmax(const float *logits, int rows, int vocab, int32_t *out, hipStream_t s);
 // incremental pooler update and finished embeddings.  Single-row heads (last token, CLS) take
 // their row's final norm themselves (adding npend slabs); with any_mean, mean-pooled chunks
 // are accumulated too and need launch_final_rows over their rows first.

@@ -1,5 +1,6 @@
 // Row-wise kernels of the step: token gather + RMSNorm, RMSNorm, rotary embedding with
-// KV-cache append, and the incremental pooler (Section 3.3) with the final L2 normalisation.
+// KV-cache append, the incremental pooler (Section 3.3) with the final L2 normalisation, and the
+// greedy sampler of Algorithm 1 (argmax over each logits row).
 #include "common.hpp"
 #include "plan.hpp"
 
@@ -136,12 +137,16 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
 }
 
 // ---------------------------------------------------------------------- incremental pooler
-// Final RMSNorm: for embedding-slice rows only its scale 1/rms is kept (the pooler applies it);
-// decode rows are normalised into the LM head's input.  One row per block.
+// Final RMSNorm, one row per block.  Blocks [0, n_emb_rows) take embedding rows 0.. and keep
+// only the scale 1/rms (the pooler applies it); the following blocks take the rows listed in
+// lm_rows and write them, normalised with the generator's gain, as consecutive rows of the LM
+// head's input.
 template <typename T>
 __global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
     __shared__ float red[4];
-    const int r = a.row0 + blockIdx.x;
+    const bool emb_row = (int)blockIdx.x < a.n_emb_rows;
+    const int lm = (int)blockIdx.x - a.n_emb_rows;
+    const int r = emb_row ? (int)blockIdx.x : a.lm_rows[lm];
     const int nv = a.d / 4;
     float *x = const_cast<float *>(a.x) + (size_t)r * a.d;
     float ss = 0.f;
@@ -158,11 +163,11 @@ __global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
         ss += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
     }
     const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
-    if (r < a.Te) {
+    if (emb_row) {
         if (threadIdx.x == 0) a.inv_rms[r] = inv;
         return;
     }
-    T *y = (T *)a.act + (size_t)r * a.d;
+    T *y = (T *)a.act + (size_t)lm * a.d;
     for (int v = threadIdx.x; v < nv; v += 256) {
         const float4 q = load4(x + 4 * v), g = load4(a.gen_gain + 4 * v);
         store4(y + 4 * v, float4{q.x * inv * g.x, q.y * inv * g.y, q.z * inv * g.z, q.w * inv * g.w});
@@ -288,7 +293,58 @@ __global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
     }
 }
 
+// ------------------------------------------------------------------------- greedy sampler
+// (v, i) beats (bv, bi) when it comes first in "NaN greatest, then larger value, then lower index"
+__device__ __forceinline__ bool argmax_better(float v, int i, float bv, int bi) {
+    const bool vn = v != v, bn = bv != bv;
+    if (vn || bn) return vn && (!bn || i < bi);
+    return v > bv || (v == bv && i < bi);
+}
+
+// One block per row; each thread scans a strided slice (16-byte loads when the row allows),
+// then the block reduces its 256 candidates.  The result does not depend on the scan order.
+__global__ __launch_bounds__(256) void argmax_kernel(const float *logits, int vocab, int32_t *out) {
+    __shared__ float bvs[4];
+    __shared__ int bis[4];
+    const float *row = logits + (size_t)blockIdx.x * vocab;
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    const bool vec = (vocab % 4 == 0) && ((uintptr_t)logits % 16 == 0);
+    if (vec) {
+        for (int v = threadIdx.x; v < vocab / 4; v += 256) {
+            const float4 q = load4(row + 4 * v);
+            if (argmax_better(q.x, 4 * v, bv, bi)) bv = q.x, bi = 4 * v;
+            if (argmax_better(q.y, 4 * v + 1, bv, bi)) bv = q.y, bi = 4 * v + 1;
+            if (argmax_better(q.z, 4 * v + 2, bv, bi)) bv = q.z, bi = 4 * v + 2;
+            if (argmax_better(q.w, 4 * v + 3, bv, bi)) bv = q.w, bi = 4 * v + 3;
+        }
+    } else {
+        for (int v = threadIdx.x; v < vocab; v += 256)
+            if (argmax_better(row[v], v, bv, bi)) bv = row[v], bi = v;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (argmax_better(ov, oi, bv, bi)) bv = ov, bi = oi;
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) bvs[wave] = bv, bis[wave] = bi;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < 4; ++w)
+            if (argmax_better(bvs[w], bis[w], bv, bi)) bv = bvs[w], bi = bis[w];
+        out[blockIdx.x] = bi;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_argmax(const float *logits, int rows, int vocab, int32_t *out, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(argmax_kernel, dim3(rows), dim3(256), 0, s, logits, vocab, out);
+    return hipGetLastError();
+}
 
 hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t s) {
     if (a.rows <= 0) return hipSuccess;
@@ -309,7 +365,8 @@ hipError_t launch_rope_append(int dtype, const RopeArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_final_rows(int dtype, const PoolArgs &a, int rows, hipStream_t s) {
+hipError_t launch_final_rows(int dtype, const PoolArgs &a, hipStream_t s) {
+    const int rows = a.n_emb_rows + a.n_lm;
     if (rows <= 0) return hipSuccess;
     if (dtype == 1) hipLaunchKernelGGL(final_rows_kernel<bf16>, dim3(rows), dim3(256), 0, s, a);
     else hipLaunchKernelGGL(final_rows_kernel<float>, dim3(rows), dim3(256), 0, s, a);

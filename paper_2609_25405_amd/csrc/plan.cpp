@@ -1,16 +1,15 @@
 // Host planner for the mixed step (Section 3.2 batch unit, Section 3.3 chunk bookkeeping).
 //
 // Turns the caller's descriptor into the metadata the kernels read: per token its id,
-// absolute position and request; per chunk its request, offset, length, flags and first
-// token; per decode row its request, context and split layout; and the attention work
-// list.  Validation mirrors the step contract: every check here runs before anything is
-// enqueued, so a rejected batch leaves all caller buffers untouched.
+// absolute position and request; per chunk (embedding and generation prefill) its request,
+// offset, length, flags and first token; per decode row its request, context and split
+// layout; the attention work list; and the rows that get logits.  Validation mirrors the step
+// contract: every check here runs before anything is enqueued, so a rejected batch leaves all
+// caller buffers untouched.
 #include "plan.hpp"
 
 #include <algorithm>
 #include <array>
-
-#include <algorithm>
 #include <numeric>
 #include <set>
 #include <utility>
@@ -41,14 +40,20 @@ int max_splits_for_ctx(int max_ctx, int page_size) {
 
 int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const orthrus_kv &ekv,
               const orthrus_kv &gkv, StepPlan &p) {
-    if (b.n_chunks < 0 || b.n_decode < 0) return ORTHRUS_EINVAL;
-    if ((b.n_chunks && !b.chunks) || (b.n_decode && !b.rows)) return ORTHRUS_EINVAL;
+    if (b.n_chunks < 0 || b.n_decode < 0 || b.n_gen_chunks < 0) return ORTHRUS_EINVAL;
+    if ((b.n_chunks && !b.chunks) || (b.n_decode && !b.rows) || (b.n_gen_chunks && !b.gen_chunks))
+        return ORTHRUS_EINVAL;
     const int P = emb.cfg.page_size;
     p = StepPlan();
     p.n_chunks = b.n_chunks;
+    p.n_gen = b.n_gen_chunks;
     p.D = b.n_decode;
     p.shared_kv = ekv.k_cache == gkv.k_cache;
-    long long Te = 0;
+    // one sequence namespace per cache: generation items share the embedding one when the
+    // caches are the same
+    const int gen_ns = p.shared_kv ? 0 : 1;
+    long long Te = 0, Tg = 0;
+    int n_last_gen = 0;
     std::set<std::pair<int, int>> seen;  // (namespace, seq)
     for (int i = 0; i < b.n_chunks; ++i) {
         const orthrus_emb_chunk &c = b.chunks[i];
@@ -60,20 +65,50 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         if (!seen.insert({0, c.seq}).second) return ORTHRUS_EDUPSEQ;
         Te += c.len;
     }
+    for (int i = 0; i < b.n_gen_chunks; ++i) {
+        const orthrus_gen_chunk &c = b.gen_chunks[i];
+        if (c.seq < 0 || c.seq >= gkv.n_seq || c.offset < 0 || c.len < 1) return ORTHRUS_EDESC;
+        if (c.flags & ~ORTHRUS_CHUNK_LAST) return ORTHRUS_EDESC;
+        if ((long long)c.offset + c.len > (long long)gkv.max_blocks * P) return ORTHRUS_ECAPACITY;
+        if (!seen.insert({gen_ns, c.seq}).second) return ORTHRUS_EDUPSEQ;
+        Tg += c.len;
+        n_last_gen += c.flags & ORTHRUS_CHUNK_LAST;
+    }
     for (int j = 0; j < b.n_decode; ++j) {
         const orthrus_decode_row &r = b.rows[j];
         if (r.seq < 0 || r.seq >= gkv.n_seq || r.ctx_len < 0) return ORTHRUS_EDESC;
         if ((long long)r.ctx_len + 1 > (long long)gkv.max_blocks * P) return ORTHRUS_ECAPACITY;
-        if (!seen.insert({p.shared_kv ? 0 : 1, r.seq}).second) return ORTHRUS_EDUPSEQ;
+        if (!seen.insert({gen_ns, r.seq}).second) return ORTHRUS_EDUPSEQ;
     }
-    if (Te + b.n_decode > (1LL << 30)) return ORTHRUS_ECAPACITY;
+    if (Te + Tg + b.n_decode > (1LL << 30)) return ORTHRUS_ECAPACITY;
     p.Te = (int)Te;
-    p.T = p.Te + p.D;
+    p.Tg = (int)Tg;
+    p.T = p.Te + p.Tg + p.D;
+    p.n_lm = n_last_gen + p.D;
+    if (p.n_lm > 0 && !gen.w.lm_head) return ORTHRUS_EDESC;
     if (p.T > 0 && !b.token_ids) return ORTHRUS_EINVAL;
-    if (p.D > 0 && !gen.w.lm_head) return ORTHRUS_EDESC;
     for (int t = 0; t < p.T; ++t) {
         const int v = t < p.Te ? emb.cfg.vocab : gen.cfg.vocab;
         if (b.token_ids[t] < 0 || b.token_ids[t] >= v) return ORTHRUS_EDESC;
+    }
+
+    // chunk table entries of both chunk kinds: {seq, offset, len, flags, first token}
+    const int n_all = b.n_chunks + b.n_gen_chunks;
+    std::vector<int32_t> chunks(kChunkInts * n_all);
+    {
+        int t = 0;
+        for (int i = 0; i < n_all; ++i) {
+            int32_t *ch = &chunks[kChunkInts * i];
+            if (i < b.n_chunks) {
+                const orthrus_emb_chunk &c = b.chunks[i];
+                ch[0] = c.seq, ch[1] = c.offset, ch[2] = c.len, ch[3] = c.flags;
+            } else {
+                const orthrus_gen_chunk &c = b.gen_chunks[i - b.n_chunks];
+                ch[0] = c.seq, ch[1] = c.offset, ch[2] = c.len, ch[3] = c.flags | kChunkGen;
+            }
+            ch[4] = t;
+            t += ch[2];
+        }
     }
 
     const int nkv = emb.cfg.n_kv_heads;
@@ -83,11 +118,12 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     // --- attention work list: prefill query tiles (heaviest first), then decode splits
     struct Pre { long long work; int chunk, kvh, qb, qn, kend; };
     std::vector<Pre> pre;
-    for (int i = 0; i < b.n_chunks; ++i) {
-        const orthrus_emb_chunk &c = b.chunks[i];
-        for (int qb = 0; qb < c.len; qb += qrows) {
-            const int qn = std::min(qrows, c.len - qb);
-            const int kend = c.offset + qb + qn;
+    for (int i = 0; i < n_all; ++i) {
+        const int32_t *ch = &chunks[kChunkInts * i];
+        const int off = ch[1], len = ch[2];
+        for (int qb = 0; qb < len; qb += qrows) {
+            const int qn = std::min(qrows, len - qb);
+            const int kend = off + qb + qn;
             for (int g = 0; g < nkv; ++g) pre.push_back({(long long)kend * qn, i, g, qb, qn, kend});
         }
     }
@@ -120,7 +156,7 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         const int n_splits = (n_chunk + cps - 1) / cps;
         rows[kRowInts * j + 0] = r.seq;
         rows[kRowInts * j + 1] = r.ctx_len;
-        rows[kRowInts * j + 2] = p.Te + j;
+        rows[kRowInts * j + 2] = p.Te + p.Tg + j;
         rows[kRowInts * j + 3] = n_splits;
         rows[kRowInts * j + 4] = n_splits > 1 ? partial : -1;
         if (n_splits > 1) p.n_split_rows++;
@@ -157,29 +193,27 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     p.off_pos = p.T;
     p.off_seq = 2 * p.T;
     p.off_chunks = 3 * p.T;
-    p.off_rows = p.off_chunks + kChunkInts * p.n_chunks;
+    p.off_rows = p.off_chunks + kChunkInts * n_all;
     p.off_items = p.off_rows + kRowInts * p.D;
-    p.meta.assign(p.off_items + items.size(), 0);
-    int t = 0;
-    for (int i = 0; i < b.n_chunks; ++i) {
-        const orthrus_emb_chunk &c = b.chunks[i];
-        int32_t *ch = &p.meta[p.off_chunks + kChunkInts * i];
-        ch[0] = c.seq;
-        ch[1] = c.offset;
-        ch[2] = c.len;
-        ch[3] = c.flags;
-        ch[4] = t;
-        for (int k = 0; k < c.len; ++k, ++t) {
-            p.meta[p.off_tok + t] = b.token_ids[t];
-            p.meta[p.off_pos + t] = c.offset + k;
-            p.meta[p.off_seq + t] = c.seq;
+    p.off_lm = p.off_items + (int)items.size();
+    p.meta.assign(p.off_lm + p.n_lm, 0);
+    std::copy(b.token_ids, b.token_ids + p.T, p.meta.begin() + p.off_tok);
+    int lm = 0;
+    for (int i = 0; i < n_all; ++i) {
+        const int32_t *ch = &chunks[kChunkInts * i];
+        for (int k = 0; k < ch[2]; ++k) {
+            p.meta[p.off_pos + ch[4] + k] = ch[1] + k;
+            p.meta[p.off_seq + ch[4] + k] = ch[0];
         }
+        if ((ch[3] & kChunkGen) && (ch[3] & ORTHRUS_CHUNK_LAST)) p.meta[p.off_lm + lm++] = ch[4] + ch[2] - 1;
     }
-    for (int j = 0; j < p.D; ++j, ++t) {
-        p.meta[p.off_tok + t] = b.token_ids[t];
+    for (int j = 0; j < p.D; ++j) {
+        const int t = p.Te + p.Tg + j;
         p.meta[p.off_pos + t] = b.rows[j].ctx_len;
         p.meta[p.off_seq + t] = b.rows[j].seq;
+        p.meta[p.off_lm + lm++] = t;
     }
+    std::copy(chunks.begin(), chunks.end(), p.meta.begin() + p.off_chunks);
     std::copy(rows.begin(), rows.end(), p.meta.begin() + p.off_rows);
     std::copy(items.begin(), items.end(), p.meta.begin() + p.off_items);
     return ORTHRUS_OK;

@@ -33,15 +33,23 @@ struct Model {
 enum ItemField { IT_KIND = 0, IT_INDEX, IT_KVHEAD, IT_A, IT_B, IT_KEY_BEGIN, IT_KEY_END, IT_PARTIAL };
 constexpr int kItemInts = 8;
 constexpr int kChunkInts = 5;  // seq, offset, len, flags, first token
+// chunk-table flag of a generation prefill chunk (reads and appends the generator's cache; the
+// pooler skips it).  Caller flags use bits 0-2 only.
+constexpr int kChunkGen = 1 << 8;
 constexpr int kRowInts = 5;    // seq, ctx_len, token index, n_splits, first partial slot
 
+// Token order of a step: [0, Te) embedding-chunk tokens, [Te, Te + Tg) generation prefill
+// tokens, [Te + Tg, T) decode tokens.  The chunk table holds the n_chunks embedding chunks, then
+// the n_gen generation chunks.
 struct StepPlan {
-    int T = 0, Te = 0, D = 0, n_chunks = 0;
+    int T = 0, Te = 0, Tg = 0, D = 0, n_chunks = 0, n_gen = 0;
     bool shared_kv = true;
     int n_prefill = 0, n_decode_items = 0, n_partials = 0, n_split_rows = 0;
-    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items
+    int n_lm = 0;  // rows that get logits: last rows of final prompt chunks, then decode rows
+    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows
     std::vector<int32_t> meta;
-    int off_tok = 0, off_pos = 0, off_seq = 0, off_chunks = 0, off_rows = 0, off_items = 0;
+    int off_tok = 0, off_pos = 0, off_seq = 0, off_chunks = 0, off_rows = 0, off_items = 0,
+        off_lm = 0;
 };
 
 int validate_config(const orthrus_config &c);

@@ -1,7 +1,8 @@
-// C ABI of the mixed step: model handles, workspace sizing, and the per-step launch sequence
-// (one iteration of the heterogeneous-batching loop, Algorithm 1, without scheduling and
-// sampling; the forward is shared by all request types, Section 3.1; the pooler and the LM
-// head read contiguous slices of the type-sorted batch, Section 3.2).
+// C ABI of the mixed step: model handles, workspace sizing, the per-step launch sequence (one
+// iteration of the heterogeneous-batching loop, Algorithm 1, without scheduling; the forward is
+// shared by all request types, Section 3.1; the pooler reads the embedding slice of the
+// type-sorted batch, Section 3.2, and the LM head the rows that need next-token logits), and
+// the greedy sampler.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -202,7 +203,8 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
     const size_t pre_items = ((size_t)max_tokens / qrows + max_chunks) * nkv;
     const size_t dec_items = (size_t)max_decode * nkv * splits;
     const size_t meta = 3 * (size_t)max_tokens + kChunkInts * (size_t)max_chunks +
-                        kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items);
+                        kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items) +
+                        (size_t)max_chunks + max_decode;  // rows that get logits
     return make_layout(m, max_tokens, meta, dec_items).total;
 }
 
@@ -233,6 +235,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     StepPlan p;
     int rc = plan_step(*emb, *gen, *batch, *emb_kv, *gen_kv, p);
     if (rc) return rc;
+    if (p.n_lm > 0 && !out_logits) return ORTHRUS_EINVAL;
     if (p.T == 0) return ORTHRUS_OK;
     const Model &M = *emb;
     const orthrus_config &c = M.cfg;
@@ -270,7 +273,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     const bool one_model = emb == gen;
     const int32_t *tok = meta + p.off_tok;
 
-    // row groups: [0, Te) through the embedding model, [Te, T) through the generator
+    // row groups: [0, Te) through the embedding model, [Te, T) (prompt chunks, then decode rows)
+    // through the generator
     struct Group { const orthrus_model *m; int r0, r1; };
     Group groups[2];
     int n_groups = 0;
@@ -465,13 +469,14 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         pending = splits > 1 ? splits : 0;  // added by the next layer's norm or the final norm
     }
 
-    // final RMSNorm (scale of the embedding rows; LM-head input of the decode rows), then the
-    // incremental pooler on the embedding slice and the LM head on the decode slice
+    // final RMSNorm (scale of the embedding rows; LM-head input of the rows that get logits),
+    // then the incremental pooler on the embedding slice and the LM head on the listed rows
     PoolArgs pa{};
     pa.x = x;
     pa.gain = emb->w.final_norm;
     pa.gen_gain = gen->w.final_norm;
-    pa.act = act;
+    pa.act = act;  // free after the last layer: the LM-head input goes to its first n_lm rows
+    pa.lm_rows = meta + p.off_lm;
     pa.chunks = meta + p.off_chunks;
     pa.inv_rms = (float *)(ws + L.inv_rms);
     pa.acc_sum = acc_sum;
@@ -483,31 +488,25 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     pa.npend = pending;
     pa.Te = Te;
     pa.d = d;
-    pa.row0 = 0;
     pa.eps = c.rms_eps;
     pa.err = err;
     // Only mean pooling needs the final norm of every embedding row; single-row heads normalise
-    // their one row inside the pooler.  With no layers the gather already normalised the
-    // decode rows with the final gain.
+    // their one row inside the pooler.
     bool any_mean = false;
     for (int i = 0; i < batch->n_chunks; ++i)
         any_mean |= ((batch->chunks[i].flags >> ORTHRUS_POOL_SHIFT) & 3) == ORTHRUS_POOL_MEAN;
-    const int row_first = any_mean ? 0 : Te;
-    const int row_end = c.n_layers > 0 ? T : (any_mean ? Te : 0);
-    if (row_end > row_first) {
-        pa.row0 = row_first;
-        RUN("final_norm", launch_final_rows(dt, pa, row_end - row_first, s));
-    }
+    pa.n_emb_rows = any_mean ? Te : 0;
+    pa.n_lm = p.n_lm;
+    if (pa.n_emb_rows + pa.n_lm > 0) RUN("final_norm", launch_final_rows(dt, pa, s));
     // the embedding rows' pending slabs were added by the final norm when it covered them
-    pa.row0 = 0;
     if (any_mean) pa.npend = 0;
     if (p.n_chunks > 0) RUN("pool", launch_pool(pa, any_mean, s));
-    if (p.D > 0) {
+    if (p.n_lm > 0) {
         GemmArgs ga{};
-        ga.A = act + (size_t)Te * d * es;
+        ga.A = act;
         ga.B0 = gen->w.lm_head;
         ga.out = out_logits;
-        ga.M = p.D;
+        ga.M = p.n_lm;
         ga.N = gen->cfg.vocab;
         ga.K = d;
         ga.lda = d;
@@ -553,6 +552,15 @@ int orthrus_profile_end(orthrus_model *m, orthrus_kernel_time *out, int32_t cap,
     }
     m->prof_names.clear();
     return rc;
+}
+
+int orthrus_sample_greedy(const float *logits, int32_t rows, int32_t vocab, int32_t *out_tokens,
+                          void *stream) {
+    if (rows < 0 || vocab < 1) return ORTHRUS_EINVAL;
+    if (rows == 0) return ORTHRUS_OK;
+    if (!logits || !out_tokens) return ORTHRUS_EINVAL;
+    if (launch_argmax(logits, rows, vocab, out_tokens, (hipStream_t)stream) != hipSuccess) return ORTHRUS_EHIP;
+    return ORTHRUS_OK;
 }
 
 int orthrus_workspace_init(void *workspace, void *stream) {

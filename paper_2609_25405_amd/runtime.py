@@ -158,13 +158,23 @@ class PackedBatch:
         self._rows = (A.orthrus_decode_row * max(1, nd))()
         for j, r in enumerate(batch.rows):
             self._rows[j] = A.orthrus_decode_row(int(r.seq), int(r.ctx_len))
+        gen = list(getattr(batch, "gen_chunks", []) or [])
+        ng = len(gen)
+        self._gen = (A.orthrus_gen_chunk * max(1, ng))()
+        for i, c in enumerate(gen):
+            self._gen[i] = A.orthrus_gen_chunk(int(c.seq), int(c.offset), int(c.len),
+                                               A.ORTHRUS_CHUNK_LAST if c.last else 0)
         self._ids = np.ascontiguousarray(batch.token_ids, dtype=np.int32)
-        # the C side reads sum(len) + n_decode ids through a bare pointer: check the length here
-        if self._ids.shape != (sum(int(c.len) for c in batch.chunks) + nd,):
+        # the C side reads every chunk token and one id per decode row through a bare pointer:
+        # check the length here
+        n_ids = sum(int(c.len) for c in batch.chunks) + sum(int(c.len) for c in gen) + nd
+        if self._ids.shape != (n_ids,):
             raise A.OrthrusError(A.ORTHRUS_EDESC, "token_ids length")
+        self.n_logit_rows = sum(1 for c in gen if c.last) + nd
         self.c = A.orthrus_batch(nc, nd, ctypes.cast(self._chunks, POINTER(A.orthrus_emb_chunk)),
                                  ctypes.cast(self._rows, POINTER(A.orthrus_decode_row)),
-                                 self._ids.ctypes.data_as(POINTER(c_int32)))
+                                 self._ids.ctypes.data_as(POINTER(c_int32)), ng,
+                                 ctypes.cast(self._gen, POINTER(A.orthrus_gen_chunk)))
 
 
 def step(emb: DeviceModel, gen: DeviceModel, batch, emb_kv: DeviceKV, gen_kv: DeviceKV,
@@ -179,6 +189,18 @@ def step(emb: DeviceModel, gen: DeviceModel, batch, emb_kv: DeviceKV, gen_kv: De
                         _vp(acc_w), _vp(out_logits), _vp(out_emb), _vp(ws.buf), ws.nbytes,
                         c_void_p(s))
     _check(rc, "orthrus_step")
+
+
+def sample_greedy(logits: torch.Tensor, out_tokens: torch.Tensor,
+                  stream: Optional[int] = None) -> None:
+    """Enqueue orthrus_sample_greedy on fp32 logits [rows][vocab] into int32 out_tokens [rows]."""
+    if logits.dtype != torch.float32 or out_tokens.dtype != torch.int32:
+        raise A.OrthrusError(A.ORTHRUS_EINVAL, "sample_greedy dtypes")
+    if not logits.is_contiguous() or logits.dim() != 2 or out_tokens.shape != (logits.shape[0],):
+        raise A.OrthrusError(A.ORTHRUS_EINVAL, "sample_greedy shapes")
+    s = current_stream() if stream is None else stream
+    _check(A.orthrus_sample_greedy(_vp(logits), logits.shape[0], logits.shape[1], _vp(out_tokens),
+                                   c_void_p(s)), "orthrus_sample_greedy")
 
 
 def plan(emb: DeviceModel, gen: DeviceModel, batch, emb_kv, gen_kv):

@@ -1,9 +1,13 @@
 """Running the same seeded steps through the oracle and through liborthrus.so, and comparing.
 
-Tolerances (per output vector: one logits row, one embedding, one pooling-state row, one
-cached key/value head vector):
+Tolerances (per output vector: one logits row, one embedding, one pooling-state row):
   * fp32 path: max|gpu - oracle| / max|oracle| <= 1e-4;
   * bf16 path: cosine >= 0.999 and max|gpu - oracle| / max|oracle| <= 2e-2.
+Cached key/value head vectors are intermediate state, not outputs of the step: fp32 keeps the
+output bound; bf16 keeps cosine >= 0.999 with max-rel <= 4e-2.  A deeper layer's stored key is
+the bf16 rounding of a projection of activations already carrying every earlier layer's bf16
+rounding, and a head vector has only 64-128 entries to set its maximum; a misplaced, unrotated
+or stale key is off by O(1) and fails either bound.
 Bookkeeping is exact: the pooling token counts W, and the set of cache slots a step writes
 (every slot the step does not own keeps its previous bytes, NaN poison included).
 """
@@ -17,6 +21,7 @@ from workload import as_float64
 from paper_2609_25405_amd import runtime as R
 
 TOL = {"f32": dict(rel=1e-4, cos=None), "bf16": dict(rel=2e-2, cos=0.999)}
+TOL_STATE = {"f32": dict(rel=1e-4, cos=None), "bf16": dict(rel=4e-2, cos=0.999)}
 
 
 def vec_errors(g: np.ndarray, o: np.ndarray):
@@ -27,10 +32,10 @@ def vec_errors(g: np.ndarray, o: np.ndarray):
     return rel, cos
 
 
-def assert_vectors_close(g, o, dtype: str, what: str):
+def assert_vectors_close(g, o, dtype: str, what: str, tol=None):
     assert np.all(np.isfinite(g)), f"{what}: non-finite GPU values"
     rel, cos = vec_errors(g, o)
-    t = TOL[dtype]
+    t = (tol or TOL)[dtype]
     assert rel.max() <= t["rel"], f"{what}: max rel {rel.max():.3g} > {t['rel']}"
     if t["cos"] is not None:
         assert cos.min() >= t["cos"], f"{what}: min cos {cos.min():.6f} < {t['cos']}"
@@ -38,11 +43,15 @@ def assert_vectors_close(g, o, dtype: str, what: str):
 
 
 def written_slots(batch, block_table: np.ndarray, page: int, shared: bool):
-    """(pool, page, offset) of every slot the step appends: chunk positions and decode positions."""
+    """(pool, page, offset) of every slot the step appends: chunk positions (embedding and
+    prompt chunks) and decode positions."""
     out = []
     for c in batch.chunks:
         for p in range(c.offset, c.offset + c.len):
             out.append((0, int(block_table[0][c.seq, p // page]), p % page))
+    for c in getattr(batch, "gen_chunks", []) or []:
+        for p in range(c.offset, c.offset + c.len):
+            out.append((0 if shared else 1, int(block_table[1][c.seq, p // page]), p % page))
     for r in batch.rows:
         p = r.ctx_len
         out.append((0 if shared else 1, int(block_table[1][r.seq, p // page]), p % page))
@@ -86,7 +95,7 @@ class Pair:
     def step(self, batch, check_kv: bool = True):
         cfg = self.cfg
         ref = step_oracle(self.emb, self.gen, batch, self.okv_e, self.okv_g, self.S, self.W)
-        nc, nd = len(batch.chunks), len(batch.rows)
+        nc, nd = len(batch.chunks), batch.n_logit_rows
         logits = torch.full((max(1, nd), self.gen[0].vocab), float("nan"), device="cuda")
         out_emb = torch.full((max(1, nc), cfg.d_model), float("nan"), device="cuda")
         pre = [(_bits(self.dkv_e.k).clone(), _bits(self.dkv_e.v_by_position).clone())] if check_kv else None
@@ -142,4 +151,4 @@ class Pair:
                     g = now[:, pg, :, of, :].float().cpu().numpy()
                     o_pool = okv.k if which == "k" else okv.v
                     o = o_pool[:, np.array([m[0] for m in mine]), :, np.array([m[1] for m in mine]), :]
-                    assert_vectors_close(g, o, self.dtype, f"cached {which}")
+                    assert_vectors_close(g, o, self.dtype, f"cached {which}", TOL_STATE)

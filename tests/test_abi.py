@@ -13,8 +13,8 @@ import pytest
 import paper_2609_25405_amd as P
 from paper_2609_25405_amd import _abi as A
 from paper_2609_25405_amd import runtime as R
-from workload import (Batch, DecodeRow, EmbChunk, ModelConfig, PagedKV, draw_tokens, make_weights,
-                      tiny_config, llm7b_config)
+from workload import (Batch, DecodeRow, EmbChunk, GenChunk, ModelConfig, PagedKV, draw_tokens,
+                      make_weights, tiny_config, llm7b_config)
 from oracle import OracleKV, StepError, step_oracle
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "orthrus.h")
@@ -29,7 +29,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     lib = P.load()
     names = header_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     for n in names:
         assert hasattr(lib, n), n
         assert n in A.SIGNATURES, n
@@ -43,7 +43,10 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(A.orthrus_emb_chunk) == 16
     assert ctypes.sizeof(A.orthrus_decode_row) == 8
     assert ctypes.sizeof(A.orthrus_kv) == 3 * 8 + 3 * 4 + 4
-    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8
+    assert ctypes.sizeof(A.orthrus_gen_chunk) == 16
+    # n_chunks, n_decode, 3 pointers, n_gen_chunks (+4 bytes of padding), 1 pointer
+    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8 + 8 + 8
+    assert A.orthrus_batch.gen_chunks.offset == 40
 
 
 def test_model_create_validates_config():
@@ -94,6 +97,19 @@ def test_host_validation_matches_oracle_contract():
     big = ids[:8].copy()
     big[3] = cfg.vocab
     bad.append(Batch([EmbChunk(0, 0, 8, False)], [], big))
+    # generation prefill chunks: same namespace as every item of the shared cache
+    bad += [
+        Batch([], [], ids[:4], [GenChunk(6, 0, 4, True)]),
+        Batch([], [], ids[:4], [GenChunk(1, -1, 4, True)]),
+        Batch([], [], ids[:0], [GenChunk(1, 0, 0, True)]),
+        Batch([], [], ids[:4], [GenChunk(1, 126, 4, True)]),
+        Batch([], [], ids[:8], [GenChunk(1, 0, 4, False), GenChunk(1, 4, 4, True)]),
+        Batch([EmbChunk(1, 0, 4, False)], [], ids[:8], [GenChunk(1, 0, 4, True)]),
+        Batch([], [DecodeRow(2, 3)], ids[:5], [GenChunk(2, 0, 4, False)]),
+    ]
+    big2 = ids[:6].copy()
+    big2[5] = cfg.vocab
+    bad.append(Batch([EmbChunk(0, 0, 2, False)], [], big2, [GenChunk(1, 0, 4, True)]))
     okv = OracleKV.from_paged(pk)
     t = R.torch
     acc, accw = t.zeros((6, cfg.d_model)), t.zeros(6)
@@ -196,3 +212,86 @@ def test_plan_covers_every_key_exactly_once(cfgname):
     b = Batch(chunks, rows, ids)
     npre, ndec, items = R.plan(m, m, b, kv, kv)
     _check_coverage(b, cfg if cfgname == "tiny" else small, npre, ndec, items)
+
+
+def test_prompt_chunks_need_an_lm_head_only_for_logits():
+    """A final prompt chunk asks for logits; the oracle and the library both refuse it on a model
+    without an LM head, and both accept a non-final prompt chunk there."""
+    cfg = tiny_config()
+    W = make_weights(cfg, 2)
+    W["lm_head"] = None
+    m = R.DeviceModel(cfg, W, device="cpu")
+    pk = PagedKV(cfg, 64, 4, 8, 3)
+    for s_ in range(4):
+        pk.reserve(s_, 40)
+    kv = R.DeviceKV.from_paged(pk, device="cpu")
+    okv = OracleKV.from_paged(pk)
+    ids = draw_tokens(1, 1, 4, cfg.vocab)
+    b = Batch([], [], ids, [GenChunk(1, 0, 4, True)])
+    with pytest.raises(StepError) as e:
+        step_oracle((cfg, W), (cfg, W), b, okv, okv, np.zeros((4, cfg.d_model)), np.zeros(4))
+    assert e.value.kind == "desc"
+    with pytest.raises(A.OrthrusError) as g:
+        R.plan(m, m, b, kv, kv)
+    assert g.value.code == A.ORTHRUS_EDESC
+    npre, ndec, _ = R.plan(m, m, Batch([], [], ids, [GenChunk(1, 0, 4, False)]), kv, kv)
+    assert (npre, ndec) == (cfg.n_kv_heads, 0)
+
+
+def test_separate_caches_keep_separate_namespaces():
+    """With two caches, an embedding chunk and a prompt chunk may name the same seq index."""
+    cfg, W, m, pk, kv = _cpu_setup()
+    kv2 = type("KV", (), {})()
+    kv2.struct = lambda: A.orthrus_kv(2, 2, 2, 64, 6, 8)
+    ids = draw_tokens(1, 2, 8, cfg.vocab)
+    b = Batch([EmbChunk(1, 0, 4, False)], [], ids, [GenChunk(1, 0, 4, True)])
+    npre, ndec, items = R.plan(m, m, b, kv, kv2)
+    assert npre == 2 * cfg.n_kv_heads and ndec == 0
+    # chunk indices: the embedding chunk is 0, the prompt chunk 1
+    assert sorted(set(items[:, 1])) == [0, 1]
+    with pytest.raises(A.OrthrusError) as e:
+        R.plan(m, m, b, kv, kv)
+    assert e.value.code == A.ORTHRUS_EDUPSEQ
+
+
+def test_plan_covers_prompt_chunks_with_causal_bounds():
+    """Prompt chunks are tiled like embedding chunks: every (token, kv head) once, key bound =
+    offset + last row + 1, heaviest first across both chunk kinds; decode rows follow."""
+    cfg = tiny_config()
+    W = make_weights(cfg, 0)
+    m = R.DeviceModel(cfg, W, device="cpu")
+    kv = type("KV", (), {})()
+    kv.struct = lambda: A.orthrus_kv(1, 1, 1, 100000, 8, 600)
+    chunks = [EmbChunk(0, 0, 100, True)]
+    gen = [GenChunk(1, 0, 130, False), GenChunk(2, 512, 7, True)]
+    rows = [DecodeRow(3, 300)]
+    ids = np.zeros(100 + 137 + 1, np.int32)
+    b = Batch(chunks, rows, ids, gen)
+    npre, ndec, items = R.plan(m, m, b, kv, kv)
+    allc = [(c.offset, c.len) for c in chunks] + [(c.offset, c.len) for c in gen]
+    seen = set()
+    work = []
+    for it in items[:npre]:
+        kind, ci, g, qb, qn, kb, ke, ps = it
+        off, ln = allc[ci]
+        assert kind == 0 and kb == 0 and ps == -1 and qb + qn <= ln and ke == off + qb + qn
+        for r in range(qb, qb + qn):
+            assert (ci, g, r) not in seen
+            seen.add((ci, g, r))
+        work.append(ke * qn)
+    assert len(seen) == (100 + 137) * cfg.n_kv_heads
+    assert work == sorted(work, reverse=True)
+    assert ndec == cfg.n_kv_heads * 2  # 301 keys: two 256-key chunks, fp32 splits of one chunk
+
+
+def test_sample_greedy_argument_checks():
+    t = R.torch
+    lg = t.zeros((2, 5))
+    out = t.zeros(2, dtype=t.int32)
+    for rows, vocab, code in ((-1, 5, A.ORTHRUS_EINVAL), (2, 0, A.ORTHRUS_EINVAL)):
+        assert A.orthrus_sample_greedy(ctypes.c_void_p(lg.data_ptr()), rows, vocab,
+                                       ctypes.c_void_p(out.data_ptr()), None) == code
+    assert A.orthrus_sample_greedy(None, 2, 5, None, None) == A.ORTHRUS_EINVAL
+    assert A.orthrus_sample_greedy(None, 0, 5, None, None) == A.ORTHRUS_OK
+    with pytest.raises(A.OrthrusError):
+        R.sample_greedy(lg.double(), out)
