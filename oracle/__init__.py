@@ -1,4 +1,4 @@
-"""CPU oracle for the mixed embedding-chunk + decode step (test infrastructure only).
+"""CPU oracle for the mixed step and its scheduler (test infrastructure only).
 
 This package is a plain, slow, float64 NumPy restatement of what one step of the
 paper's heterogeneous batch computes.  It exists to check the GPU library and is
@@ -15,6 +15,9 @@ baseline leg of the benchmark; the product path never imports it.
   per-request pooling state by Eq. (1)-(2) and the positional heads, finishes
   embeddings after a request's final chunk, and emits next-token logits for
   the last row of a prompt's final chunk and for every decode token.
+* ``oracle.sched`` -- intra-batch scheduling (Algorithm 2 with ScheduleRunning
+  and ScheduleOne): which items of which requests one iteration's batch holds,
+  under the token budget, the chunk cap and the cache capacity.
 
 Where the paper leaves a detail open (the model family's normalisation, RoPE
 variant, grouping of query heads, the L2 normalisation of finished embeddings,
@@ -27,7 +30,9 @@ from .model import (rmsnorm, rope_rotate, causal_gqa_attention, silu, forward_fu
                     pool_single_pass, l2_normalize, embed_single_pass, decode_full_recompute,
                     lm_logits, greedy_token)
 from .step import OracleKV, StepError, step_oracle
+from .sched import IBSOracle, SchedConfig, SchedError, Schedule
 
 __all__ = ["rmsnorm", "rope_rotate", "causal_gqa_attention", "silu", "forward_full",
            "pool_single_pass", "l2_normalize", "embed_single_pass", "decode_full_recompute",
-           "lm_logits", "greedy_token", "OracleKV", "StepError", "step_oracle"]
+           "lm_logits", "greedy_token", "OracleKV", "StepError", "step_oracle", "IBSOracle",
+           "SchedConfig", "SchedError", "Schedule"]
