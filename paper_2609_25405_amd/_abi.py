@@ -1,4 +1,5 @@
-"""ctypes mirror of include/orthrus.h: the structs and the entry points, same names.
+"""ctypes mirror of include/orthrus.h and include/orthrus_sched.h: the structs and the entry
+points, same names.
 
 Argument marshalling only.  Loading fails loudly if liborthrus.so has not been built;
 there is no fallback implementation.
@@ -7,7 +8,8 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, Structure, c_float, c_int, c_int32, c_size_t, c_void_p, c_char_p
+from ctypes import (POINTER, Structure, c_char_p, c_float, c_int, c_int32, c_int64, c_size_t,
+                    c_void_p)
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liborthrus.so")
 
@@ -77,7 +79,37 @@ class orthrus_kernel_time(Structure):
     _fields_ = [("name", ctypes.c_char * 32), ("launches", c_int32), ("total_ms", ctypes.c_double)]
 
 
-# name -> (restype, argtypes); every symbol include/orthrus.h declares
+class orthrus_sched_config(Structure):
+    _fields_ = [("budget", c_int32), ("chunk", c_int32), ("atomic_embeddings", c_int32),
+                ("decode_tokens", c_int32), ("page_size", c_int32), ("shared_cache", c_int32),
+                ("eos_token", c_int32), ("n_seq", c_int32 * 2), ("n_pages", c_int32 * 2),
+                ("max_blocks", c_int32 * 2)]
+
+
+class orthrus_sched_batch(Structure):
+    _fields_ = [("batch", orthrus_batch), ("chunk_ids", POINTER(c_int64)),
+                ("gen_chunk_ids", POINTER(c_int64)), ("row_ids", POINTER(c_int64)),
+                ("row_tokens", POINTER(c_int32)), ("n_logit_rows", c_int32),
+                ("logit_ids", POINTER(c_int64)), ("tokens_used", c_int32), ("n_picks", c_int32),
+                ("picks", c_void_p), ("n_finishing", c_int32), ("finishing_ids", POINTER(c_int64)),
+                ("n_table_rows", c_int32), ("table_rows", POINTER(c_int32)), ("credit_e", c_int64),
+                ("credit_g", c_int64)]
+
+
+class orthrus_runner_buffers(Structure):
+    _fields_ = [("acc_sum", c_void_p), ("acc_w", c_void_p), ("logits", c_void_p),
+                ("out_emb", c_void_p), ("tokens", c_void_p), ("workspace", c_void_p),
+                ("ws_bytes", c_size_t)]
+
+
+class orthrus_runner_output(Structure):
+    _fields_ = [("n_tokens", c_int32), ("token_ids", POINTER(c_int64)), ("tokens", POINTER(c_int32)),
+                ("n_embeddings", c_int32), ("embedding_ids", POINTER(c_int64)),
+                ("embeddings", POINTER(c_float)), ("n_finished", c_int32),
+                ("finished_ids", POINTER(c_int64)), ("tokens_used", c_int32), ("n_items", c_int32)]
+
+
+# name -> (restype, argtypes); every symbol include/orthrus.h and include/orthrus_sched.h declare
 SIGNATURES = {
     "orthrus_model_create": (c_int, [POINTER(orthrus_config), POINTER(orthrus_weights),
                                      POINTER(c_void_p)]),
@@ -97,6 +129,20 @@ SIGNATURES = {
     "orthrus_profile_end": (c_int, [c_void_p, POINTER(orthrus_kernel_time), c_int32,
                                     POINTER(c_int32)]),
     "orthrus_strerror": (c_char_p, [c_int]),
+    "orthrus_sched_create": (c_int, [POINTER(orthrus_sched_config), POINTER(c_void_p)]),
+    "orthrus_sched_destroy": (None, [c_void_p]),
+    "orthrus_sched_submit_embedding": (c_int, [c_void_p, c_int64, c_void_p, c_int32, c_int32]),
+    "orthrus_sched_submit_generation": (c_int, [c_void_p, c_int64, c_void_p, c_int32, c_int32]),
+    "orthrus_sched_next": (c_int, [c_void_p, POINTER(orthrus_sched_batch)]),
+    "orthrus_sched_commit": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32),
+                                     POINTER(c_int64), c_int32]),
+    "orthrus_sched_block_table": (POINTER(c_int32), [c_void_p, c_int32]),
+    "orthrus_sched_get_config": (c_int, [c_void_p, POINTER(orthrus_sched_config)]),
+    "orthrus_sched_counts": (c_int, [c_void_p, POINTER(c_int64)]),
+    "orthrus_runner_create": (c_int, [c_void_p, c_void_p, POINTER(orthrus_kv), POINTER(orthrus_kv),
+                                      c_void_p, POINTER(orthrus_runner_buffers), POINTER(c_void_p)]),
+    "orthrus_runner_destroy": (None, [c_void_p]),
+    "orthrus_runner_iterate": (c_int, [c_void_p, c_void_p, POINTER(orthrus_runner_output)]),
 }
 
 _lib = None
@@ -167,3 +213,51 @@ def orthrus_profile_end(model, out, cap, n_out):
 
 def orthrus_strerror(code):
     return load().orthrus_strerror(code).decode()
+
+
+def orthrus_sched_create(cfg, out):
+    return load().orthrus_sched_create(cfg, out)
+
+
+def orthrus_sched_destroy(s):
+    load().orthrus_sched_destroy(s)
+
+
+def orthrus_sched_submit_embedding(s, rid, tokens, n, pool):
+    return load().orthrus_sched_submit_embedding(s, rid, tokens, n, pool)
+
+
+def orthrus_sched_submit_generation(s, rid, prompt, n, max_new):
+    return load().orthrus_sched_submit_generation(s, rid, prompt, n, max_new)
+
+
+def orthrus_sched_next(s, out):
+    return load().orthrus_sched_next(s, out)
+
+
+def orthrus_sched_commit(s, sampled, n, n_finished, finished, cap):
+    return load().orthrus_sched_commit(s, sampled, n, n_finished, finished, cap)
+
+
+def orthrus_sched_block_table(s, cache):
+    return load().orthrus_sched_block_table(s, cache)
+
+
+def orthrus_sched_get_config(s, out):
+    return load().orthrus_sched_get_config(s, out)
+
+
+def orthrus_sched_counts(s, counts7):
+    return load().orthrus_sched_counts(s, counts7)
+
+
+def orthrus_runner_create(emb, gen, emb_kv, gen_kv, sched, buf, out):
+    return load().orthrus_runner_create(emb, gen, emb_kv, gen_kv, sched, buf, out)
+
+
+def orthrus_runner_destroy(r):
+    load().orthrus_runner_destroy(r)
+
+
+def orthrus_runner_iterate(r, stream, out):
+    return load().orthrus_runner_iterate(r, stream, out)

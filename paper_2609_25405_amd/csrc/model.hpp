@@ -1,0 +1,25 @@
+// The host-side model handle behind orthrus_model: configuration, weight pointers, and the
+// per-handle state of the step (metadata staging, kernel timing).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "plan.hpp"
+
+struct orthrus_model : public orthrus::Model {
+    // pinned host staging for the per-step metadata upload, double-buffered with events
+    std::mutex mu;
+    void *stage[2] = {nullptr, nullptr};
+    size_t stage_bytes[2] = {0, 0};
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    int next = 0;
+    // kernel timing (orthrus_profile_begin / _end)
+    bool profiling = false;
+    struct Mark { int name; hipEvent_t a, b; };
+    std::vector<std::string> prof_names;
+    std::vector<Mark> marks;
+};

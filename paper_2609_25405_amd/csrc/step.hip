@@ -13,22 +13,10 @@
 #include <vector>
 
 #include "common.hpp"
+#include "model.hpp"
 #include "orthrus.h"
 #include "plan.hpp"
 
-struct orthrus_model : public orthrus::Model {
-    // pinned host staging for the per-step metadata upload, double-buffered with events
-    std::mutex mu;
-    void *stage[2] = {nullptr, nullptr};
-    size_t stage_bytes[2] = {0, 0};
-    hipEvent_t ev[2] = {nullptr, nullptr};
-    int next = 0;
-    // kernel timing (orthrus_profile_begin / _end)
-    bool profiling = false;
-    struct Mark { int name; hipEvent_t a, b; };
-    std::vector<std::string> prof_names;
-    std::vector<Mark> marks;
-};
 
 namespace orthrus {
 namespace {

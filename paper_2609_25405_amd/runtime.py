@@ -228,3 +228,164 @@ def profile_end(model: DeviceModel):
     n = c_int32(0)
     _check(A.orthrus_profile_end(model.handle, out, cap, byref(n)), "orthrus_profile_end")
     return {out[i].name.decode(): (out[i].launches, out[i].total_ms) for i in range(min(n.value, cap))}
+
+
+class Scheduler:
+    """The native intra-batch scheduler (include/orthrus_sched.h); marshalling only.
+
+    ``caches`` holds (n_seq, n_pages, max_blocks) of the embedding (or shared) cache and, unless
+    ``shared``, of the generator's cache."""
+
+    def __init__(self, budget: int, chunk: int, caches, shared: bool = True,
+                 atomic_embeddings: bool = False, decode_tokens: int = 1, page_size: int = 16,
+                 eos: int = -1):
+        c = A.orthrus_sched_config()
+        c.budget, c.chunk, c.atomic_embeddings = budget, chunk, int(atomic_embeddings)
+        c.decode_tokens, c.page_size, c.shared_cache, c.eos_token = decode_tokens, page_size, int(shared), eos
+        for i, (n_seq, n_pages, max_blocks) in enumerate(caches[:1 if shared else 2]):
+            c.n_seq[i], c.n_pages[i], c.max_blocks[i] = n_seq, n_pages, max_blocks
+        self.cfg = c
+        self.shared = shared
+        h = c_void_p()
+        _check(A.orthrus_sched_create(byref(c), byref(h)), "orthrus_sched_create")
+        self.handle = h
+        self._b = A.orthrus_sched_batch()
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            A.orthrus_sched_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @staticmethod
+    def _ids(tokens, n):
+        if tokens is None:
+            return None, None
+        a = np.ascontiguousarray(tokens, np.int32)
+        if a.shape != (n,):
+            raise A.OrthrusError(A.ORTHRUS_EINVAL, "token count")
+        return a, c_void_p(a.ctypes.data)
+
+    def submit_embedding(self, rid: int, n: int, tokens=None, pool: str = "mean") -> None:
+        a, p = self._ids(tokens, n)
+        _check(A.orthrus_sched_submit_embedding(self.handle, rid, p, n, POOL_CODES[pool]),
+               "orthrus_sched_submit_embedding")
+
+    def submit_generation(self, rid: int, n: int, max_new: int, prompt=None) -> None:
+        a, p = self._ids(prompt, n)
+        _check(A.orthrus_sched_submit_generation(self.handle, rid, p, n, max_new),
+               "orthrus_sched_submit_generation")
+
+    def next(self) -> dict:
+        """The next batch: items by request id (the fields of the scheduling reference model)
+        plus the raw descriptor for orthrus_step."""
+        b = self._b
+        _check(A.orthrus_sched_next(self.handle, byref(b)), "orthrus_sched_next")
+        bt = b.batch
+        emb = [(b.chunk_ids[i], bt.chunks[i].offset, bt.chunks[i].len,
+                bool(bt.chunks[i].flags & A.ORTHRUS_CHUNK_LAST)) for i in range(bt.n_chunks)]
+        gen = [(b.gen_chunk_ids[i], bt.gen_chunks[i].offset, bt.gen_chunks[i].len,
+                bool(bt.gen_chunks[i].flags & A.ORTHRUS_CHUNK_LAST)) for i in range(bt.n_gen_chunks)]
+        dec = [(b.row_ids[j], bt.rows[j].ctx_len, b.row_tokens[j]) for j in range(bt.n_decode)]
+        picks = ctypes.string_at(b.picks, b.n_picks).decode() if b.n_picks else ""
+        n_tok = sum(c[2] for c in emb) + sum(c[2] for c in gen) + len(dec)
+        return {
+            "emb_chunks": emb, "gen_chunks": gen, "decodes": dec, "order": list(picks),
+            "used": b.tokens_used, "logit_ids": [b.logit_ids[i] for i in range(b.n_logit_rows)],
+            "finished": [b.finishing_ids[i] for i in range(b.n_finishing)],
+            "credits": (b.credit_e, b.credit_g),
+            "slots": {"emb": [bt.chunks[i].seq for i in range(bt.n_chunks)],
+                      "gen": [bt.gen_chunks[i].seq for i in range(bt.n_gen_chunks)],
+                      "dec": [bt.rows[j].seq for j in range(bt.n_decode)]},
+            "token_ids": np.ctypeslib.as_array(bt.token_ids, (n_tok,)).copy() if n_tok else
+            np.zeros(0, np.int32),
+            "table_rows": [(b.table_rows[2 * i], b.table_rows[2 * i + 1]) for i in range(b.n_table_rows)],
+        }
+
+    def commit(self, sampled=None):
+        n_logit = self._b.n_logit_rows
+        cap = self._b.n_finishing + n_logit
+        fin = (ctypes.c_int64 * max(1, cap))()
+        nf = c_int32(0)
+        if sampled is None:
+            rc = A.orthrus_sched_commit(self.handle, None, 0, byref(nf), fin, cap)
+        else:
+            a = np.ascontiguousarray(sampled, np.int32)
+            rc = A.orthrus_sched_commit(self.handle, c_void_p(a.ctypes.data), a.size, byref(nf), fin, cap)
+        _check(rc, "orthrus_sched_commit")
+        return [fin[i] for i in range(nf.value)]
+
+    def block_table(self, cache: int = 0) -> np.ndarray:
+        p = A.orthrus_sched_block_table(self.handle, cache)
+        if not p:
+            raise A.OrthrusError(A.ORTHRUS_EINVAL, "orthrus_sched_block_table")
+        i = 0 if self.shared else cache
+        shape = (self.cfg.n_seq[i], self.cfg.max_blocks[i])
+        return np.ctypeslib.as_array(p, shape).copy()
+
+    def counts(self) -> dict:
+        c = (ctypes.c_int64 * 7)()
+        _check(A.orthrus_sched_counts(self.handle, c), "orthrus_sched_counts")
+        keys = ("queued_emb", "queued_gen", "running", "free_slots0", "free_pages0", "free_slots1",
+                "free_pages1")
+        return dict(zip(keys, list(c)))
+
+
+class Runner:
+    """One GPU's iteration loop (orthrus_runner_*): device buffers in torch tensors, sized for the
+    scheduler's budget."""
+
+    def __init__(self, emb: DeviceModel, gen: DeviceModel, emb_kv: DeviceKV, gen_kv: DeviceKV,
+                 sched: Scheduler, device="cuda"):
+        B = sched.cfg.budget
+        d, V = emb.cfg.d_model, gen.cfg.vocab
+        n_seq0 = sched.cfg.n_seq[0]
+        self.acc_sum = torch.zeros((n_seq0, d), dtype=torch.float32, device=device)
+        self.acc_w = torch.zeros(n_seq0, dtype=torch.float32, device=device)
+        self.logits = torch.zeros((B, V), dtype=torch.float32, device=device)
+        self.out_emb = torch.zeros((B, d), dtype=torch.float32, device=device)
+        self.tokens = torch.zeros(B, dtype=torch.int32, device=device)
+        max_ctx = max(sched.cfg.max_blocks[i] for i in range(1 if sched.shared else 2)) * sched.cfg.page_size
+        self.ws = Workspace(emb, gen, B, B, B, max_ctx, device=device)
+        self._keep = (emb, gen, emb_kv, gen_kv, sched)
+        self._ekv, self._gkv = emb_kv.struct(), (emb_kv.struct() if gen_kv is emb_kv else gen_kv.struct())
+        buf = A.orthrus_runner_buffers(_vp(self.acc_sum), _vp(self.acc_w), _vp(self.logits),
+                                       _vp(self.out_emb), _vp(self.tokens), _vp(self.ws.buf),
+                                       self.ws.nbytes)
+        self._buf = buf
+        h = c_void_p()
+        _check(A.orthrus_runner_create(emb.handle, gen.handle, byref(self._ekv), byref(self._gkv),
+                                       sched.handle, byref(buf), byref(h)), "orthrus_runner_create")
+        self.handle = h
+        self.d = d
+        self._out = A.orthrus_runner_output()
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            A.orthrus_runner_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def iterate(self, stream: Optional[int] = None) -> dict:
+        """Run one loop iteration; returns the sampled tokens and finished embeddings by request."""
+        o = self._out
+        s = current_stream() if stream is None else stream
+        _check(A.orthrus_runner_iterate(self.handle, c_void_p(s), byref(o)), "orthrus_runner_iterate")
+        toks = {o.token_ids[i]: o.tokens[i] for i in range(o.n_tokens)}
+        embs = {}
+        if o.n_embeddings:
+            e = np.ctypeslib.as_array(o.embeddings, (o.n_embeddings, self.d))
+            embs = {o.embedding_ids[i]: e[i].copy() for i in range(o.n_embeddings)}
+        return {"tokens": toks, "embeddings": embs,
+                "finished": [o.finished_ids[i] for i in range(o.n_finished)],
+                "used": o.tokens_used, "n_items": o.n_items}

@@ -6,6 +6,7 @@ model handles) or is rejected by host validation before anything is enqueued.
 import ctypes
 import os
 import re
+import subprocess
 
 import numpy as np
 import pytest
@@ -17,19 +18,23 @@ from workload import (Batch, DecodeRow, EmbChunk, GenChunk, ModelConfig, PagedKV
                       make_weights, tiny_config, llm7b_config)
 from oracle import OracleKV, StepError, step_oracle
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "orthrus.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include")
+HEADERS = sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
 
 
 def header_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(orthrus_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(orthrus_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_symbol():
     lib = P.load()
     names = header_functions()
-    assert len(names) == 11
+    assert [os.path.basename(h) for h in HEADERS] == ["orthrus.h", "orthrus_sched.h"]
+    assert len(names) == 11 + 12
     for n in names:
         assert hasattr(lib, n), n
         assert n in A.SIGNATURES, n
@@ -47,6 +52,32 @@ def test_struct_layouts_match_header():
     # n_chunks, n_decode, 3 pointers, n_gen_chunks (+4 bytes of padding), 1 pointer
     assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8 + 8 + 8
     assert A.orthrus_batch.gen_chunks.offset == 40
+
+
+STRUCTS = ["orthrus_config", "orthrus_layer_weights", "orthrus_weights", "orthrus_emb_chunk",
+           "orthrus_decode_row", "orthrus_gen_chunk", "orthrus_batch", "orthrus_kv",
+           "orthrus_kernel_time", "orthrus_sched_config", "orthrus_sched_batch",
+           "orthrus_runner_buffers", "orthrus_runner_output"]
+
+
+def test_ctypes_mirror_matches_the_c_compiler(tmp_path):
+    """Size and every field offset of each header struct, as a C compiler lays them out, equal
+    the ctypes mirror's."""
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "orthrus_sched.h"', "int main(void) {"]
+    for st in STRUCTS:
+        lines.append(f'printf("{st} size %zu\\n", sizeof({st}));')
+        for f, _ in getattr(A, st)._fields_:
+            lines.append(f'printf("{st} {f} %zu\\n", offsetof({st}, {f}));')
+    lines.append("return 0; }")
+    src = tmp_path / "probe.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "probe"
+    subprocess.run(["gcc", "-std=c99", "-I", INCLUDE, str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    for line in filter(None, out):
+        st, f, v = line.split()
+        want = ctypes.sizeof(getattr(A, st)) if f == "size" else getattr(getattr(A, st), f).offset
+        assert int(v) == want, line
 
 
 def test_model_create_validates_config():
