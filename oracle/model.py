@@ -125,11 +125,17 @@ def l2_normalize(v: np.ndarray) -> np.ndarray:
     return v / max(float(np.linalg.norm(v)), 1e-12)
 
 
-def pool_single_pass(H: np.ndarray, head: str) -> np.ndarray:
-    """Section 3.3 heads over all n rows at once: mean (w = 1), CLS (row 0), last (row n-1)."""
+def pool_single_pass(H: np.ndarray, head: str, weights=None) -> np.ndarray:
+    """Section 3.3 heads over all n rows at once: mean (w = 1), weighted mean
+    (sum_j w_j H_j / sum_j w_j, Eq. (1)-(2) in one step; the zero vector when every weight is
+    0), CLS (row 0), last (row n-1)."""
     H = np.asarray(H, F64)
     if head == "mean":
         return H.sum(axis=0) / H.shape[0]
+    if head == "wmean":
+        w = np.asarray(weights, F64)
+        tot = w.sum()
+        return (w[:, None] * H).sum(axis=0) / tot if tot > 0 else np.zeros(H.shape[1])
     if head == "cls":
         return H[0].copy()
     if head == "last":
@@ -137,9 +143,9 @@ def pool_single_pass(H: np.ndarray, head: str) -> np.ndarray:
     raise ValueError(f"unknown pooling head {head!r}")
 
 
-def embed_single_pass(cfg, weights, ids, head: str) -> np.ndarray:
+def embed_single_pass(cfg, weights, ids, head: str, token_weights=None) -> np.ndarray:
     """Unchunked embedding: forward, pool, L2-normalise."""
-    return l2_normalize(pool_single_pass(forward_full(cfg, weights, ids), head))
+    return l2_normalize(pool_single_pass(forward_full(cfg, weights, ids), head, token_weights))
 
 
 def lm_logits(weights, h: np.ndarray) -> np.ndarray:

@@ -29,6 +29,14 @@ Readings taken where the paper is silent (also listed in the design notes):
   row.  Every pooled chunk adds len to W so the offset check holds for all heads;
 * a finished embedding (chunk flagged last) is v / max(||v||_2, 1e-12);
 * pooling kind "none" writes keys/values only (a cache-filling prefill chunk);
+* weighted mean (Eq. (1)-(2) with caller weights w_{k,j} >= 0, one per embedding-chunk token):
+  S += sum_j w_j H_j.  The state's W keeps counting tokens (the offset check above), because
+  the emitted embedding normalize(S / sum w) equals normalize(S) for any positive weight sum,
+  so the weight sum is never needed; with every weight 0 the embedding is the zero vector;
+* buffered head (an arbitrary head applied after the final chunk, buffering the hidden states
+  A = [A; H]): the chunk's final-normed hidden rows are returned for buffer rows
+  seq * hidden_stride + offset .. + len - 1; W counts tokens as for every pooled chunk, and no
+  embedding is emitted (the caller applies its head to the buffer);
 * a generation prefill chunk (seq, offset, len, last) runs through the generator
   and its cache like a decode row of ``len`` tokens at positions offset ..
   offset+len-1; only the final chunk of a prompt (last) emits logits, for its
@@ -121,10 +129,13 @@ def validate(emb, gen, batch, emb_kv: OracleKV, gen_kv: OracleKV) -> None:
     for c in batch.chunks:
         if not (0 <= c.seq < emb_kv.n_seq) or c.offset < 0 or c.len < 1:
             raise StepError("desc", f"bad chunk {c}")
-        if c.pool not in ("mean", "last", "cls", "none") or (c.pool == "none" and c.last):
+        if (c.pool not in ("mean", "last", "cls", "none", "wmean", "buffer")
+                or (c.pool == "none" and c.last)):
             raise StepError("desc", f"bad pooling for chunk {c}")
         if c.offset + c.len > emb_kv.max_blocks * emb_kv.page:
             raise StepError("capacity", f"chunk {c} exceeds the block table")
+        if c.pool == "buffer" and c.offset + c.len > getattr(batch, "hidden_stride", 0):
+            raise StepError("capacity", f"chunk {c} exceeds the hidden-state buffer")
         if ("e", c.seq) in seen:
             raise StepError("dupseq", f"seq {c.seq} twice")
         seen.add(("e", c.seq))
@@ -150,6 +161,16 @@ def validate(emb, gen, batch, emb_kv: OracleKV, gen_kv: OracleKV) -> None:
         raise StepError("desc", "logits need a model with an LM head")
     if n_emb and ((ids[:n_emb] < 0).any() or (ids[:n_emb] >= emb_cfg.vocab).any()):
         raise StepError("desc", "chunk token id out of range")
+    if any(c.pool == "wmean" for c in batch.chunks):
+        w = getattr(batch, "token_weights", None)
+        if w is None or np.asarray(w).shape != (n_emb,):
+            raise StepError("desc", "weighted-mean chunks need one weight per embedding token")
+        t = 0
+        for c in batch.chunks:
+            cw = np.asarray(w[t:t + c.len], F64)
+            t += c.len
+            if c.pool == "wmean" and not (np.isfinite(cw).all() and (cw >= 0).all()):
+                raise StepError("desc", f"weights of chunk {c} must be finite and >= 0")
     if T > n_emb and ((ids[n_emb:] < 0).any() or (ids[n_emb:] >= gen_cfg.vocab).any()):
         raise StepError("desc", "generation token id out of range")
 
@@ -160,7 +181,9 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
 
     ``emb_kv`` / ``gen_kv`` are updated in place (the step appends keys and values).
     Returns float64 ``logits``[n_last_prompt_chunks + n_decode, vocab], ``out_emb``[n_chunks, d]
-    (NaN rows for chunks not flagged last) and the updated ``acc_sum``[n_seq, d], ``acc_w``[n_seq].
+    (NaN rows for chunks not flagged last and for buffered-head chunks), ``hidden`` (chunk index
+    -> its final-normed hidden rows, buffered-head chunks only) and the updated
+    ``acc_sum``[n_seq, d], ``acc_w``[n_seq].
     """
     validate(emb, gen, batch, emb_kv, gen_kv)
     emb_cfg, emb_w = emb
@@ -170,6 +193,8 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
     d = emb_cfg.d_model
     out_emb = np.full((len(batch.chunks), d), np.nan, F64)
     ids = np.asarray(batch.token_ids, np.int64)
+    tw = getattr(batch, "token_weights", None)
+    hidden = {}
     t = 0
     for i, c in enumerate(batch.chunks):
         if c.pool != "none" and c.offset > 0 and W[c.seq] != c.offset:
@@ -177,14 +202,21 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
                                       f"chunk starts at {c.offset}")
         pos = np.arange(c.offset, c.offset + c.len)
         H = _forward_cached(emb_cfg, emb_w, emb_kv, c.seq, ids[t:t + c.len], pos)
+        w = None if tw is None else np.asarray(tw[t:t + c.len], F64)
         t += c.len
         if c.pool == "none":
             continue
         if c.offset == 0:
             S[c.seq] = 0.0
             W[c.seq] = 0.0
+        if c.pool == "buffer":
+            hidden[i] = H
+            W[c.seq] += c.len
+            continue
         if c.pool == "mean":
             S[c.seq] += H.sum(axis=0)
+        elif c.pool == "wmean":
+            S[c.seq] += (w[:, None] * H).sum(axis=0)
         elif c.pool == "last" and c.last:
             S[c.seq] = H[-1]
         elif c.pool == "cls" and c.offset == 0:
@@ -209,4 +241,4 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
         t += 1
         logits[j] = lm_logits(gen_w, H[0])
         j += 1
-    return {"logits": logits, "out_emb": out_emb, "acc_sum": S, "acc_w": W}
+    return {"logits": logits, "out_emb": out_emb, "hidden": hidden, "acc_sum": S, "acc_w": W}

@@ -17,7 +17,7 @@ import pytest
 import oracle
 from oracle import OracleKV, StepError, step_oracle
 from workload import (Batch, DecodeRow, EmbChunk, GenChunk, ModelConfig, PagedKV, draw_tokens,
-                      make_weights, tiny_config)
+                      draw_token_weights, make_weights, tiny_config)
 from tests import bruteforce
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -208,21 +208,28 @@ def _fresh_kv(cfg, n_seq, max_tokens, seed, n_pages=None):
     return pk
 
 
-def run_chunked_embedding(cfg, W, ids, C, head, seq=0, seed=0):
+def run_chunked_embedding(cfg, W, ids, C, head, seq=0, seed=0, weights=None):
     pk = _fresh_kv(cfg, 1 + seq, len(ids), seed)
     pk.reserve(seq, len(ids))
     kv = OracleKV.from_paged(pk)
     S = np.zeros((1 + seq, cfg.d_model))
     Wc = np.zeros(1 + seq)
     out = None
+    rows = []
     for off in range(0, len(ids), C):
         ln = min(C, len(ids) - off)
         b = Batch(chunks=[EmbChunk(seq, off, ln, last=off + ln == len(ids), pool=head)],
-                  rows=[], token_ids=ids[off:off + ln])
+                  rows=[], token_ids=ids[off:off + ln],
+                  token_weights=None if weights is None else weights[off:off + ln],
+                  hidden_stride=len(ids))
         r = step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
         S, Wc = r["acc_sum"], r["acc_w"]
         assert Wc[seq] == off + ln
         out = r["out_emb"][0]
+        if head == "buffer":
+            rows.append(r["hidden"][0])
+    if head == "buffer":
+        return np.concatenate(rows), kv, S, Wc
     return out, kv, S, Wc
 
 
@@ -238,7 +245,8 @@ def test_chunked_equals_single_pass(head, C):
 
 
 def test_pooling_equivalence_table_protocol():
-    """Appendix, pooling-equivalence table: mean and CLS heads at C = 256/512/1024.
+    """Appendix, pooling-equivalence table: mean, CLS and weighted-mean heads at C = 256/512/1024
+    (weighted mean with seeded uniform weights: the paper does not say which weights it used).
 
     The paper's worst observed agreement (fixture) bounds what the oracle must meet
     on a random-weight model; in float64 the two paths agree to rounding.
@@ -254,11 +262,12 @@ def test_pooling_equivalence_table_protocol():
     cfg = micro_config(n_layers=1, d_model=32, head_dim=8, d_ff=32, vocab=64)
     W = sharp_weights(cfg, 31)
     ids = draw_tokens(6, 3, 1100, cfg.vocab)
+    w = draw_token_weights(6, 3, len(ids))
     for (head, C), (min_cos, p99) in bounds.items():
-        if head == "weighted_mean":
-            continue  # weights undefined in the paper; that head is not built
-        ref = oracle.embed_single_pass(cfg, W, ids, head)
-        got, _, _, _ = run_chunked_embedding(cfg, W, ids, C, head)
+        head = "wmean" if head == "weighted_mean" else head
+        tw = w if head == "wmean" else None
+        ref = oracle.embed_single_pass(cfg, W, ids, head, tw)
+        got, _, _, _ = run_chunked_embedding(cfg, W, ids, C, head, weights=tw)
         cos = float(got @ ref / (np.linalg.norm(got) * np.linalg.norm(ref)))
         rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
         assert cos >= min_cos and rel <= p99
@@ -499,3 +508,98 @@ def test_prompt_chunk_contract_errors():
 def test_greedy_token_takes_the_lowest_index_on_ties():
     logits = np.array([[0.5, 2.0, 2.0, -1.0], [3.0, 3.0, 3.0, 3.0], [-np.inf, -5.0, -7.0, -5.0]])
     np.testing.assert_array_equal(oracle.greedy_token(logits), [1, 0, 1])
+
+
+# ---------------------------------------------------------------------------
+# weighted-mean and buffered heads (Section 3.3, Eq. (1)-(2) with general weights)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("C", [1, 7, 16, 23])
+def test_weighted_mean_chunked_equals_definition(C):
+    """Chunked weighted mean equals sum_j w_j H_j / sum_j w_j of the single-pass hidden
+    states, L2-normalised, with the weight sum written out here, not taken from the oracle."""
+    cfg = micro_config()
+    W = sharp_weights(cfg, 41)
+    ids = draw_tokens(7, 1, 23, cfg.vocab)
+    w = draw_token_weights(7, 1, 23).astype(np.float64)
+    H = oracle.forward_full(cfg, W, ids)
+    v = (w[:, None] * H).sum(axis=0) / w.sum()
+    want = v / np.linalg.norm(v)
+    got, _, S, Wc = run_chunked_embedding(cfg, W, ids, C, "wmean", weights=w)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-13)
+    assert Wc[0] == 23                      # the state keeps counting tokens
+
+
+def test_weighted_mean_special_cases():
+    """Unit weights give the mean head; a one-hot weight on the last (first) token gives the
+    last-token (CLS) head; scaling every weight changes nothing; all-zero weights give the
+    zero vector."""
+    cfg = micro_config()
+    W = sharp_weights(cfg, 43)
+    ids = draw_tokens(8, 1, 19, cfg.vocab)
+    mean = oracle.embed_single_pass(cfg, W, ids, "mean")
+    last = oracle.embed_single_pass(cfg, W, ids, "last")
+    cls = oracle.embed_single_pass(cfg, W, ids, "cls")
+    ones = np.ones(19)
+    onehot_last = np.zeros(19)
+    onehot_last[-1] = 1.0
+    onehot_first = np.zeros(19)
+    onehot_first[0] = 2.5
+    w = draw_token_weights(8, 2, 19).astype(np.float64)
+    for C in (5, 19):
+        np.testing.assert_allclose(run_chunked_embedding(cfg, W, ids, C, "wmean", weights=ones)[0], mean,
+                                   rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(run_chunked_embedding(cfg, W, ids, C, "wmean", weights=onehot_last)[0],
+                                   last, rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(run_chunked_embedding(cfg, W, ids, C, "wmean", weights=onehot_first)[0],
+                                   cls, rtol=1e-12, atol=1e-13)
+        a = run_chunked_embedding(cfg, W, ids, C, "wmean", weights=w)[0]
+        b = run_chunked_embedding(cfg, W, ids, C, "wmean", weights=3.0 * w)[0]
+        np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-13)
+        z = run_chunked_embedding(cfg, W, ids, C, "wmean", weights=np.zeros(19))[0]
+        np.testing.assert_array_equal(z, np.zeros(cfg.d_model))
+
+
+@pytest.mark.parametrize("C", [1, 6, 19])
+def test_buffered_head_equals_single_pass_rows(C):
+    """The buffered head hands back every final-normed hidden row; concatenated over the chunks
+    they are the single-pass hidden states, so any head applied to them (here an
+    element-wise max, which no streaming head of the paper computes) matches."""
+    cfg = micro_config()
+    W = sharp_weights(cfg, 47)
+    ids = draw_tokens(9, 1, 19, cfg.vocab)
+    H = oracle.forward_full(cfg, W, ids)
+    rows, _, _, Wc = run_chunked_embedding(cfg, W, ids, C, "buffer")
+    np.testing.assert_allclose(rows, H, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(rows.max(axis=0), H.max(axis=0), rtol=1e-12, atol=1e-13)
+    assert Wc[0] == 19
+
+
+def test_weighted_and_buffered_contract_errors():
+    cfg = micro_config()
+    W = sharp_weights(cfg, 49)
+    pk = _fresh_kv(cfg, 2, 64, 1)
+    pk.reserve(0, 64)
+    kv = OracleKV.from_paged(pk)
+    S, Wc = np.zeros((2, cfg.d_model)), np.zeros(2)
+    ids = draw_tokens(9, 2, 8, cfg.vocab)
+    w = np.ones(8, np.float32)
+    bad = [
+        (Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids), "desc"),                     # no weights
+        (Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids, token_weights=w[:7]), "desc"),
+        (Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids,
+               token_weights=np.where(np.arange(8) == 3, -1.0, 1.0)), "desc"),
+        (Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids,
+               token_weights=np.where(np.arange(8) == 5, np.nan, 1.0)), "desc"),
+        (Batch([EmbChunk(0, 0, 8, True, "buffer")], [], ids, hidden_stride=7), "capacity"),
+        (Batch([EmbChunk(0, 0, 8, True, "median")], [], ids), "desc"),
+    ]
+    for b, kind in bad:
+        with pytest.raises(StepError) as e:
+            step_oracle((cfg, W), (cfg, W), b, kv, kv, S, Wc)
+        assert e.value.kind == kind, (b, e.value.kind)
+    # a negative weight on a token of a chunk that does not use weights is not looked at
+    ok = Batch([EmbChunk(0, 0, 4, False, "mean"), EmbChunk(1, 0, 4, True, "wmean")], [], ids,
+               token_weights=np.array([-1, -1, -1, -1, 1, 1, 1, 1], np.float32))
+    pk.reserve(1, 4)
+    kv = OracleKV.from_paged(pk)
+    step_oracle((cfg, W), (cfg, W), ok, kv, kv, S, Wc)

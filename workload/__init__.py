@@ -26,7 +26,9 @@ POOL_MEAN = "mean"
 POOL_LAST = "last"
 POOL_CLS = "cls"
 POOL_NONE = "none"
-POOL_KINDS = (POOL_MEAN, POOL_LAST, POOL_CLS, POOL_NONE)
+POOL_WMEAN = "wmean"
+POOL_BUFFER = "buffer"
+POOL_KINDS = (POOL_MEAN, POOL_LAST, POOL_CLS, POOL_NONE, POOL_WMEAN, POOL_BUFFER)
 
 
 # ---------------------------------------------------------------------------
@@ -193,12 +195,16 @@ class Batch:
     """One step, type-sorted: embedding chunks, generation prefill chunks, decode rows.
 
     ``token_ids`` holds every embedding chunk's tokens in chunk order, then every prompt
-    chunk's tokens, then one input token per decode row.
+    chunk's tokens, then one input token per decode row.  ``token_weights`` (weighted-mean
+    chunks) holds one weight per embedding-chunk token, in the same order.  ``hidden_stride``
+    is the number of rows per request of the buffer that buffered-head chunks fill.
     """
     chunks: List[EmbChunk] = field(default_factory=list)
     rows: List[DecodeRow] = field(default_factory=list)
     token_ids: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int32))
     gen_chunks: List[GenChunk] = field(default_factory=list)
+    token_weights: Optional[np.ndarray] = None
+    hidden_stride: int = 0
 
     @property
     def n_emb_tokens(self) -> int:
@@ -286,6 +292,12 @@ class PagedKV:
 def draw_tokens(seed: int, tag: int, n: int, vocab: int) -> np.ndarray:
     rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(90, tag)))
     return rng.integers(0, vocab, size=n, dtype=np.int64).astype(np.int32)
+
+
+def draw_token_weights(seed: int, tag: int, n: int) -> np.ndarray:
+    """Per-token pooling weights for weighted-mean requests: uniform on [0, 1), fp32."""
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(91, tag)))
+    return rng.random(n).astype(np.float32)
 
 
 @dataclass
