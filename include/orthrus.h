@@ -48,13 +48,20 @@ extern "C" {
 #define ORTHRUS_F32 0
 #define ORTHRUS_BF16 1
 
-/* orthrus_emb_chunk.flags: bit 0 = final chunk of its request; bits 1-2 = pooling head */
+/* orthrus_emb_chunk.flags: bit 0 = final chunk of its request; bits 1-3 = pooling head.  Every
+ * pooled head (all but NONE) adds len to the request's W, which counts tokens (offset check). */
 #define ORTHRUS_CHUNK_LAST 1
 #define ORTHRUS_POOL_SHIFT 1
-#define ORTHRUS_POOL_MEAN 0 /* S += sum of rows, W += len; emits S / W (Eq. (1)-(2), w = 1) */
-#define ORTHRUS_POOL_LAST 1 /* keeps the last row of the final chunk                      */
-#define ORTHRUS_POOL_CLS 2  /* keeps the first row of the offset-0 chunk                  */
-#define ORTHRUS_POOL_NONE 3 /* writes keys/values only (cache-filling prefill chunk)      */
+#define ORTHRUS_POOL_MASK 7
+#define ORTHRUS_POOL_MEAN 0   /* S += sum of rows; emits S / W (Eq. (1)-(2), w = 1)           */
+#define ORTHRUS_POOL_LAST 1   /* keeps the last row of the final chunk                        */
+#define ORTHRUS_POOL_CLS 2    /* keeps the first row of the offset-0 chunk                    */
+#define ORTHRUS_POOL_NONE 3   /* writes keys/values only (cache-filling prefill chunk)        */
+#define ORTHRUS_POOL_WMEAN 4  /* S += sum of w_j * row_j with the batch's token_weights       */
+                              /* (Eq. (1)-(2)); emits S, L2-normalised (the weight sum W of   */
+                              /* Eq. (2) cancels in the L2 finish, so it is never formed)     */
+#define ORTHRUS_POOL_BUFFER 5 /* writes the final-normed rows to the batch's hidden buffer    */
+                              /* (the buffered arbitrary head); emits no embedding            */
 
 /* device error bits reported by orthrus_device_error() */
 #define ORTHRUS_DEVERR_PAGE 1 /* block-table entry outside [0, n_pages) on a used block     */
@@ -114,9 +121,15 @@ typedef struct orthrus_gen_chunk {
     int32_t seq, offset, len, flags;
 } orthrus_gen_chunk;
 
-/* The batch (HOST memory), type-sorted as in Section 3.2: token_ids holds the embedding chunks'
- * tokens in chunk order, then the generation prefill chunks' tokens in chunk order, then one
- * input token per decode row.  n_gen_chunks / gen_chunks may be 0 / NULL. */
+/* The batch (HOST memory, except `hidden`), type-sorted as in Section 3.2: token_ids holds the
+ * embedding chunks' tokens in chunk order, then the generation prefill chunks' tokens in chunk
+ * order, then one input token per decode row.  n_gen_chunks / gen_chunks may be 0 / NULL.
+ *   token_weights: HOST fp32, one weight per embedding-chunk token (same order as token_ids);
+ *     read for ORTHRUS_POOL_WMEAN chunks, whose weights must be finite and >= 0 (EDESC); may be
+ *     NULL when no chunk uses that head.
+ *   hidden: DEVICE fp32 [emb_kv n_seq][hidden_stride][d]: an ORTHRUS_POOL_BUFFER chunk of request
+ *     s writes its final-normed hidden rows to rows s * hidden_stride + offset .. + len - 1
+ *     (ECAPACITY if offset + len > hidden_stride); may be NULL when no chunk uses that head. */
 typedef struct orthrus_batch {
     int32_t n_chunks, n_decode;
     const orthrus_emb_chunk *chunks;
@@ -124,6 +137,9 @@ typedef struct orthrus_batch {
     const int32_t *token_ids;
     int32_t n_gen_chunks;
     const orthrus_gen_chunk *gen_chunks;
+    const float *token_weights;
+    float *hidden;
+    int32_t hidden_stride;
 } orthrus_batch;
 
 /* A paged KV cache (device), model dtype.  k_cache: [n_layers][n_pages][n_kv_heads][page][hd]
@@ -163,8 +179,9 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
  *   out_logits [n_logit_rows][vocab] fp32 device, n_logit_rows = (generation chunks flagged
  *            LAST) + n_decode: next-token logits of the last row of each final prompt chunk, in
  *            chunk order, then of each decode row.  May be NULL when n_logit_rows is 0.
- *   out_emb  [n_chunks][d] fp32 device: row i is written only if chunk i has ORTHRUS_CHUNK_LAST;
- *            it holds v / max(||v||_2, 1e-12) with v = S / W (mean) or S (last, CLS).
+ *   out_emb  [n_chunks][d] fp32 device: row i is written only if chunk i has ORTHRUS_CHUNK_LAST
+ *            and a head that emits; it holds v / max(||v||_2, 1e-12) with v = S / W (mean) or S
+ *            (weighted mean, last, CLS).
  *   workspace: device buffer of ws_bytes >= orthrus_workspace_bytes(...) for this batch.
  * Host-side validation (EINVAL, EDESC, EDUPSEQ, ECAPACITY) runs before anything is enqueued.
  * One step in flight per workspace.  Outputs are valid once the stream has synchronised. */

@@ -69,13 +69,18 @@ int orthrus_sched_create(const orthrus_sched_config *cfg, orthrus_sched **out);
 void orthrus_sched_destroy(orthrus_sched *s);
 
 /* Queue a request (arrival order = call order).  tokens: n token ids (host), copied; NULL stands
- * for n zeros (scheduling studies).  pool: ORTHRUS_POOL_MEAN / _LAST / _CLS.  EINVAL: id already
+ * for n zeros (scheduling studies).  pool: ORTHRUS_POOL_MEAN / _LAST / _CLS (buffered heads are
+ * left to callers of orthrus_step, which own the hidden buffer).  EINVAL: id already
  * live, n < 1, max_new < 1, bad pool; ECAPACITY: the request's reservation exceeds the block
  * table or the cache's pages (it could never be admitted). */
 int orthrus_sched_submit_embedding(orthrus_sched *s, int64_t id, const int32_t *tokens, int32_t n,
                                    int32_t pool);
 int orthrus_sched_submit_generation(orthrus_sched *s, int64_t id, const int32_t *prompt, int32_t n,
                                     int32_t max_new);
+/* A weighted-mean embedding request (ORTHRUS_POOL_WMEAN): weights holds one finite, non-negative
+ * weight per token (host, copied); EINVAL otherwise.  Other errors as above. */
+int orthrus_sched_submit_embedding_weighted(orthrus_sched *s, int64_t id, const int32_t *tokens,
+                                            const float *weights, int32_t n);
 
 /* One iteration's batch.  `batch` is ready for orthrus_step: chunk and row `seq` fields are cache
  * slots (embedding chunks in cache 0; prompt chunks and decode rows in cache 1, or 0 when shared)

@@ -29,6 +29,9 @@ ORTHRUS_POOL_MEAN = 0
 ORTHRUS_POOL_LAST = 1
 ORTHRUS_POOL_CLS = 2
 ORTHRUS_POOL_NONE = 3
+ORTHRUS_POOL_WMEAN = 4
+ORTHRUS_POOL_BUFFER = 5
+ORTHRUS_POOL_MASK = 7
 ORTHRUS_DEVERR_PAGE = 1
 ORTHRUS_DEVERR_ACC = 2
 
@@ -67,7 +70,8 @@ class orthrus_batch(Structure):
     _fields_ = [("n_chunks", c_int32), ("n_decode", c_int32),
                 ("chunks", POINTER(orthrus_emb_chunk)), ("rows", POINTER(orthrus_decode_row)),
                 ("token_ids", POINTER(c_int32)), ("n_gen_chunks", c_int32),
-                ("gen_chunks", POINTER(orthrus_gen_chunk))]
+                ("gen_chunks", POINTER(orthrus_gen_chunk)), ("token_weights", POINTER(c_float)),
+                ("hidden", c_void_p), ("hidden_stride", c_int32)]
 
 
 class orthrus_kv(Structure):
@@ -133,6 +137,8 @@ SIGNATURES = {
     "orthrus_sched_destroy": (None, [c_void_p]),
     "orthrus_sched_submit_embedding": (c_int, [c_void_p, c_int64, c_void_p, c_int32, c_int32]),
     "orthrus_sched_submit_generation": (c_int, [c_void_p, c_int64, c_void_p, c_int32, c_int32]),
+    "orthrus_sched_submit_embedding_weighted": (c_int, [c_void_p, c_int64, c_void_p, c_void_p,
+                                                        c_int32]),
     "orthrus_sched_next": (c_int, [c_void_p, POINTER(orthrus_sched_batch)]),
     "orthrus_sched_commit": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32),
                                      POINTER(c_int64), c_int32]),
@@ -229,6 +235,10 @@ def orthrus_sched_submit_embedding(s, rid, tokens, n, pool):
 
 def orthrus_sched_submit_generation(s, rid, prompt, n, max_new):
     return load().orthrus_sched_submit_generation(s, rid, prompt, n, max_new)
+
+
+def orthrus_sched_submit_embedding_weighted(s, rid, tokens, weights, n):
+    return load().orthrus_sched_submit_embedding_weighted(s, rid, tokens, weights, n)
 
 
 def orthrus_sched_next(s, out):

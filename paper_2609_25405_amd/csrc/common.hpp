@@ -149,19 +149,22 @@ struct PoolArgs {
     const float *pend;        // pending split-K slabs added to x first (npend of them, or none)
     size_t pend_stride;
     int npend;
+    const float *weights;     // [Te] per-token weights (weighted-mean chunks), or null
+    const int32_t *hid_rows;  // [Te] hidden-buffer row of each embedding token (-1: none), or null
+    float *hidden;            // buffered-head output [rows][d] fp32
     int n_chunks, Te, d;
     int n_emb_rows, n_lm;     // final-norm launch: embedding rows [0, n_emb_rows), lm_rows
     float eps;
     int *err;
 };
-// final RMSNorm: 1/rms of embedding rows [0, n_emb_rows), then the n_lm rows listed in lm_rows
-// normalised into act
+// final RMSNorm: 1/rms of embedding rows [0, n_emb_rows) (and the normalised row into the
+// hidden buffer for buffered-head tokens), then the n_lm rows listed in lm_rows normalised into act
 hipError_t launch_final_rows(int dtype, const PoolArgs &a, hipStream_t s);
 // greedy sampler: out[r] = first index of the largest logits[r][.] (NaN compares greatest)
 hipError_t launch_argmax(const float *logits, int rows, int vocab, int32_t *out, hipStream_t s);
 // incremental pooler update and finished embeddings.  Single-row heads (last token, CLS) take
-// their row's final norm themselves (adding npend slabs); with any_mean, mean-pooled chunks
-// are accumulated too and need launch_final_rows over their rows first.
-hipError_t launch_pool(const PoolArgs &a, bool any_mean, hipStream_t s);
+// their row's final norm themselves (adding npend slabs); with any_rows, mean, weighted-mean and
+// buffered chunks are handled too and need launch_final_rows over the embedding rows first.
+hipError_t launch_pool(const PoolArgs &a, bool any_rows, hipStream_t s);
 
 }  // namespace orthrus

@@ -165,6 +165,14 @@ __global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
     const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
     if (emb_row) {
         if (threadIdx.x == 0) a.inv_rms[r] = inv;
+        const int hr = a.hid_rows ? a.hid_rows[r] : -1;
+        if (hr >= 0) {
+            float *h = a.hidden + (size_t)hr * a.d;
+            for (int v = threadIdx.x; v < nv; v += 256) {
+                const float4 q = load4(x + 4 * v), g = load4(a.gain + 4 * v);
+                store4(h + 4 * v, float4{q.x * inv * g.x, q.y * inv * g.y, q.z * inv * g.z, q.w * inv * g.w});
+            }
+        }
         return;
     }
     T *y = (T *)a.act + (size_t)lm * a.d;
@@ -179,15 +187,18 @@ __device__ __forceinline__ bool chunk_state_ok(const int32_t *ch, const float *a
     return off == 0 || acc_w[seq] == (float)off;
 }
 
-// S update of Eq. (1) for mean pooling (w = 1).  Block = 64 columns x 4 row slices; grid =
-// (chunks, d / 64).  Needs the final-norm scales of the chunk's rows (final_rows_kernel).
+// S update of Eq. (1) for mean (w = 1) and weighted-mean pooling.  Block = 64 columns x 4 row
+// slices; grid = (chunks, d / 64).  Needs the final-norm scales of the chunk's rows
+// (final_rows_kernel).
 __global__ __launch_bounds__(256) void pool_accum_kernel(PoolArgs a) {
     __shared__ float part[4][64];
     const int ci = blockIdx.x;
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3], t0 = ch[4];
-    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
-    if (pool != ORTHRUS_POOL_MEAN) return;   // single-row heads are done by pool_rows_kernel
+    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK;
+    // single-row heads are done by pool_rows_kernel; buffered rows need no S
+    if (pool != ORTHRUS_POOL_MEAN && pool != ORTHRUS_POOL_WMEAN) return;
+    const float *w = pool == ORTHRUS_POOL_WMEAN ? a.weights + t0 : nullptr;
     if (!chunk_state_ok(ch, a.acc_w)) {
         if (blockIdx.y == 0 && threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_ACC);
         return;
@@ -196,7 +207,11 @@ __global__ __launch_bounds__(256) void pool_accum_kernel(PoolArgs a) {
     const float gc = a.gain[c];
     float *S = a.acc_sum + (size_t)seq * a.d + c;
     float s = 0.f;
-    for (int r = slice; r < len; r += 4) s += a.x[(size_t)(t0 + r) * a.d + c] * a.inv_rms[t0 + r];
+    if (w) {
+        for (int r = slice; r < len; r += 4) s += a.x[(size_t)(t0 + r) * a.d + c] * (a.inv_rms[t0 + r] * w[r]);
+    } else {
+        for (int r = slice; r < len; r += 4) s += a.x[(size_t)(t0 + r) * a.d + c] * a.inv_rms[t0 + r];
+    }
     part[slice][threadIdx.x & 63] = s;
     __syncthreads();
     if (slice == 0) {
@@ -205,23 +220,26 @@ __global__ __launch_bounds__(256) void pool_accum_kernel(PoolArgs a) {
     }
 }
 
-// W update of Eq. (2) and, for a request's final chunk, v / max(||v||, 1e-12), mean pooling
+// Token count W (Eq. (2) for w = 1; the offset check for every head) and, for a request's final
+// chunk, v / max(||v||, 1e-12) with v = S / W (mean) or S (weighted mean: the weight sum of
+// Eq. (2) cancels in the L2 finish).  Buffered chunks only advance W (and flag a state mismatch).
 __global__ __launch_bounds__(256) void pool_finish_kernel(PoolArgs a) {
     __shared__ float red[4];
     const int ci = blockIdx.x;
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3];
-    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
-    if (pool != ORTHRUS_POOL_MEAN) return;
+    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK;
+    if (pool != ORTHRUS_POOL_MEAN && pool != ORTHRUS_POOL_WMEAN && pool != ORTHRUS_POOL_BUFFER) return;
     const bool ok = chunk_state_ok(ch, a.acc_w);
+    if (!ok && pool == ORTHRUS_POOL_BUFFER && threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_ACC);
     __syncthreads();
     if (!ok) return;
     const float W = (off == 0 ? 0.f : a.acc_w[seq]) + (float)len;
     __syncthreads();  // every thread has read the old W
     if (threadIdx.x == 0) a.acc_w[seq] = W;
-    if (!(flags & ORTHRUS_CHUNK_LAST)) return;
+    if (!(flags & ORTHRUS_CHUNK_LAST) || pool == ORTHRUS_POOL_BUFFER) return;
     const float *S = a.acc_sum + (size_t)seq * a.d;
-    const float div = W;
+    const float div = pool == ORTHRUS_POOL_MEAN ? W : 1.f;
     float ss = 0.f;
     for (int i = threadIdx.x; i < a.d; i += 256) {
         const float v = S[i] / div;
@@ -243,9 +261,9 @@ __global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
     const int ci = blockIdx.x;
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3], t0 = ch[4];
-    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & 3;
+    const int pool = (flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK;
     const bool last = flags & ORTHRUS_CHUNK_LAST;
-    if (pool == ORTHRUS_POOL_NONE || pool == ORTHRUS_POOL_MEAN) return;
+    if (pool != ORTHRUS_POOL_LAST && pool != ORTHRUS_POOL_CLS) return;
     const float w_old = a.acc_w[seq];
     if (!(off == 0 || w_old == (float)off)) {
         if (threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_ACC);
@@ -373,10 +391,10 @@ hipError_t launch_final_rows(int dtype, const PoolArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_pool(const PoolArgs &a, bool any_mean, hipStream_t s) {
+hipError_t launch_pool(const PoolArgs &a, bool any_rows, hipStream_t s) {
     if (a.n_chunks <= 0) return hipSuccess;
     hipLaunchKernelGGL(pool_rows_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
-    if (any_mean) {
+    if (any_rows) {
         hipLaunchKernelGGL(pool_accum_kernel, dim3(a.n_chunks, a.d / 64), dim3(256), 0, s, a);
         hipLaunchKernelGGL(pool_finish_kernel, dim3(a.n_chunks), dim3(256), 0, s, a);
     }

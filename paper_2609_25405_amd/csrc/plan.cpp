@@ -10,6 +10,9 @@
 
 #include <algorithm>
 #include <array>
+#include <climits>
+#include <cmath>
+#include <cstring>
 #include <numeric>
 #include <set>
 #include <utility>
@@ -57,14 +60,21 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     std::set<std::pair<int, int>> seen;  // (namespace, seq)
     for (int i = 0; i < b.n_chunks; ++i) {
         const orthrus_emb_chunk &c = b.chunks[i];
-        const int pool = (c.flags >> ORTHRUS_POOL_SHIFT) & 3;
+        const int pool = (c.flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK;
         if (c.seq < 0 || c.seq >= ekv.n_seq || c.offset < 0 || c.len < 1) return ORTHRUS_EDESC;
-        if (c.flags & ~(ORTHRUS_CHUNK_LAST | (3 << ORTHRUS_POOL_SHIFT))) return ORTHRUS_EDESC;
+        if (c.flags & ~(ORTHRUS_CHUNK_LAST | (ORTHRUS_POOL_MASK << ORTHRUS_POOL_SHIFT))) return ORTHRUS_EDESC;
+        if (pool > ORTHRUS_POOL_BUFFER) return ORTHRUS_EDESC;
         if (pool == ORTHRUS_POOL_NONE && (c.flags & ORTHRUS_CHUNK_LAST)) return ORTHRUS_EDESC;
         if ((long long)c.offset + c.len > (long long)ekv.max_blocks * P) return ORTHRUS_ECAPACITY;
+        if (pool == ORTHRUS_POOL_BUFFER && (long long)c.offset + c.len > b.hidden_stride) return ORTHRUS_ECAPACITY;
         if (!seen.insert({0, c.seq}).second) return ORTHRUS_EDUPSEQ;
         Te += c.len;
+        p.any_mean |= pool == ORTHRUS_POOL_MEAN;
+        p.any_wmean |= pool == ORTHRUS_POOL_WMEAN;
+        p.any_buffer |= pool == ORTHRUS_POOL_BUFFER;
     }
+    if (p.any_buffer && !b.hidden) return ORTHRUS_EINVAL;
+    if (p.any_buffer && (long long)ekv.n_seq * b.hidden_stride > INT32_MAX) return ORTHRUS_ECAPACITY;
     for (int i = 0; i < b.n_gen_chunks; ++i) {
         const orthrus_gen_chunk &c = b.gen_chunks[i];
         if (c.seq < 0 || c.seq >= gkv.n_seq || c.offset < 0 || c.len < 1) return ORTHRUS_EDESC;
@@ -90,6 +100,19 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     for (int t = 0; t < p.T; ++t) {
         const int v = t < p.Te ? emb.cfg.vocab : gen.cfg.vocab;
         if (b.token_ids[t] < 0 || b.token_ids[t] >= v) return ORTHRUS_EDESC;
+    }
+    if (p.any_wmean) {
+        if (!b.token_weights) return ORTHRUS_EDESC;
+        int t = 0;
+        for (int i = 0; i < b.n_chunks; ++i) {
+            const orthrus_emb_chunk &c = b.chunks[i];
+            if (((c.flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK) == ORTHRUS_POOL_WMEAN)
+                for (int k = 0; k < c.len; ++k) {
+                    const float w = b.token_weights[t + k];
+                    if (!std::isfinite(w) || w < 0.f) return ORTHRUS_EDESC;
+                }
+            t += c.len;
+        }
     }
 
     // chunk table entries of both chunk kinds: {seq, offset, len, flags, first token}
@@ -196,7 +219,25 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     p.off_rows = p.off_chunks + kChunkInts * n_all;
     p.off_items = p.off_rows + kRowInts * p.D;
     p.off_lm = p.off_items + (int)items.size();
-    p.meta.assign(p.off_lm + p.n_lm, 0);
+    int end = p.off_lm + p.n_lm;
+    if (p.any_wmean) {
+        p.off_wts = end;
+        end += p.Te;
+    }
+    if (p.any_buffer) {
+        p.off_hid = end;
+        end += p.Te;
+    }
+    p.meta.assign(end, 0);
+    if (p.any_wmean) std::memcpy(&p.meta[p.off_wts], b.token_weights, (size_t)p.Te * 4);
+    if (p.any_buffer) {
+        for (int i = 0, t = 0; i < b.n_chunks; t += b.chunks[i].len, ++i) {
+            const orthrus_emb_chunk &c = b.chunks[i];
+            const bool buf = ((c.flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK) == ORTHRUS_POOL_BUFFER;
+            for (int k = 0; k < c.len; ++k)
+                p.meta[p.off_hid + t + k] = buf ? c.seq * b.hidden_stride + c.offset + k : -1;
+        }
+    }
     std::copy(b.token_ids, b.token_ids + p.T, p.meta.begin() + p.off_tok);
     int lm = 0;
     for (int i = 0; i < n_all; ++i) {

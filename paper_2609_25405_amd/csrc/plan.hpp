@@ -46,10 +46,14 @@ struct StepPlan {
     bool shared_kv = true;
     int n_prefill = 0, n_decode_items = 0, n_partials = 0, n_split_rows = 0;
     int n_lm = 0;  // rows that get logits: last rows of final prompt chunks, then decode rows
-    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows
+    // heads in the batch that need every embedding row's final norm (mean, weighted mean,
+    // buffered), and the optional per-token arrays they read
+    bool any_mean = false, any_wmean = false, any_buffer = false;
+    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows, then
+    // (weighted mean) fp32 weights[Te] and (buffered head) hidden-buffer row[Te] (-1: none)
     std::vector<int32_t> meta;
     int off_tok = 0, off_pos = 0, off_seq = 0, off_chunks = 0, off_rows = 0, off_items = 0,
-        off_lm = 0;
+        off_lm = 0, off_wts = -1, off_hid = -1;
 };
 
 int validate_config(const orthrus_config &c);

@@ -9,6 +9,7 @@
 // across iterations and reset when their queue is empty at the start of one.
 #include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstring>
 #include <deque>
 #include <memory>
@@ -30,6 +31,7 @@ struct Req {
     int32_t cache = 0, slot = -1;
     std::vector<int32_t> pages;
     std::vector<int32_t> tokens;  // empty: zeros
+    std::vector<float> weights;   // weighted-mean requests: one per token
     int32_t last_token = 0;
     int64_t batch_iter = -1;      // iteration whose batch holds this request
     int32_t remaining() const { return n - done; }
@@ -56,6 +58,7 @@ struct orthrus_sched {
     std::vector<orthrus_gen_chunk> gchunks;
     std::vector<orthrus_decode_row> rows;
     std::vector<int32_t> tokens, row_tokens, table_rows;
+    std::vector<float> token_weights;
     std::vector<int64_t> chunk_ids, gen_ids, row_ids, logit_ids, finishing_ids;
     std::vector<Req *> logit_reqs, finishing;
     std::string picks;
@@ -207,6 +210,21 @@ int orthrus_sched_submit_embedding(orthrus_sched *s, int64_t id, const int32_t *
     return submit(s, std::move(r), tokens);
 }
 
+int orthrus_sched_submit_embedding_weighted(orthrus_sched *s, int64_t id, const int32_t *tokens,
+                                            const float *weights, int32_t n) {
+    if (!s || !weights || n < 1) return ORTHRUS_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+        if (!std::isfinite(weights[i]) || weights[i] < 0.f) return ORTHRUS_EINVAL;
+    std::unique_ptr<Req> r(new (std::nothrow) Req);
+    if (!r) return ORTHRUS_EINVAL;
+    r->id = id;
+    r->emb = true;
+    r->n = n;
+    r->pool = ORTHRUS_POOL_WMEAN;
+    r->weights.assign(weights, weights + n);
+    return submit(s, std::move(r), tokens);
+}
+
 int orthrus_sched_submit_generation(orthrus_sched *s, int64_t id, const int32_t *prompt, int32_t n,
                                     int32_t max_new) {
     if (!s) return ORTHRUS_EINVAL;
@@ -226,6 +244,7 @@ int orthrus_sched_next(orthrus_sched *s, orthrus_sched_batch *out) {
     s->gchunks.clear();
     s->rows.clear();
     s->tokens.clear();
+    s->token_weights.clear();
     s->row_tokens.clear();
     s->table_rows.clear();
     s->chunk_ids.clear();
@@ -304,6 +323,17 @@ int orthrus_sched_next(orthrus_sched *s, orthrus_sched_batch *out) {
         else s->tokens.insert(s->tokens.end(), r.tokens.begin() + c.offset, r.tokens.begin() + c.offset + c.len);
     }
     for (Req *r : decoded) s->tokens.push_back(r->last_token);
+    // per-token weights of the embedding chunks, when a weighted-mean request is in the batch
+    bool any_weighted = false;
+    for (size_t i = 0; i < s->chunks.size(); ++i) any_weighted |= !s->reqs[s->chunk_ids[i]]->weights.empty();
+    if (any_weighted)
+        for (size_t i = 0; i < s->chunks.size(); ++i) {
+            const Req &r = *s->reqs[s->chunk_ids[i]];
+            const orthrus_emb_chunk &c = s->chunks[i];
+            if (r.weights.empty()) s->token_weights.insert(s->token_weights.end(), c.len, 1.f);
+            else s->token_weights.insert(s->token_weights.end(), r.weights.begin() + c.offset,
+                                         r.weights.begin() + c.offset + c.len);
+        }
     // logits rows: final prompt chunks, then decode rows
     for (Req *r : decoded) s->logit_reqs.push_back(r);
     for (Req *r : s->logit_reqs) s->logit_ids.push_back(r->id);
@@ -317,6 +347,7 @@ int orthrus_sched_next(orthrus_sched *s, orthrus_sched_batch *out) {
     out->batch.token_ids = s->tokens.data();
     out->batch.n_gen_chunks = (int32_t)s->gchunks.size();
     out->batch.gen_chunks = s->gchunks.data();
+    out->batch.token_weights = any_weighted ? s->token_weights.data() : nullptr;
     out->chunk_ids = s->chunk_ids.data();
     out->gen_chunk_ids = s->gen_ids.data();
     out->row_ids = s->row_ids.data();

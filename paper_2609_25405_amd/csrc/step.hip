@@ -192,7 +192,8 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
     const size_t dec_items = (size_t)max_decode * nkv * splits;
     const size_t meta = 3 * (size_t)max_tokens + kChunkInts * (size_t)max_chunks +
                         kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items) +
-                        (size_t)max_chunks + max_decode;  // rows that get logits
+                        (size_t)max_chunks + max_decode +  // rows that get logits
+                        2 * (size_t)max_tokens;            // token weights, hidden-buffer rows
     return make_layout(m, max_tokens, meta, dec_items).total;
 }
 
@@ -478,17 +479,18 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     pa.d = d;
     pa.eps = c.rms_eps;
     pa.err = err;
-    // Only mean pooling needs the final norm of every embedding row; single-row heads normalise
-    // their one row inside the pooler.
-    bool any_mean = false;
-    for (int i = 0; i < batch->n_chunks; ++i)
-        any_mean |= ((batch->chunks[i].flags >> ORTHRUS_POOL_SHIFT) & 3) == ORTHRUS_POOL_MEAN;
-    pa.n_emb_rows = any_mean ? Te : 0;
+    // Mean, weighted-mean and buffered heads need the final norm of every embedding row;
+    // single-row heads normalise their one row inside the pooler.
+    const bool any_rows = p.any_mean || p.any_wmean || p.any_buffer;
+    pa.weights = p.any_wmean ? (const float *)(meta + p.off_wts) : nullptr;
+    pa.hid_rows = p.any_buffer ? meta + p.off_hid : nullptr;
+    pa.hidden = batch->hidden;
+    pa.n_emb_rows = any_rows ? Te : 0;
     pa.n_lm = p.n_lm;
     if (pa.n_emb_rows + pa.n_lm > 0) RUN("final_norm", launch_final_rows(dt, pa, s));
     // the embedding rows' pending slabs were added by the final norm when it covered them
-    if (any_mean) pa.npend = 0;
-    if (p.n_chunks > 0) RUN("pool", launch_pool(pa, any_mean, s));
+    if (any_rows) pa.npend = 0;
+    if (p.n_chunks > 0) RUN("pool", launch_pool(pa, any_rows, s));
     if (p.n_lm > 0) {
         GemmArgs ga{};
         ga.A = act;

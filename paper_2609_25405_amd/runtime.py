@@ -15,7 +15,8 @@ import torch
 from . import _abi as A
 
 POOL_CODES = {"mean": A.ORTHRUS_POOL_MEAN, "last": A.ORTHRUS_POOL_LAST,
-              "cls": A.ORTHRUS_POOL_CLS, "none": A.ORTHRUS_POOL_NONE}
+              "cls": A.ORTHRUS_POOL_CLS, "none": A.ORTHRUS_POOL_NONE,
+              "wmean": A.ORTHRUS_POOL_WMEAN, "buffer": A.ORTHRUS_POOL_BUFFER}
 
 
 def _vp(t: Optional[torch.Tensor]):
@@ -171,18 +172,36 @@ class PackedBatch:
         if self._ids.shape != (n_ids,):
             raise A.OrthrusError(A.ORTHRUS_EDESC, "token_ids length")
         self.n_logit_rows = sum(1 for c in gen if c.last) + nd
+        # per-token weights of the embedding chunks (weighted-mean heads), bounds-checked here
+        tw = getattr(batch, "token_weights", None)
+        n_emb = sum(int(c.len) for c in batch.chunks)
+        self._w = None
+        wptr = None
+        if tw is not None:
+            self._w = np.ascontiguousarray(tw, dtype=np.float32)
+            if self._w.shape != (n_emb,):
+                raise A.OrthrusError(A.ORTHRUS_EDESC, "token_weights length")
+            wptr = self._w.ctypes.data_as(POINTER(ctypes.c_float))
         self.c = A.orthrus_batch(nc, nd, ctypes.cast(self._chunks, POINTER(A.orthrus_emb_chunk)),
                                  ctypes.cast(self._rows, POINTER(A.orthrus_decode_row)),
                                  self._ids.ctypes.data_as(POINTER(c_int32)), ng,
-                                 ctypes.cast(self._gen, POINTER(A.orthrus_gen_chunk)))
+                                 ctypes.cast(self._gen, POINTER(A.orthrus_gen_chunk)), wptr, None,
+                                 int(getattr(batch, "hidden_stride", 0)))
 
 
 def step(emb: DeviceModel, gen: DeviceModel, batch, emb_kv: DeviceKV, gen_kv: DeviceKV,
          acc_sum: torch.Tensor, acc_w: torch.Tensor, out_logits: Optional[torch.Tensor],
          out_emb: Optional[torch.Tensor], ws: Workspace, stream: Optional[int] = None,
-         packed: Optional[PackedBatch] = None) -> None:
-    """Enqueue one orthrus_step on `stream` (default: torch's current stream); raises on error."""
+         packed: Optional[PackedBatch] = None, hidden: Optional[torch.Tensor] = None) -> None:
+    """Enqueue one orthrus_step on `stream` (default: torch's current stream); raises on error.
+    ``hidden``: fp32 [n_seq][hidden_stride][d] buffer that buffered-head chunks fill."""
     pb = packed if packed is not None else PackedBatch(batch)
+    if hidden is not None:
+        if hidden.dtype != torch.float32 or not hidden.is_contiguous() or hidden.dim() != 3 or \
+                hidden.shape[0] < emb_kv.n_seq or hidden.shape[1] != pb.c.hidden_stride or \
+                hidden.shape[2] != emb.cfg.d_model:
+            raise A.OrthrusError(A.ORTHRUS_EINVAL, "hidden buffer shape")
+        pb.c.hidden = hidden.data_ptr()
     ekv, gkv = emb_kv.struct(), (emb_kv.struct() if gen_kv is emb_kv else gen_kv.struct())
     s = current_stream() if stream is None else stream
     rc = A.orthrus_step(emb.handle, gen.handle, byref(pb.c), byref(ekv), byref(gkv), _vp(acc_sum),
@@ -271,8 +290,16 @@ class Scheduler:
             raise A.OrthrusError(A.ORTHRUS_EINVAL, "token count")
         return a, c_void_p(a.ctypes.data)
 
-    def submit_embedding(self, rid: int, n: int, tokens=None, pool: str = "mean") -> None:
+    def submit_embedding(self, rid: int, n: int, tokens=None, pool: str = "mean",
+                         weights=None) -> None:
         a, p = self._ids(tokens, n)
+        if pool == "wmean":
+            w = np.ascontiguousarray(weights, np.float32)
+            if w.shape != (n,):
+                raise A.OrthrusError(A.ORTHRUS_EINVAL, "weight count")
+            _check(A.orthrus_sched_submit_embedding_weighted(self.handle, rid, p, c_void_p(w.ctypes.data), n),
+                   "orthrus_sched_submit_embedding_weighted")
+            return
         _check(A.orthrus_sched_submit_embedding(self.handle, rid, p, n, POOL_CODES[pool]),
                "orthrus_sched_submit_embedding")
 

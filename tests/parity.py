@@ -101,26 +101,45 @@ class Pair:
         pre = [(_bits(self.dkv_e.k).clone(), _bits(self.dkv_e.v_by_position).clone())] if check_kv else None
         if check_kv and not self.shared_kv:
             pre.append((_bits(self.dkv_g.k).clone(), _bits(self.dkv_g.v_by_position).clone()))
+        hidden = None
+        if any(c.pool == "buffer" for c in batch.chunks):
+            hidden = torch.full((self.dkv_e.n_seq, batch.hidden_stride, cfg.d_model), float("nan"),
+                                device="cuda")
         R.step(self.dm_e, self.dm_g, batch, self.dkv_e, self.dkv_g, self.acc_sum, self.acc_w,
-               logits, out_emb, self.ws)
+               logits, out_emb, self.ws, hidden=hidden)
         torch.cuda.synchronize()
         assert self.ws.device_error() == 0
         rec = {}
         if nd:
             rec["logits"] = assert_vectors_close(logits[:nd].cpu().numpy(), ref["logits"], self.dtype,
                                                  "logits")
-        last = [i for i, c in enumerate(batch.chunks) if c.last]
+        last = [i for i, c in enumerate(batch.chunks) if c.last and c.pool != "buffer"]
         if last:
             g = out_emb[last].cpu().numpy()
-            rec["emb"] = assert_vectors_close(g, ref["out_emb"][last], self.dtype, "embedding")
-            np.testing.assert_allclose(np.linalg.norm(g, axis=1), 1.0, rtol=1e-5)
-        untouched = [i for i, c in enumerate(batch.chunks) if not c.last]
+            o = ref["out_emb"][last]
+            zero = np.all(o == 0, axis=1)     # weighted mean with all-zero weights: zero vector
+            assert np.all(g[zero] == 0), "zero embedding expected"
+            if (~zero).any():
+                rec["emb"] = assert_vectors_close(g[~zero], o[~zero], self.dtype, "embedding")
+                np.testing.assert_allclose(np.linalg.norm(g[~zero], axis=1), 1.0, rtol=1e-5)
+        untouched = [i for i, c in enumerate(batch.chunks) if not c.last or c.pool == "buffer"]
         if untouched:
             assert torch.isnan(out_emb[untouched]).all(), "out_emb rows of non-final chunks written"
+        if hidden is not None:
+            h = hidden.cpu().numpy()
+            mask = np.zeros(h.shape[:2], bool)
+            for i, c in enumerate(batch.chunks):
+                if c.pool == "buffer":
+                    mask[c.seq, c.offset:c.offset + c.len] = True
+                    rec.setdefault("hidden", [])
+                    rec["hidden"].append(assert_vectors_close(h[c.seq, c.offset:c.offset + c.len],
+                                                              ref["hidden"][i], self.dtype,
+                                                              "buffered hidden rows"))
+            assert np.isnan(h[~mask]).all(), "hidden-buffer rows outside the buffered chunks written"
         # pooling state: W exact, S per request close (rows that hold a state)
         W_gpu = self.acc_w.cpu().numpy().astype(np.float64)
         np.testing.assert_array_equal(W_gpu, ref["acc_w"])
-        pooled = sorted({c.seq for c in batch.chunks if c.pool != "none"})
+        pooled = sorted({c.seq for c in batch.chunks if c.pool not in ("none", "buffer")})
         live = [s for s in pooled if np.any(ref["acc_sum"][s] != 0)]
         if live:
             rec["acc"] = assert_vectors_close(self.acc_sum[live].cpu().numpy(), ref["acc_sum"][live],

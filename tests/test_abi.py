@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = P.load()
     names = header_functions()
     assert [os.path.basename(h) for h in HEADERS] == ["orthrus.h", "orthrus_sched.h"]
-    assert len(names) == 11 + 12
+    assert len(names) == 11 + 13
     for n in names:
         assert hasattr(lib, n), n
         assert n in A.SIGNATURES, n
@@ -49,8 +49,9 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(A.orthrus_decode_row) == 8
     assert ctypes.sizeof(A.orthrus_kv) == 3 * 8 + 3 * 4 + 4
     assert ctypes.sizeof(A.orthrus_gen_chunk) == 16
-    # n_chunks, n_decode, 3 pointers, n_gen_chunks (+4 bytes of padding), 1 pointer
-    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8 + 8 + 8
+    # n_chunks, n_decode, 3 pointers, n_gen_chunks (+4 bytes of padding), 3 pointers,
+    # hidden_stride (+4 bytes of padding)
+    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8 + 8 + 3 * 8 + 8
     assert A.orthrus_batch.gen_chunks.offset == 40
 
 
@@ -141,6 +142,19 @@ def test_host_validation_matches_oracle_contract():
     big2 = ids[:6].copy()
     big2[5] = cfg.vocab
     bad.append(Batch([EmbChunk(0, 0, 2, False)], [], big2, [GenChunk(1, 0, 4, True)]))
+    # weighted-mean and buffered heads
+    neg = np.ones(8, np.float32)
+    neg[3] = -0.5
+    nan = np.ones(8, np.float32)
+    nan[6] = np.nan
+    bad += [
+        Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids[:8]),
+        Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids[:8], token_weights=neg),
+        Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids[:8], token_weights=nan),
+        Batch([EmbChunk(0, 0, 8, True, "wmean")], [], ids[:8], token_weights=neg[:7]),
+        Batch([EmbChunk(0, 0, 8, True, "buffer")], [], ids[:8], hidden_stride=7),
+        Batch([EmbChunk(0, 4, 8, True, "buffer")], [], ids[:8], hidden_stride=11),
+    ]
     okv = OracleKV.from_paged(pk)
     t = R.torch
     acc, accw = t.zeros((6, cfg.d_model)), t.zeros(6)
@@ -326,3 +340,23 @@ def test_sample_greedy_argument_checks():
     assert A.orthrus_sample_greedy(None, 0, 5, None, None) == A.ORTHRUS_OK
     with pytest.raises(A.OrthrusError):
         R.sample_greedy(lg.double(), out)
+
+
+def test_unknown_pooling_codes_and_missing_hidden_buffer():
+    cfg, W, m, pk, kv = _cpu_setup()
+    t = R.torch
+    ids = draw_tokens(1, 0, 8, cfg.vocab)
+    acc, accw = t.zeros((6, cfg.d_model)), t.zeros(6)
+    emb = t.zeros((1, cfg.d_model))
+    ws = type("WS", (), {"buf": t.zeros(64, dtype=t.uint8), "nbytes": 64})()
+    for code in (6, 7):
+        pb = R.PackedBatch(Batch([EmbChunk(0, 0, 8, True)], [], ids))
+        pb._chunks[0].flags = 1 | (code << A.ORTHRUS_POOL_SHIFT)
+        with pytest.raises(A.OrthrusError) as e:
+            R.step(m, m, None, kv, kv, acc, accw, None, emb, ws, packed=pb)
+        assert e.value.code == A.ORTHRUS_EDESC
+    # a buffered chunk without a buffer pointer
+    b = Batch([EmbChunk(0, 0, 8, True, "buffer")], [], ids, hidden_stride=8)
+    with pytest.raises(A.OrthrusError) as e:
+        R.step(m, m, b, kv, kv, acc, accw, None, emb, ws)
+    assert e.value.code == A.ORTHRUS_EINVAL
