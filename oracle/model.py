@@ -96,27 +96,51 @@ def _split_qkv(cfg, qkv: np.ndarray):
     return q, k, v
 
 
-def mlp(layer, b: np.ndarray) -> np.ndarray:
-    gate = b @ np.asarray(layer["w_gate"], F64).T
-    up = b @ np.asarray(layer["w_up"], F64).T
-    return (silu(gate) * up) @ np.asarray(layer["w_down"], F64).T
+def lora_delta(x: np.ndarray, A, B, scale: float) -> np.ndarray:
+    """Low-rank update of a projection's output: scale * (x A^T) B^T, with A [r][in], B [out][r]
+    (the adapted projection computes x W^T + scale * x A^T B^T, i.e. x (W + scale B A)^T)."""
+    return scale * ((np.asarray(x, F64) @ np.asarray(A, F64).T) @ np.asarray(B, F64).T)
 
 
-def forward_full(cfg, weights, ids) -> np.ndarray:
-    """Final-normed hidden states H[n, d] of one request of tokens ids, positions 0..n-1."""
+def project(x: np.ndarray, W, layer_lora, site: str, scale: float, which: int = 1) -> np.ndarray:
+    """x W^T, plus the adapter's low-rank update when the adapter covers `site` (layer_lora[site]
+    = (A, B) or, for gate_up, (A, B_gate, B_up): `which` picks B_gate (1) or B_up (2))."""
+    y = np.asarray(x, F64) @ np.asarray(W, F64).T
+    ab = None if layer_lora is None else layer_lora.get(site)
+    if ab is not None:
+        y = y + lora_delta(x, ab[0], ab[which], scale)
+    return y
+
+
+def mlp(layer, b: np.ndarray, layer_lora=None, scale: float = 0.0) -> np.ndarray:
+    gate = project(b, layer["w_gate"], layer_lora, "gate_up", scale, 1)
+    up = project(b, layer["w_up"], layer_lora, "gate_up", scale, 2)
+    return project(silu(gate) * up, layer["w_down"], layer_lora, "down", scale)
+
+
+def _lora_layers(weights, lora):
+    if lora is None:
+        return [None] * len(weights["layers"]), 0.0
+    return lora["layers"], float(lora["scale"])
+
+
+def forward_full(cfg, weights, ids, lora=None) -> np.ndarray:
+    """Final-normed hidden states H[n, d] of one request of tokens ids, positions 0..n-1, through
+    the base model or, with `lora`, the base model plus that adapter's low-rank updates."""
     ids = np.asarray(ids, np.int64)
     n = ids.shape[0]
     pos = np.arange(n)
     x = np.asarray(weights["tok_emb"], F64)[ids]
-    for layer in weights["layers"]:
+    lls, sc = _lora_layers(weights, lora)
+    for layer, ll in zip(weights["layers"], lls):
         a = rmsnorm(x, layer["attn_norm"], cfg.rms_eps)
-        q, k, v = _split_qkv(cfg, a @ np.asarray(layer["w_qkv"], F64).T)
+        q, k, v = _split_qkv(cfg, project(a, layer["w_qkv"], ll, "qkv", sc))
         q = rope_rotate(q, pos, cfg.rope_base)
         k = rope_rotate(k, pos, cfg.rope_base)
         o = causal_gqa_attention(q, k, v, pos, pos)
-        x = x + o @ np.asarray(layer["w_o"], F64).T
+        x = x + project(o.reshape(n, -1), layer["w_o"], ll, "o", sc)
         b = rmsnorm(x, layer["mlp_norm"], cfg.rms_eps)
-        x = x + mlp(layer, b)
+        x = x + mlp(layer, b, ll, sc)
     return rmsnorm(x, weights["final_norm"], cfg.rms_eps)
 
 
@@ -143,9 +167,9 @@ def pool_single_pass(H: np.ndarray, head: str, weights=None) -> np.ndarray:
     raise ValueError(f"unknown pooling head {head!r}")
 
 
-def embed_single_pass(cfg, weights, ids, head: str, token_weights=None) -> np.ndarray:
-    """Unchunked embedding: forward, pool, L2-normalise."""
-    return l2_normalize(pool_single_pass(forward_full(cfg, weights, ids), head, token_weights))
+def embed_single_pass(cfg, weights, ids, head: str, token_weights=None, lora=None) -> np.ndarray:
+    """Unchunked embedding: forward (optionally through a LoRA adapter), pool, L2-normalise."""
+    return l2_normalize(pool_single_pass(forward_full(cfg, weights, ids, lora), head, token_weights))
 
 
 def lm_logits(weights, h: np.ndarray) -> np.ndarray:

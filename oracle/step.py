@@ -37,6 +37,10 @@ Readings taken where the paper is silent (also listed in the design notes):
   A = [A; H]): the chunk's final-normed hidden rows are returned for buffer rows
   seq * hidden_stride + offset .. + len - 1; W counts tokens as for every pooled chunk, and no
   embedding is emitted (the caller applies its head to the buffer);
+* LoRA (the shared-backbone deployment the paper evaluates: the embedding model is the
+  generator plus a low-rank adapter): chunk i of the embedding slice may name adapter
+  ``chunk_adapter[i]`` of the embedding model (-1: the base model); every adapted projection
+  then computes x W^T + scale (x A^T) B^T.  At most four distinct adapters per batch;
 * a generation prefill chunk (seq, offset, len, last) runs through the generator
   and its cache like a decode row of ``len`` tokens at positions offset ..
   offset+len-1; only the final chunk of a prompt (last) emits logits, for its
@@ -50,7 +54,10 @@ from typing import Dict, Optional, Tuple
 import numpy as np
 
 from .model import (F64, rmsnorm, rope_rotate, causal_gqa_attention, mlp, _split_qkv,
-                    l2_normalize, lm_logits)
+                    l2_normalize, lm_logits, project, _lora_layers)
+
+# most distinct adapters the embedding chunks of one batch may use
+MAX_STEP_ADAPTERS = 4
 
 
 class StepError(Exception):
@@ -95,22 +102,24 @@ class OracleKV:
 
 
 def _forward_cached(cfg, weights, kv: OracleKV, seq: int, ids: np.ndarray,
-                    positions: np.ndarray) -> np.ndarray:
-    """Final-normed hidden rows of one request's new tokens, attending through the cache."""
+                    positions: np.ndarray, lora=None) -> np.ndarray:
+    """Final-normed hidden rows of one request's new tokens, attending through the cache (and
+    through the adapter `lora`, if given, at every adapted projection)."""
     x = np.asarray(weights["tok_emb"], F64)[np.asarray(ids, np.int64)]
     n_keys = int(positions[-1]) + 1
     key_pos = np.arange(n_keys)
+    lls, sc = _lora_layers(weights, lora)
     for l, layer in enumerate(weights["layers"]):
         a = rmsnorm(x, layer["attn_norm"], cfg.rms_eps)
-        q, k, v = _split_qkv(cfg, a @ np.asarray(layer["w_qkv"], F64).T)
+        q, k, v = _split_qkv(cfg, project(a, layer["w_qkv"], lls[l], "qkv", sc))
         q = rope_rotate(q, positions, cfg.rope_base)
         k = rope_rotate(k, positions, cfg.rope_base)
         kv.write(l, seq, positions, k, v)
         K, V = kv.read(l, seq, n_keys)
         o = causal_gqa_attention(q, K, V, positions, key_pos)
-        x = x + o @ np.asarray(layer["w_o"], F64).T
+        x = x + project(o.reshape(len(ids), -1), layer["w_o"], lls[l], "o", sc)
         b = rmsnorm(x, layer["mlp_norm"], cfg.rms_eps)
-        x = x + mlp(layer, b)
+        x = x + mlp(layer, b, lls[l], sc)
     return rmsnorm(x, weights["final_norm"], cfg.rms_eps)
 
 
@@ -161,6 +170,13 @@ def validate(emb, gen, batch, emb_kv: OracleKV, gen_kv: OracleKV) -> None:
         raise StepError("desc", "logits need a model with an LM head")
     if n_emb and ((ids[:n_emb] < 0).any() or (ids[:n_emb] >= emb_cfg.vocab).any()):
         raise StepError("desc", "chunk token id out of range")
+    ca = getattr(batch, "chunk_adapter", None)
+    if ca is not None:
+        n_ad = len(emb[1].get("adapters") or [])
+        if len(ca) != len(batch.chunks) or any(not (-1 <= int(a) < n_ad) for a in ca):
+            raise StepError("desc", "chunk adapter index out of range")
+        if len({int(a) for a in ca if a >= 0}) > MAX_STEP_ADAPTERS:
+            raise StepError("capacity", f"more than {MAX_STEP_ADAPTERS} adapters in one batch")
     if any(c.pool == "wmean" for c in batch.chunks):
         w = getattr(batch, "token_weights", None)
         if w is None or np.asarray(w).shape != (n_emb,):
@@ -194,6 +210,8 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
     out_emb = np.full((len(batch.chunks), d), np.nan, F64)
     ids = np.asarray(batch.token_ids, np.int64)
     tw = getattr(batch, "token_weights", None)
+    ca = getattr(batch, "chunk_adapter", None)
+    adapters = emb_w.get("adapters") or []
     hidden = {}
     t = 0
     for i, c in enumerate(batch.chunks):
@@ -201,7 +219,8 @@ def step_oracle(emb: Tuple, gen: Tuple, batch, emb_kv: OracleKV, gen_kv: OracleK
             raise StepError("device", f"seq {c.seq}: accumulator holds {W[c.seq]} tokens, "
                                       f"chunk starts at {c.offset}")
         pos = np.arange(c.offset, c.offset + c.len)
-        H = _forward_cached(emb_cfg, emb_w, emb_kv, c.seq, ids[t:t + c.len], pos)
+        lora = adapters[int(ca[i])] if ca is not None and int(ca[i]) >= 0 else None
+        H = _forward_cached(emb_cfg, emb_w, emb_kv, c.seq, ids[t:t + c.len], pos, lora)
         w = None if tw is None else np.asarray(tw[t:t + c.len], F64)
         t += c.len
         if c.pool == "none":

@@ -603,3 +603,122 @@ def test_weighted_and_buffered_contract_errors():
     pk.reserve(1, 4)
     kv = OracleKV.from_paged(pk)
     step_oracle((cfg, W), (cfg, W), ok, kv, kv, S, Wc)
+
+
+# ---------------------------------------------------------------------------
+# LoRA on the embedding slice (the shared-backbone deployment: generator + adapter)
+# ---------------------------------------------------------------------------
+def _merged(W, lora):
+    """Base weights with every adapted projection replaced by W + scale * B A (built here from
+    the adapter's matrices, independently of the oracle's low-rank path)."""
+    s = lora["scale"]
+    out = {k: v for k, v in W.items() if k != "layers"}
+    out["layers"] = []
+    for lw, ll in zip(W["layers"], lora["layers"]):
+        m = dict(lw)
+        if "qkv" in ll:
+            A, B = ll["qkv"]
+            m["w_qkv"] = np.asarray(lw["w_qkv"], np.float64) + s * (np.asarray(B, np.float64) @ A)
+        if "o" in ll:
+            A, B = ll["o"]
+            m["w_o"] = np.asarray(lw["w_o"], np.float64) + s * (np.asarray(B, np.float64) @ A)
+        if "gate_up" in ll:
+            A, Bg, Bu = ll["gate_up"]
+            m["w_gate"] = np.asarray(lw["w_gate"], np.float64) + s * (np.asarray(Bg, np.float64) @ A)
+            m["w_up"] = np.asarray(lw["w_up"], np.float64) + s * (np.asarray(Bu, np.float64) @ A)
+        if "down" in ll:
+            A, B = ll["down"]
+            m["w_down"] = np.asarray(lw["w_down"], np.float64) + s * (np.asarray(B, np.float64) @ A)
+        out["layers"].append(m)
+    return out
+
+
+@pytest.mark.parametrize("sites", [("qkv", "o", "gate_up", "down"), ("qkv",), ("o", "down"), ("gate_up",)])
+def test_lora_equals_merged_weights(sites):
+    from workload import make_lora
+    cfg = micro_config()
+    W = sharp_weights(cfg, 51)
+    lora = make_lora(cfg, 51, rank=4, sites=sites)
+    ids = draw_tokens(10, 1, 17, cfg.vocab)
+    got = oracle.forward_full(cfg, W, ids, lora)
+    want = oracle.forward_full(cfg, _merged(W, lora), ids)
+    np.testing.assert_allclose(got, want, rtol=1e-11, atol=1e-12)
+    # the update is not negligible: the adapted model differs from the base one
+    base = oracle.forward_full(cfg, W, ids)
+    assert np.abs(got - base).max() > 0.05 * np.abs(base).max()
+
+
+def test_lora_with_zero_b_is_the_base_model():
+    from workload import make_lora
+    cfg = micro_config()
+    W = sharp_weights(cfg, 53)
+    lora = make_lora(cfg, 53, rank=4, std_b=0.0)
+    ids = draw_tokens(10, 2, 13, cfg.vocab)
+    np.testing.assert_array_equal(oracle.forward_full(cfg, W, ids, lora), oracle.forward_full(cfg, W, ids))
+
+
+def test_lora_chunks_in_a_mixed_batch_equal_each_request_alone():
+    """Two adapters and the base model on three embedding requests, chunked over two steps,
+    beside decode rows of the generator (never adapted): every finished embedding equals the
+    single-pass embedding through its own adapter, built from merged weights, and the decode
+    logits equal the base model's full recompute."""
+    from workload import make_lora
+    cfg = micro_config()
+    W = sharp_weights(cfg, 55)
+    ad = [make_lora(cfg, 55, rank=4, tag=1), make_lora(cfg, 55, rank=4, tag=2, scale=0.5)]
+    We = dict(W, adapters=ad)
+    n_seq = 5
+    pk = _fresh_kv(cfg, n_seq, 64, 3)
+    lens = {0: 20, 1: 15, 2: 9}
+    ids = {s: draw_tokens(11, s, n, cfg.vocab) for s, n in lens.items()}
+    for s in lens:
+        pk.reserve(s, 64)
+    pk.fill_random(3, 10, 4)
+    pk.reserve(3, 11)
+    kv = OracleKV.from_paged(pk)
+    S, Wc = np.zeros((n_seq, cfg.d_model)), np.zeros(n_seq)
+    dec_tok = draw_tokens(11, 9, 1, cfg.vocab)
+    b1 = Batch([EmbChunk(0, 0, 12, False, "mean"), EmbChunk(1, 0, 15, True, "last"),
+                EmbChunk(2, 0, 4, False, "mean")], [DecodeRow(3, 10)],
+               np.concatenate([ids[0][:12], ids[1], ids[2][:4], dec_tok]), chunk_adapter=[0, 1, -1])
+    r1 = step_oracle((cfg, We), (cfg, We), b1, kv, kv, S, Wc)
+    b2 = Batch([EmbChunk(2, 4, 5, True, "mean"), EmbChunk(0, 12, 8, True, "mean")], [],
+               np.concatenate([ids[2][4:], ids[0][12:]]), chunk_adapter=[-1, 0])
+    r2 = step_oracle((cfg, We), (cfg, We), b2, kv, kv, r1["acc_sum"], r1["acc_w"])
+    for out, s, head, lora in ((r1["out_emb"][1], 1, "last", ad[1]), (r2["out_emb"][0], 2, "mean", None),
+                               (r2["out_emb"][1], 0, "mean", ad[0])):
+        Wm = _merged(W, lora) if lora else W
+        np.testing.assert_allclose(out, oracle.embed_single_pass(cfg, Wm, ids[s], head), rtol=1e-11, atol=1e-12)
+    # the decode row attends to random cached keys: compare with the base model through the cache
+    kv_base = OracleKV.from_paged(pk)
+    r_base = step_oracle((cfg, W), (cfg, W), Batch([], [DecodeRow(3, 10)], dec_tok), kv_base, kv_base,
+                         np.zeros((n_seq, cfg.d_model)), np.zeros(n_seq))
+    np.testing.assert_allclose(r1["logits"], r_base["logits"], rtol=1e-12, atol=1e-13)
+
+
+def test_lora_contract_errors():
+    from workload import make_lora
+    cfg = micro_config()
+    W = sharp_weights(cfg, 57)
+    We = dict(W, adapters=[make_lora(cfg, 57, rank=4, tag=t) for t in range(6)])
+    pk = _fresh_kv(cfg, 6, 16, 1)
+    for s in range(6):
+        pk.reserve(s, 16)
+    kv = OracleKV.from_paged(pk)
+    S, Wc = np.zeros((6, cfg.d_model)), np.zeros(6)
+    ids = draw_tokens(12, 1, 12, cfg.vocab)
+    bad = [
+        (Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[6]), "desc"),
+        (Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[-2]), "desc"),
+        (Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[0, 1]), "desc"),
+        (Batch([EmbChunk(s, 0, 2, True) for s in range(5)], [], ids[:10], chunk_adapter=[0, 1, 2, 3, 4]),
+         "capacity"),
+    ]
+    for b, kind in bad:
+        with pytest.raises(StepError) as e:
+            step_oracle((cfg, We), (cfg, We), b, kv, kv, S, Wc)
+        assert e.value.kind == kind
+    with pytest.raises(StepError) as e:   # a model without adapters
+        step_oracle((cfg, W), (cfg, W), Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[0]),
+                    kv, kv, S, Wc)
+    assert e.value.kind == "desc"

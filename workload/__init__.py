@@ -155,12 +155,65 @@ def make_weights(cfg: ModelConfig, seed: int, model_tag: int = 0, std: float = 0
     return out
 
 
+LORA_SITES = ("qkv", "o", "gate_up", "down")
+
+
+def make_lora(cfg: ModelConfig, seed: int, rank: int, scale: float = 2.0, tag: int = 0,
+              std_a: float = 0.02, std_b: float = 0.1, sites=LORA_SITES) -> Dict:
+    """A seeded LoRA adapter of rank `rank` on the q, k, v, o, gate, up and down projections of
+    every layer (the target set of the paper's e5-mistral embedding adapter), packed per fused
+    projection of this model family:
+      qkv: A [3r][d] = [A_q; A_k; A_v], B [(nq+2nkv)hd][3r] block-diagonal (query rows use
+           columns 0..r-1, key rows r..2r-1, value rows 2r..3r-1);
+      o: A [r][nq hd], B [d][r];
+      gate_up: A [2r][d] = [A_gate; A_up], B_gate [F][2r] = [B_gate | 0], B_up [F][2r] = [0 | B_up];
+      down: A [r][F], B [d][r].
+    A ~ N(0, std_a), B ~ N(0, std_b) (bf16-rounded for bf16 models): with the default spreads
+    the update scale * B A is as large as the base weights, so it is plainly visible."""
+    bf16 = cfg.dtype == "bf16"
+    d, F, r = cfg.d_model, cfg.d_ff, rank
+
+    def draw(layer, k, shape, std):
+        ss = np.random.SeedSequence(seed, spawn_key=(200 + tag, layer, k))
+        w = np.random.default_rng(ss).standard_normal(size=shape, dtype=np.float32) * np.float32(std)
+        return round_bf16(w) if bf16 else w
+
+    layers = []
+    for l in range(cfg.n_layers):
+        ll = {}
+        if "qkv" in sites:
+            A = draw(l, 0, (3 * r, d), std_a)
+            B = np.zeros((cfg.qkv_dim, 3 * r), np.float32)
+            B[:cfg.q_dim, :r] = draw(l, 1, (cfg.q_dim, r), std_b)
+            B[cfg.q_dim:cfg.q_dim + cfg.kv_dim, r:2 * r] = draw(l, 2, (cfg.kv_dim, r), std_b)
+            B[cfg.q_dim + cfg.kv_dim:, 2 * r:] = draw(l, 3, (cfg.kv_dim, r), std_b)
+            ll["qkv"] = (A, B)
+        if "o" in sites:
+            ll["o"] = (draw(l, 4, (r, cfg.q_dim), std_a), draw(l, 5, (d, r), std_b))
+        if "gate_up" in sites:
+            A = draw(l, 6, (2 * r, d), std_a)
+            Bg = np.zeros((F, 2 * r), np.float32)
+            Bu = np.zeros((F, 2 * r), np.float32)
+            Bg[:, :r] = draw(l, 7, (F, r), std_b)
+            Bu[:, r:] = draw(l, 8, (F, r), std_b)
+            ll["gate_up"] = (A, Bg, Bu)
+        if "down" in sites:
+            ll["down"] = (draw(l, 9, (r, F), std_a), draw(l, 10, (d, r), std_b))
+        layers.append(ll)
+    return {"rank": r, "scale": float(scale), "layers": layers}
+
+
 def as_float64(weights: Dict) -> Dict:
     """The same weights as float64 arrays (a one-time upcast for float64 consumers)."""
     f = lambda a: None if a is None else np.asarray(a, dtype=np.float64)
-    return {"tok_emb": f(weights["tok_emb"]), "final_norm": f(weights["final_norm"]),
-            "lm_head": f(weights.get("lm_head")),
-            "layers": [{k: f(v) for k, v in lw.items()} for lw in weights["layers"]]}
+    out = {"tok_emb": f(weights["tok_emb"]), "final_norm": f(weights["final_norm"]),
+           "lm_head": f(weights.get("lm_head")),
+           "layers": [{k: f(v) for k, v in lw.items()} for lw in weights["layers"]]}
+    if weights.get("adapters"):
+        out["adapters"] = [{"rank": ad["rank"], "scale": ad["scale"],
+                            "layers": [{k: tuple(f(x) for x in v) for k, v in ll.items()}
+                                       for ll in ad["layers"]]} for ad in weights["adapters"]]
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -198,6 +251,7 @@ class Batch:
     chunk's tokens, then one input token per decode row.  ``token_weights`` (weighted-mean
     chunks) holds one weight per embedding-chunk token, in the same order.  ``hidden_stride``
     is the number of rows per request of the buffer that buffered-head chunks fill.
+    ``chunk_adapter`` names, per embedding chunk, the embedding model's LoRA adapter (-1: none).
     """
     chunks: List[EmbChunk] = field(default_factory=list)
     rows: List[DecodeRow] = field(default_factory=list)
@@ -205,6 +259,7 @@ class Batch:
     gen_chunks: List[GenChunk] = field(default_factory=list)
     token_weights: Optional[np.ndarray] = None
     hidden_stride: int = 0
+    chunk_adapter: Optional[List[int]] = None
 
     @property
     def n_emb_tokens(self) -> int:
