@@ -100,6 +100,30 @@ typedef struct orthrus_weights {
 
 typedef struct orthrus_model orthrus_model; /* opaque host-side handle */
 
+/* LoRA adapter of an embedding model (Section 2, parameter sharing: embedding models derived from
+ * generative ones by LoRA; the paper deploys Mistral-7B with the e5-mistral adapter, ranks up to
+ * 64).  Per layer and adapted projection, A [rank][in] and B [out][rank] in the model dtype
+ * (device); the projection computes x W^T + scale * (x A^T) B^T for the rows of every chunk that
+ * names the adapter.  Sites: qkv (A [r_qkv][d], B [(nq + 2 nkv) hd][r_qkv]), o (A [r_o][nq hd],
+ * B [d][r_o]), gate/up (one A [r_gu][d] shared, B_gate and B_up [d_ff][r_gu]), down
+ * (A [r_down][d_ff], B [d][r_down]).  Separate q, k and v adapters are one qkv site with the three
+ * A stacked and a block-diagonal B; separate gate and up adapters stack their A the same way. */
+typedef struct orthrus_lora_layer {
+    const void *qkv_a, *qkv_b;
+    const void *o_a, *o_b;
+    const void *gate_up_a, *gate_b, *up_b;
+    const void *down_a, *down_b;
+} orthrus_lora_layer;
+
+typedef struct orthrus_lora {
+    int32_t rank[4]; /* qkv, o, gate/up, down: multiples of 16 up to 256; 0 = site not adapted */
+    float scale;     /* the update's factor (alpha / r in the usual parameterisation) */
+    const orthrus_lora_layer *layers; /* HOST array of n_layers entries, copied */
+} orthrus_lora;
+
+/* Maximum distinct adapters the embedding chunks of one batch may name. */
+#define ORTHRUS_MAX_STEP_ADAPTERS 4
+
 /* One embedding chunk: tokens at positions [offset, offset + len) of request `seq`
  * (Section 3.3: the n-token input split into chunks c_1..c_K across iterations). */
 typedef struct orthrus_emb_chunk {
@@ -129,7 +153,11 @@ typedef struct orthrus_gen_chunk {
  *     NULL when no chunk uses that head.
  *   hidden: DEVICE fp32 [emb_kv n_seq][hidden_stride][d]: an ORTHRUS_POOL_BUFFER chunk of request
  *     s writes its final-normed hidden rows to rows s * hidden_stride + offset .. + len - 1
- *     (ECAPACITY if offset + len > hidden_stride); may be NULL when no chunk uses that head. */
+ *     (ECAPACITY if offset + len > hidden_stride); may be NULL when no chunk uses that head.
+ *   chunk_adapter: HOST int32 per embedding chunk: index of the embedding model's LoRA adapter
+ *     (orthrus_model_set_adapters) its rows go through, -1 for the base model (EDESC outside
+ *     [-1, n_adapters); ECAPACITY for more than ORTHRUS_MAX_STEP_ADAPTERS distinct ones); NULL =
+ *     every chunk uses the base model.  Prompt chunks and decode rows never use an adapter. */
 typedef struct orthrus_batch {
     int32_t n_chunks, n_decode;
     const orthrus_emb_chunk *chunks;
@@ -140,6 +168,7 @@ typedef struct orthrus_batch {
     const float *token_weights;
     float *hidden;
     int32_t hidden_stride;
+    const int32_t *chunk_adapter;
 } orthrus_batch;
 
 /* A paged KV cache (device), model dtype.  k_cache: [n_layers][n_pages][n_kv_heads][page][hd]
@@ -158,6 +187,12 @@ typedef struct orthrus_kv {
  * lm_head) and returns a host handle that keeps copies of both.  No device work. */
 int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, orthrus_model **out);
 void orthrus_model_destroy(orthrus_model *m);
+
+/* Registers the adapters that embedding chunks of `m` may name (index into this array), replacing
+ * earlier ones; n = 0 removes them.  All adapters must have the same four ranks (EUNSUPPORTED
+ * otherwise, or for a rank that is not a multiple of 16 up to 256); a null A or B of an adapted
+ * site is EINVAL.  Host only; size workspaces (orthrus_workspace_bytes) after this call. */
+int orthrus_model_set_adapters(orthrus_model *m, const orthrus_lora *adapters, int32_t n);
 
 /* Device workspace bytes for steps of at most max_tokens tokens (all chunk tokens + decode
  * rows), at most max_chunks chunks (embedding plus generation prefill), at most max_decode

@@ -31,6 +31,8 @@
  *   - A generation request's final prompt chunk yields its first token; with max_new > 1 it
  *     then decodes one token per iteration (decode item at ctx_len = n + generated - 1).
  *   - A sampled token equal to eos_token (if >= 0) ends its request at commit.
+ *   - A batch holds chunks of at most ORTHRUS_MAX_STEP_ADAPTERS distinct LoRA adapters; an
+ *     embedding request whose adapter would exceed that cannot be admitted this iteration.
  *
  * Conventions: host pointers only in the scheduler; the caller owns every buffer it passes;
  * arrays returned by the scheduler stay valid until its next orthrus_sched_next / _commit /
@@ -69,18 +71,17 @@ int orthrus_sched_create(const orthrus_sched_config *cfg, orthrus_sched **out);
 void orthrus_sched_destroy(orthrus_sched *s);
 
 /* Queue a request (arrival order = call order).  tokens: n token ids (host), copied; NULL stands
- * for n zeros (scheduling studies).  pool: ORTHRUS_POOL_MEAN / _LAST / _CLS (buffered heads are
- * left to callers of orthrus_step, which own the hidden buffer).  EINVAL: id already
- * live, n < 1, max_new < 1, bad pool; ECAPACITY: the request's reservation exceeds the block
- * table or the cache's pages (it could never be admitted). */
-int orthrus_sched_submit_embedding(orthrus_sched *s, int64_t id, const int32_t *tokens, int32_t n,
-                                   int32_t pool);
+ * for n zeros (scheduling studies).  pool: ORTHRUS_POOL_MEAN / _LAST / _CLS / _WMEAN (buffered
+ * heads are left to callers of orthrus_step, which own the hidden buffer); weights: with
+ * ORTHRUS_POOL_WMEAN, n finite non-negative weights (host, copied), else ignored.  adapter: the
+ * embedding model's LoRA adapter index or -1 (checked by orthrus_step); a batch takes chunks of at
+ * most ORTHRUS_MAX_STEP_ADAPTERS distinct adapters.  EINVAL: id already live, n < 1, max_new < 1,
+ * bad pool, weights or adapter; ECAPACITY: the request's reservation exceeds the block table or
+ * the cache's pages (it could never be admitted). */
+int orthrus_sched_submit_embedding(orthrus_sched *s, int64_t id, const int32_t *tokens,
+                                   const float *weights, int32_t n, int32_t pool, int32_t adapter);
 int orthrus_sched_submit_generation(orthrus_sched *s, int64_t id, const int32_t *prompt, int32_t n,
                                     int32_t max_new);
-/* A weighted-mean embedding request (ORTHRUS_POOL_WMEAN): weights holds one finite, non-negative
- * weight per token (host, copied); EINVAL otherwise.  Other errors as above. */
-int orthrus_sched_submit_embedding_weighted(orthrus_sched *s, int64_t id, const int32_t *tokens,
-                                            const float *weights, int32_t n);
 
 /* One iteration's batch.  `batch` is ready for orthrus_step: chunk and row `seq` fields are cache
  * slots (embedding chunks in cache 0; prompt chunks and decode rows in cache 1, or 0 when shared)

@@ -33,6 +33,9 @@ Readings taken where the paper leaves a detail open (also listed in the design n
   decode phase (from the next iteration) unless max_new == 1.  Decode item of a request with g
   tokens generated so far: input position n + g - 1, i.e. ``ctx_len`` = n + g - 1 cached tokens.
 * A sampled token equal to the end-of-sequence id (if one is set) ends the request at commit.
+* An embedding request may name a LoRA adapter; a batch holds chunks of at most four distinct
+  adapters (the step's limit), so an embedding request whose adapter would be a fifth cannot be
+  admitted this iteration (its queue stops contributing, as for any request that does not fit).
 """
 from __future__ import annotations
 
@@ -60,6 +63,7 @@ class _Req:
     n: int                       # embedding input length or prompt length
     max_new: int = 0
     pool: int = 0
+    adapter: int = -1
     done: int = 0                # input tokens scheduled so far
     generated: int = 0
     admitted: bool = False
@@ -73,6 +77,7 @@ class _Req:
 @dataclass
 class Schedule:
     emb_chunks: List[tuple] = field(default_factory=list)   # (id, offset, len, last)
+    emb_adapters: List[int] = field(default_factory=list)   # adapter of each embedding chunk
     gen_chunks: List[tuple] = field(default_factory=list)   # (id, offset, len, last)
     decodes: List[tuple] = field(default_factory=list)      # (id, ctx_len, tokens)
     order: List[str] = field(default_factory=list)          # "e" / "g" per credit-loop pick
@@ -83,6 +88,9 @@ class Schedule:
 
 class SchedError(Exception):
     pass
+
+
+MAX_STEP_ADAPTERS = 4
 
 
 def _pages(n_positions: int, page: int) -> int:
@@ -119,8 +127,8 @@ class IBSOracle:
         return _pages(positions, self.cfg.page_size)
 
     # -- requests
-    def submit_embedding(self, rid: int, n: int, pool: int = 0) -> None:
-        self._submit(_Req(rid, "emb", n, pool=pool))
+    def submit_embedding(self, rid: int, n: int, pool: int = 0, adapter: int = -1) -> None:
+        self._submit(_Req(rid, "emb", n, pool=pool, adapter=adapter))
 
     def submit_generation(self, rid: int, n: int, max_new: int) -> None:
         self._submit(_Req(rid, "gen", n, max_new=max_new))
@@ -172,6 +180,7 @@ class IBSOracle:
         if not self.Qg:
             self.a_g = 0
         blocked_q = {"e": False, "g": False}
+        self._adapters = set()
         while B > 0:
             ce = None if blocked_q["e"] else self._candidate(self.Qe, B, in_batch)
             cg = None if blocked_q["g"] else self._candidate(self.Qg, B, in_batch)
@@ -214,6 +223,8 @@ class IBSOracle:
             c = self._cache(r.kind)
             if self.free_slots[c] < 1 or self.free_pages[c] < self._reservation(r):
                 return None
+        if r.adapter >= 0 and r.adapter not in self._adapters and len(self._adapters) == MAX_STEP_ADAPTERS:
+            return None
         return r, n
 
     def _admit(self, r: _Req, n: int, out: Schedule, in_batch: set) -> None:
@@ -229,6 +240,9 @@ class IBSOracle:
         in_batch.add(r.id)
         if r.kind == "emb":
             out.emb_chunks.append(item)
+            out.emb_adapters.append(r.adapter)
+            if r.adapter >= 0:
+                self._adapters.add(r.adapter)
             if last:
                 self.Qe.remove(r)
                 out.finished.append(r.id)

@@ -32,6 +32,7 @@ ORTHRUS_POOL_NONE = 3
 ORTHRUS_POOL_WMEAN = 4
 ORTHRUS_POOL_BUFFER = 5
 ORTHRUS_POOL_MASK = 7
+ORTHRUS_MAX_STEP_ADAPTERS = 4
 ORTHRUS_DEVERR_PAGE = 1
 ORTHRUS_DEVERR_ACC = 2
 
@@ -54,6 +55,16 @@ class orthrus_weights(Structure):
                 ("layers", POINTER(orthrus_layer_weights))]
 
 
+class orthrus_lora_layer(Structure):
+    _fields_ = [("qkv_a", c_void_p), ("qkv_b", c_void_p), ("o_a", c_void_p), ("o_b", c_void_p),
+                ("gate_up_a", c_void_p), ("gate_b", c_void_p), ("up_b", c_void_p),
+                ("down_a", c_void_p), ("down_b", c_void_p)]
+
+
+class orthrus_lora(Structure):
+    _fields_ = [("rank", c_int32 * 4), ("scale", c_float), ("layers", POINTER(orthrus_lora_layer))]
+
+
 class orthrus_emb_chunk(Structure):
     _fields_ = [("seq", c_int32), ("offset", c_int32), ("len", c_int32), ("flags", c_int32)]
 
@@ -71,7 +82,8 @@ class orthrus_batch(Structure):
                 ("chunks", POINTER(orthrus_emb_chunk)), ("rows", POINTER(orthrus_decode_row)),
                 ("token_ids", POINTER(c_int32)), ("n_gen_chunks", c_int32),
                 ("gen_chunks", POINTER(orthrus_gen_chunk)), ("token_weights", POINTER(c_float)),
-                ("hidden", c_void_p), ("hidden_stride", c_int32)]
+                ("hidden", c_void_p), ("hidden_stride", c_int32),
+                ("chunk_adapter", POINTER(c_int32))]
 
 
 class orthrus_kv(Structure):
@@ -118,6 +130,7 @@ SIGNATURES = {
     "orthrus_model_create": (c_int, [POINTER(orthrus_config), POINTER(orthrus_weights),
                                      POINTER(c_void_p)]),
     "orthrus_model_destroy": (None, [c_void_p]),
+    "orthrus_model_set_adapters": (c_int, [c_void_p, POINTER(orthrus_lora), c_int32]),
     "orthrus_workspace_bytes": (c_size_t, [c_void_p, c_void_p, c_int32, c_int32, c_int32,
                                            c_int32]),
     "orthrus_step": (c_int, [c_void_p, c_void_p, POINTER(orthrus_batch), POINTER(orthrus_kv),
@@ -135,10 +148,9 @@ SIGNATURES = {
     "orthrus_strerror": (c_char_p, [c_int]),
     "orthrus_sched_create": (c_int, [POINTER(orthrus_sched_config), POINTER(c_void_p)]),
     "orthrus_sched_destroy": (None, [c_void_p]),
-    "orthrus_sched_submit_embedding": (c_int, [c_void_p, c_int64, c_void_p, c_int32, c_int32]),
+    "orthrus_sched_submit_embedding": (c_int, [c_void_p, c_int64, c_void_p, c_void_p, c_int32, c_int32,
+                                               c_int32]),
     "orthrus_sched_submit_generation": (c_int, [c_void_p, c_int64, c_void_p, c_int32, c_int32]),
-    "orthrus_sched_submit_embedding_weighted": (c_int, [c_void_p, c_int64, c_void_p, c_void_p,
-                                                        c_int32]),
     "orthrus_sched_next": (c_int, [c_void_p, POINTER(orthrus_sched_batch)]),
     "orthrus_sched_commit": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32),
                                      POINTER(c_int64), c_int32]),
@@ -181,6 +193,10 @@ def orthrus_model_create(cfg, weights, out):
 
 def orthrus_model_destroy(model):
     load().orthrus_model_destroy(model)
+
+
+def orthrus_model_set_adapters(model, adapters, n):
+    return load().orthrus_model_set_adapters(model, adapters, n)
 
 
 def orthrus_workspace_bytes(emb, gen, max_tokens, max_chunks, max_decode, max_ctx):
@@ -229,16 +245,12 @@ def orthrus_sched_destroy(s):
     load().orthrus_sched_destroy(s)
 
 
-def orthrus_sched_submit_embedding(s, rid, tokens, n, pool):
-    return load().orthrus_sched_submit_embedding(s, rid, tokens, n, pool)
+def orthrus_sched_submit_embedding(s, rid, tokens, weights, n, pool, adapter):
+    return load().orthrus_sched_submit_embedding(s, rid, tokens, weights, n, pool, adapter)
 
 
 def orthrus_sched_submit_generation(s, rid, prompt, n, max_new):
     return load().orthrus_sched_submit_generation(s, rid, prompt, n, max_new)
-
-
-def orthrus_sched_submit_embedding_weighted(s, rid, tokens, weights, n):
-    return load().orthrus_sched_submit_embedding_weighted(s, rid, tokens, weights, n)
 
 
 def orthrus_sched_next(s, out):

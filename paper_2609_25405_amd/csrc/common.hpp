@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "orthrus.h"
+
 namespace orthrus {
 
 typedef __bf16 bf16;
@@ -71,6 +73,17 @@ struct QkvRope {
     int *err;
 };
 
+// LoRA update of a projection (rows [0, rows) of the launch): out += U B^T, with U [rows][ldu]
+// the scaled, per-row-masked shrink x A^T of the n adapters in use side by side (adapter j owns
+// columns j*r .. j*r + r - 1) and B_j [N][r].  SwiGLU launches read b0 for gate, b1 for up.
+constexpr int kMaxStepAdapters = ORTHRUS_MAX_STEP_ADAPTERS;
+struct LoraGemm {
+    const void *u;
+    const void *u_lo;          // bf16 path: U = u + u_lo (u the bf16 rounding, u_lo the rest)
+    int ldu, rows, r, n;       // n = 0: no update
+    const void *b0[kMaxStepAdapters], *b1[kMaxStepAdapters];
+};
+
 struct GemmArgs {
     const void *A;   // [M][K] activations, row stride lda (elements)
     const void *B0;  // [N][K] weights (gate for SwiGLU)
@@ -83,11 +96,26 @@ struct GemmArgs {
     float *partial;
     size_t split_stride;
     QkvRope rope;    // EPI_QKV_ROPE only
+    LoraGemm lora;   // adds the low-rank update before the epilogue (split 0 of a split-K launch)
 };
 hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
 // split-K factor (<= max_splits, dividing K into whole stages) for a bf16 residual-add
 // projection of this shape; launch_gemm ignores a requested split that does not divide K
 int gemm_add_splits(int M, int N, int K, int max_splits);
+
+// LoRA shrink: u[row][j*r + k] = scale[j] * sum_i x[row][i] a_j[k][i] for the adapter j of the
+// row (row_adapter[row]), 0 in the other adapters' columns.  x [rows][K] with row stride ldx,
+// a_j [r][K], u [rows][n*r] (bf16 on the bf16 path, with u_lo; fp32 on the fp32 path).
+struct LoraShrink {
+    const void *x;
+    int ldx, K, rows, r, n;
+    const void *a[kMaxStepAdapters];
+    float scale[kMaxStepAdapters];
+    const int32_t *row_adapter;
+    void *u;
+    void *u_lo;                // bf16 path: the rounding remainder of u (u + u_lo = U to ~16 bits)
+};
+hipError_t launch_lora_shrink(int dtype, const LoraShrink &p, hipStream_t s);
 
 struct NormArgs {
     const float *x;         // fp32 residual rows [rows][d]

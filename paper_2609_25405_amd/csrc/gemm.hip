@@ -212,6 +212,47 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     // epilogues reuse the stage buffers
     __builtin_amdgcn_s_waitcnt(0);
 
+    // LoRA update: acc += U B^T for the launch's rows below lora.rows (split 0 of a split-K
+    // launch), 16 columns of U per MFMA step (U as its bf16 rounding plus remainder, two MFMAs),
+    // operands straight from global memory in the same fragment layout as the main loop (rows
+    // of U and of B are contiguous in the rank)
+    if (a.lora.n > 0 && split == 0 && m0 < a.lora.rows) {
+        const LoraGemm &L = a.lora;
+        const int ldu = L.n * L.r;
+        const bf16x8 zero = {};
+        for (int c0 = 0; c0 < ldu; c0 += 16) {
+            const int j = c0 / L.r, kk = c0 % L.r + 8 * (lane >> 5);
+            bf16x8 ua[FM], ul[FM], ub[FN];
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi) {
+                const int row = m0 + wm * TM + mi * 32 + (lane & 31);
+                const size_t off = (size_t)row * ldu + c0 + 8 * (lane >> 5);
+                ua[mi] = row < L.rows ? *(const bf16x8 *)((const bf16 *)L.u + off) : zero;
+                ul[mi] = row < L.rows ? *(const bf16x8 *)((const bf16 *)L.u_lo + off) : zero;
+            }
+#pragma unroll
+            for (int ni = 0; ni < FN; ++ni) {
+                int col;
+                const bf16 *src;
+                if constexpr (EPI == EPI_SWIGLU) {
+                    col = n0 + wn * (TN / 2) + (ni % (FN / 2)) * 32 + (lane & 31);
+                    src = (const bf16 *)(ni < FN / 2 ? L.b0[j] : L.b1[j]);
+                } else {
+                    col = n0 + wn * TN + ni * 32 + (lane & 31);
+                    src = (const bf16 *)L.b0[j];
+                }
+                ub[ni] = *(const bf16x8 *)(src + (size_t)min(col, a.N - 1) * L.r + kk);
+            }
+#pragma unroll
+            for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < FN; ++ni) {
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ua[mi], ub[ni], acc[mi][ni], 0, 0, 0);
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ul[mi], ub[ni], acc[mi][ni], 0, 0, 0);
+                }
+        }
+    }
+
     if constexpr (EPI == EPI_QKV_ROPE) {
         // Rotation of q and k at each token's position (pairs (i, i + hd/2)), q stored for
         // attention, rotated k and raw v appended to the paged cache.  The fp32 tile goes
@@ -411,6 +452,29 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
                 }
         }
         __syncthreads();
+    }
+    // LoRA update U B^T for the rows below lora.rows
+    if (a.lora.n > 0) {
+        const LoraGemm &L = a.lora;
+        const int ldu = L.n * L.r;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = m0 + ty * 4 + i;
+            if (row >= a.M || row >= L.rows) continue;
+            const float *u = (const float *)L.u + (size_t)row * ldu;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int col = min(n0 + tx * 4 + j, a.N - 1);
+                float d0 = 0.f, d1 = 0.f;
+                for (int c = 0; c < ldu; ++c) {
+                    const int ad = c / L.r, kk = c % L.r;
+                    d0 = fmaf(u[c], ((const float *)L.b0[ad])[(size_t)col * L.r + kk], d0);
+                    if (EPI == EPI_SWIGLU) d1 = fmaf(u[c], ((const float *)L.b1[ad])[(size_t)col * L.r + kk], d1);
+                }
+                acc[i][j] += d0;
+                if (EPI == EPI_SWIGLU) accu[i][j] += d1;
+            }
+        }
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

@@ -101,6 +101,18 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         const int v = t < p.Te ? emb.cfg.vocab : gen.cfg.vocab;
         if (b.token_ids[t] < 0 || b.token_ids[t] >= v) return ORTHRUS_EDESC;
     }
+    if (b.chunk_adapter) {
+        for (int i = 0; i < b.n_chunks; ++i) {
+            const int ad = b.chunk_adapter[i];
+            if (ad < -1 || ad >= (int)emb.adapters.size()) return ORTHRUS_EDESC;
+            if (ad < 0) continue;
+            bool seen_ad = false;
+            for (int u = 0; u < p.n_used; ++u) seen_ad |= p.used[u] == ad;
+            if (seen_ad) continue;
+            if (p.n_used == ORTHRUS_MAX_STEP_ADAPTERS) return ORTHRUS_ECAPACITY;
+            p.used[p.n_used++] = ad;
+        }
+    }
     if (p.any_wmean) {
         if (!b.token_weights) return ORTHRUS_EDESC;
         int t = 0;
@@ -228,7 +240,19 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         p.off_hid = end;
         end += p.Te;
     }
+    if (p.n_used > 0) {
+        p.off_radp = end;
+        end += p.Te;
+    }
     p.meta.assign(end, 0);
+    if (p.n_used > 0) {
+        for (int i = 0, t = 0; i < b.n_chunks; t += b.chunks[i].len, ++i) {
+            int slot = -1;
+            for (int u = 0; u < p.n_used; ++u)
+                if (p.used[u] == b.chunk_adapter[i]) slot = u;
+            for (int k = 0; k < b.chunks[i].len; ++k) p.meta[p.off_radp + t + k] = slot;
+        }
+    }
     if (p.any_wmean) std::memcpy(&p.meta[p.off_wts], b.token_weights, (size_t)p.Te * 4);
     if (p.any_buffer) {
         for (int i = 0, t = 0; i < b.n_chunks; t += b.chunks[i].len, ++i) {

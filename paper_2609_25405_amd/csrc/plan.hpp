@@ -23,6 +23,10 @@ struct Model {
     orthrus_config cfg;
     orthrus_weights w;
     std::vector<orthrus_layer_weights> layers;
+    // LoRA adapters chunks may name (orthrus_model_set_adapters); equal ranks for all of them
+    std::vector<orthrus_lora> adapters;
+    std::vector<std::vector<orthrus_lora_layer>> adapter_layers;
+    int lora_rank[4] = {0, 0, 0, 0};
     int group() const { return cfg.n_q_heads / cfg.n_kv_heads; }
     int q_dim() const { return cfg.n_q_heads * cfg.head_dim; }
     int kv_dim() const { return cfg.n_kv_heads * cfg.head_dim; }
@@ -49,6 +53,11 @@ struct StepPlan {
     // heads in the batch that need every embedding row's final norm (mean, weighted mean,
     // buffered), and the optional per-token arrays they read
     bool any_mean = false, any_wmean = false, any_buffer = false;
+    // adapters the batch's embedding chunks name, in order of first use; per embedding token the
+    // position of its adapter in that list or -1 (metadata at off_radp)
+    int n_used = 0;
+    int used[ORTHRUS_MAX_STEP_ADAPTERS] = {0, 0, 0, 0};
+    int off_radp = -1;
     // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows, then
     // (weighted mean) fp32 weights[Te] and (buffered head) hidden-buffer row[Te] (-1: none)
     std::vector<int32_t> meta;

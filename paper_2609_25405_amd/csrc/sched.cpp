@@ -25,7 +25,7 @@ namespace {
 struct Req {
     int64_t id = 0;
     bool emb = true;
-    int32_t n = 0, max_new = 0, pool = 0;
+    int32_t n = 0, max_new = 0, pool = 0, adapter = -1;
     int32_t done = 0, generated = 0;
     bool admitted = false;
     int32_t cache = 0, slot = -1;
@@ -57,8 +57,9 @@ struct orthrus_sched {
     std::vector<orthrus_emb_chunk> chunks;
     std::vector<orthrus_gen_chunk> gchunks;
     std::vector<orthrus_decode_row> rows;
-    std::vector<int32_t> tokens, row_tokens, table_rows;
+    std::vector<int32_t> tokens, row_tokens, table_rows, chunk_adapter;
     std::vector<float> token_weights;
+    std::vector<int32_t> batch_adapters;  // distinct adapters of this batch's embedding chunks
     std::vector<int64_t> chunk_ids, gen_ids, row_ids, logit_ids, finishing_ids;
     std::vector<Req *> logit_reqs, finishing;
     std::string picks;
@@ -107,6 +108,10 @@ int32_t candidate(orthrus_sched *s, std::vector<Req *> &Q, int32_t B, Req **out)
         const Cache &c = s->caches[s->cache_of(*r)];
         if (c.free_slots.empty() || (int64_t)c.free_pages.size() < s->reservation(*r)) return 0;
     }
+    if (r->adapter >= 0 &&
+        std::find(s->batch_adapters.begin(), s->batch_adapters.end(), r->adapter) == s->batch_adapters.end() &&
+        (int)s->batch_adapters.size() == ORTHRUS_MAX_STEP_ADAPTERS)
+        return 0;
     *out = r;
     return n;
 }
@@ -135,6 +140,10 @@ void admit(orthrus_sched *s, Req *r, int32_t n) {
         orthrus_emb_chunk c{r->slot, r->done, n, (last ? ORTHRUS_CHUNK_LAST : 0) | (r->pool << ORTHRUS_POOL_SHIFT)};
         s->chunks.push_back(c);
         s->chunk_ids.push_back(r->id);
+        s->chunk_adapter.push_back(r->adapter);
+        if (r->adapter >= 0 &&
+            std::find(s->batch_adapters.begin(), s->batch_adapters.end(), r->adapter) == s->batch_adapters.end())
+            s->batch_adapters.push_back(r->adapter);
     } else {
         orthrus_gen_chunk c{r->slot, r->done, n, last ? ORTHRUS_CHUNK_LAST : 0};
         s->gchunks.push_back(c);
@@ -197,31 +206,25 @@ int orthrus_sched_create(const orthrus_sched_config *cfg, orthrus_sched **out) {
 
 void orthrus_sched_destroy(orthrus_sched *s) { delete s; }
 
-int orthrus_sched_submit_embedding(orthrus_sched *s, int64_t id, const int32_t *tokens, int32_t n,
-                                   int32_t pool) {
-    if (!s) return ORTHRUS_EINVAL;
-    if (pool != ORTHRUS_POOL_MEAN && pool != ORTHRUS_POOL_LAST && pool != ORTHRUS_POOL_CLS) return ORTHRUS_EINVAL;
+int orthrus_sched_submit_embedding(orthrus_sched *s, int64_t id, const int32_t *tokens,
+                                   const float *weights, int32_t n, int32_t pool, int32_t adapter) {
+    if (!s || n < 1 || adapter < -1) return ORTHRUS_EINVAL;
+    if (pool != ORTHRUS_POOL_MEAN && pool != ORTHRUS_POOL_LAST && pool != ORTHRUS_POOL_CLS &&
+        pool != ORTHRUS_POOL_WMEAN)
+        return ORTHRUS_EINVAL;
+    if (pool == ORTHRUS_POOL_WMEAN) {
+        if (!weights) return ORTHRUS_EINVAL;
+        for (int32_t i = 0; i < n; ++i)
+            if (!std::isfinite(weights[i]) || weights[i] < 0.f) return ORTHRUS_EINVAL;
+    }
     std::unique_ptr<Req> r(new (std::nothrow) Req);
     if (!r) return ORTHRUS_EINVAL;
     r->id = id;
     r->emb = true;
     r->n = n;
     r->pool = pool;
-    return submit(s, std::move(r), tokens);
-}
-
-int orthrus_sched_submit_embedding_weighted(orthrus_sched *s, int64_t id, const int32_t *tokens,
-                                            const float *weights, int32_t n) {
-    if (!s || !weights || n < 1) return ORTHRUS_EINVAL;
-    for (int32_t i = 0; i < n; ++i)
-        if (!std::isfinite(weights[i]) || weights[i] < 0.f) return ORTHRUS_EINVAL;
-    std::unique_ptr<Req> r(new (std::nothrow) Req);
-    if (!r) return ORTHRUS_EINVAL;
-    r->id = id;
-    r->emb = true;
-    r->n = n;
-    r->pool = ORTHRUS_POOL_WMEAN;
-    r->weights.assign(weights, weights + n);
+    r->adapter = adapter;
+    if (pool == ORTHRUS_POOL_WMEAN) r->weights.assign(weights, weights + n);
     return submit(s, std::move(r), tokens);
 }
 
@@ -245,6 +248,8 @@ int orthrus_sched_next(orthrus_sched *s, orthrus_sched_batch *out) {
     s->rows.clear();
     s->tokens.clear();
     s->token_weights.clear();
+    s->chunk_adapter.clear();
+    s->batch_adapters.clear();
     s->row_tokens.clear();
     s->table_rows.clear();
     s->chunk_ids.clear();
@@ -348,6 +353,7 @@ int orthrus_sched_next(orthrus_sched *s, orthrus_sched_batch *out) {
     out->batch.n_gen_chunks = (int32_t)s->gchunks.size();
     out->batch.gen_chunks = s->gchunks.data();
     out->batch.token_weights = any_weighted ? s->token_weights.data() : nullptr;
+    out->batch.chunk_adapter = s->batch_adapters.empty() ? nullptr : s->chunk_adapter.data();
     out->chunk_ids = s->chunk_ids.data();
     out->gen_chunk_ids = s->gen_ids.data();
     out->row_ids = s->row_ids.data();

@@ -25,7 +25,7 @@ constexpr size_t kAlign = 256;
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, split_slabs, rope_cs, total;
+    size_t err, meta, x, act, qkv, q, o, u, inv_rms, partials, split_slabs, rope_cs, lora_u, total;
 };
 // split-K slabs of one residual-add projection: at most kMaxSplits fp32 [T][d] slabs
 constexpr int kMaxSplits = 4;
@@ -48,6 +48,10 @@ Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials
     L.partials = o; o += up(n_partials * (size_t)m.group() * (m.cfg.head_dim + 2) * 4);
     L.split_slabs = o; o += m.cfg.dtype == ORTHRUS_BF16 ? up((size_t)kMaxSplits * T * d * 4) : 0;
     L.rope_cs = o; o += m.cfg.dtype == ORTHRUS_BF16 ? up(T * (size_t)(m.cfg.head_dim / 2) * 8) : 0;
+    // LoRA shrink output of one projection: [T][adapters in use x rank], the widest site
+    const int max_rank = *std::max_element(m.lora_rank, m.lora_rank + 4);
+    // (bf16 path: the rounding and its remainder, two arrays)
+    L.lora_u = o; o += m.adapters.empty() ? 0 : up(T * (size_t)kMaxStepAdapters * max_rank * 4);
     L.total = o;
     return L;
 }
@@ -165,6 +169,34 @@ int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, or
     m->layers.assign(w->layers, w->layers + cfg->n_layers);
     m->w.layers = m->layers.data();
     *out = m;
+    return ORTHRUS_OK;
+}
+
+int orthrus_model_set_adapters(orthrus_model *m, const orthrus_lora *adapters, int32_t n) {
+    if (!m || n < 0 || (n > 0 && !adapters)) return ORTHRUS_EINVAL;
+    for (int32_t i = 0; i < n; ++i) {
+        const orthrus_lora &a = adapters[i];
+        for (int k = 0; k < 4; ++k) {
+            if (a.rank[k] != adapters[0].rank[k]) return ORTHRUS_EUNSUPPORTED;
+            if (a.rank[k] < 0 || a.rank[k] > 256 || a.rank[k] % 16) return ORTHRUS_EUNSUPPORTED;
+        }
+        if (!(a.scale == a.scale) || (m->cfg.n_layers > 0 && !a.layers)) return ORTHRUS_EINVAL;
+        for (int l = 0; l < m->cfg.n_layers; ++l) {
+            const orthrus_lora_layer &ll = a.layers[l];
+            if ((a.rank[0] && (!ll.qkv_a || !ll.qkv_b)) || (a.rank[1] && (!ll.o_a || !ll.o_b)) ||
+                (a.rank[2] && (!ll.gate_up_a || !ll.gate_b || !ll.up_b)) ||
+                (a.rank[3] && (!ll.down_a || !ll.down_b)))
+                return ORTHRUS_EINVAL;
+        }
+    }
+    std::lock_guard<std::mutex> lk(m->mu);
+    m->adapters.assign(adapters, adapters + n);
+    m->adapter_layers.clear();
+    for (int32_t i = 0; i < n; ++i) {
+        m->adapter_layers.emplace_back(adapters[i].layers, adapters[i].layers + m->cfg.n_layers);
+        m->adapters[i].layers = m->adapter_layers.back().data();
+    }
+    for (int k = 0; k < 4; ++k) m->lora_rank[k] = n > 0 ? adapters[0].rank[k] : 0;
     return ORTHRUS_OK;
 }
 
@@ -300,8 +332,49 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         }
         return launch_rmsnorm(dt, gather, n, s);
     };
+    // LoRA: the shrink of site `site` (0 qkv, 1 o, 2 gate/up, 3 down) for the embedding rows of
+    // group g in layer l, launched now on the GEMM input X; returns the GEMM's update arguments
+    // (none when no chunk of the batch names an adapter or the site is not adapted)
+    void *lora_u = ws + L.lora_u;
+    auto lora_on = [&](int site, const Group &g) {
+        return p.n_used > 0 && emb->lora_rank[site] > 0 && g.m == emb && g.r0 == 0 && Te > 0;
+    };
+    auto lora = [&](int site, int l, const Group &g, const char *X, int ldx, int K, LoraGemm &lg) -> hipError_t {
+        lg = LoraGemm{};
+        const int r = emb->lora_rank[site];
+        if (!lora_on(site, g)) return hipSuccess;
+        LoraShrink sh{};
+        sh.x = X;
+        sh.ldx = ldx;
+        sh.K = K;
+        sh.rows = Te;
+        sh.r = r;
+        sh.n = p.n_used;
+        sh.row_adapter = meta + p.off_radp;
+        sh.u = lora_u;
+        lg.u = lora_u;
+        if (dt == ORTHRUS_BF16) {
+            // the remainder array follows the rounding array
+            sh.u_lo = (char *)lora_u + (size_t)Te * p.n_used * r * 2;
+            lg.u_lo = sh.u_lo;
+        }
+        lg.ldu = p.n_used * r;
+        lg.rows = Te;
+        lg.r = r;
+        lg.n = p.n_used;
+        for (int j = 0; j < p.n_used; ++j) {
+            const orthrus_lora &ad = emb->adapters[p.used[j]];
+            const orthrus_lora_layer &ll = emb->adapter_layers[p.used[j]][l];
+            sh.scale[j] = ad.scale;
+            const void *A = site == 0 ? ll.qkv_a : site == 1 ? ll.o_a : site == 2 ? ll.gate_up_a : ll.down_a;
+            sh.a[j] = A;
+            lg.b0[j] = site == 0 ? ll.qkv_b : site == 1 ? ll.o_b : site == 2 ? ll.gate_b : ll.down_b;
+            lg.b1[j] = site == 2 ? ll.up_b : nullptr;
+        }
+        return launch_lora_shrink(dt, sh, s);
+    };
     auto gemm = [&](int epi, const Group &g, const char *A, int lda, const void *B0, const void *B1,
-                    void *out, int ldo, size_t out_es, int N, int K) -> hipError_t {
+                    void *out, int ldo, size_t out_es, int N, int K, const LoraGemm &lg) -> hipError_t {
         GemmArgs ga{};
         ga.A = A + (size_t)g.r0 * lda * es;
         ga.B0 = B0;
@@ -313,11 +386,13 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.lda = lda;
         ga.ldo = ldo;
         ga.splits = 1;
+        ga.lora = lg;
         return launch_gemm(dt, epi, ga, s);
     };
     // residual-add projection into x; one model and bf16: split K when the tile count is low and
     // leave the slabs for the next row-wise kernel (returns the split count)
-    auto add_proj = [&](const Group &g, const char *A, int lda, const void *B, int K, int &splits) -> hipError_t {
+    auto add_proj = [&](const Group &g, const char *A, int lda, const void *B, int K, int &splits,
+                        const LoraGemm &lg) -> hipError_t {
         GemmArgs ga{};
         ga.A = A + (size_t)g.r0 * lda * es;
         ga.B0 = B;
@@ -331,6 +406,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.splits = splits;
         ga.partial = slabs;
         ga.split_stride = slab_stride;
+        ga.lora = lg;
         return launch_gemm(dt, EPI_ADD_F32, ga, s);
     };
 
@@ -424,12 +500,15 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
                 q.hd = c.head_dim;
                 q.page = c.page_size;
                 q.err = err;
+                if (lora_on(0, g)) RUN("lora_shrink", lora(0, l, g, act, d, d, ga.lora));
                 RUN("gemm_qkv_rope", launch_gemm(dt, EPI_QKV_ROPE, ga, s));
             }
         } else {
             for (int gi = 0; gi < n_groups; ++gi) {
                 const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-                RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d));
+                LoraGemm lg{};
+                if (lora_on(0, groups[gi])) RUN("lora_shrink", lora(0, l, groups[gi], act, d, d, lg));
+                RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d, lg));
             }
             RUN("rope_append", launch_rope_append(dt, ra, s));
         }
@@ -442,18 +521,24 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         int splits = 1;
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-            RUN("gemm_o", add_proj(groups[gi], ob, qd, lw.w_o, qd, splits));
+            LoraGemm lg{};
+            if (lora_on(1, groups[gi])) RUN("lora_shrink", lora(1, l, groups[gi], ob, qd, qd, lg));
+            RUN("gemm_o", add_proj(groups[gi], ob, qd, lw.w_o, qd, splits, lg));
         }
         pending = splits > 1 ? splits : 0;
         for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].mlp_norm));
         pending = 0;
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-            RUN("gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d));
+            LoraGemm lg{};
+            if (lora_on(2, groups[gi])) RUN("lora_shrink", lora(2, l, groups[gi], act, d, d, lg));
+            RUN("gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d, lg));
         }
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
-            RUN("gemm_down", add_proj(groups[gi], ub, F, lw.w_down, F, splits));
+            LoraGemm lg{};
+            if (lora_on(3, groups[gi])) RUN("lora_shrink", lora(3, l, groups[gi], ub, F, F, lg));
+            RUN("gemm_down", add_proj(groups[gi], ub, F, lw.w_down, F, splits, lg));
         }
         pending = splits > 1 ? splits : 0;  // added by the next layer's norm or the final norm
     }

@@ -67,6 +67,51 @@ class DeviceModel:
         _check(A.orthrus_model_create(byref(self._cfg), byref(self._w), byref(h)),
                "orthrus_model_create")
         self.handle = h
+        self.adapters = []
+        if weights.get("adapters"):
+            self.set_adapters(weights["adapters"], device)
+
+    def set_adapters(self, adapters, device="cuda"):
+        """Upload LoRA adapters (workload.make_lora layout: per layer {site: (A, B) or
+        (A, B_gate, B_up)}) and register them with the library."""
+        dt = torch_dtype(self.cfg)
+
+        def up(a):
+            return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(device=device, dtype=dt)
+
+        L = len(self.layers)
+        self.adapters = []
+        arr = (A.orthrus_lora * max(1, len(adapters)))()
+        self._lora_keep = []
+        for i, ad in enumerate(adapters):
+            lls = (A.orthrus_lora_layer * max(1, L))()
+            tensors = []
+            ranks = [0, 0, 0, 0]
+            for l, ll in enumerate(ad["layers"]):
+                t = {k: tuple(up(x) for x in v) for k, v in ll.items()}
+                tensors.append(t)
+                f = {}
+                if "qkv" in t:
+                    f.update(qkv_a=_vp(t["qkv"][0]), qkv_b=_vp(t["qkv"][1]))
+                    ranks[0] = t["qkv"][0].shape[0]
+                if "o" in t:
+                    f.update(o_a=_vp(t["o"][0]), o_b=_vp(t["o"][1]))
+                    ranks[1] = t["o"][0].shape[0]
+                if "gate_up" in t:
+                    f.update(gate_up_a=_vp(t["gate_up"][0]), gate_b=_vp(t["gate_up"][1]),
+                             up_b=_vp(t["gate_up"][2]))
+                    ranks[2] = t["gate_up"][0].shape[0]
+                if "down" in t:
+                    f.update(down_a=_vp(t["down"][0]), down_b=_vp(t["down"][1]))
+                    ranks[3] = t["down"][0].shape[0]
+                lls[l] = A.orthrus_lora_layer(**f)
+            arr[i].rank[:] = ranks
+            arr[i].scale = float(ad["scale"])
+            arr[i].layers = ctypes.cast(lls, POINTER(A.orthrus_lora_layer))
+            self._lora_keep.append(lls)
+            self.adapters.append(tensors)
+        _check(A.orthrus_model_set_adapters(self.handle, arr, len(adapters)),
+               "orthrus_model_set_adapters")
 
     def close(self):
         if getattr(self, "handle", None) is not None and self.handle.value:
@@ -182,11 +227,19 @@ class PackedBatch:
             if self._w.shape != (n_emb,):
                 raise A.OrthrusError(A.ORTHRUS_EDESC, "token_weights length")
             wptr = self._w.ctypes.data_as(POINTER(ctypes.c_float))
+        ca = getattr(batch, "chunk_adapter", None)
+        self._ca = None
+        captr = None
+        if ca is not None:
+            self._ca = np.ascontiguousarray(ca, dtype=np.int32)
+            if self._ca.shape != (nc,):
+                raise A.OrthrusError(A.ORTHRUS_EDESC, "chunk_adapter length")
+            captr = self._ca.ctypes.data_as(POINTER(c_int32))
         self.c = A.orthrus_batch(nc, nd, ctypes.cast(self._chunks, POINTER(A.orthrus_emb_chunk)),
                                  ctypes.cast(self._rows, POINTER(A.orthrus_decode_row)),
                                  self._ids.ctypes.data_as(POINTER(c_int32)), ng,
                                  ctypes.cast(self._gen, POINTER(A.orthrus_gen_chunk)), wptr, None,
-                                 int(getattr(batch, "hidden_stride", 0)))
+                                 int(getattr(batch, "hidden_stride", 0)), captr)
 
 
 def step(emb: DeviceModel, gen: DeviceModel, batch, emb_kv: DeviceKV, gen_kv: DeviceKV,
@@ -291,16 +344,15 @@ class Scheduler:
         return a, c_void_p(a.ctypes.data)
 
     def submit_embedding(self, rid: int, n: int, tokens=None, pool: str = "mean",
-                         weights=None) -> None:
+                         weights=None, adapter: int = -1) -> None:
         a, p = self._ids(tokens, n)
-        if pool == "wmean":
+        wp = None
+        if weights is not None:
             w = np.ascontiguousarray(weights, np.float32)
             if w.shape != (n,):
                 raise A.OrthrusError(A.ORTHRUS_EINVAL, "weight count")
-            _check(A.orthrus_sched_submit_embedding_weighted(self.handle, rid, p, c_void_p(w.ctypes.data), n),
-                   "orthrus_sched_submit_embedding_weighted")
-            return
-        _check(A.orthrus_sched_submit_embedding(self.handle, rid, p, n, POOL_CODES[pool]),
+            wp = c_void_p(w.ctypes.data)
+        _check(A.orthrus_sched_submit_embedding(self.handle, rid, p, wp, n, POOL_CODES[pool], adapter),
                "orthrus_sched_submit_embedding")
 
     def submit_generation(self, rid: int, n: int, max_new: int, prompt=None) -> None:
@@ -321,8 +373,11 @@ class Scheduler:
         dec = [(b.row_ids[j], bt.rows[j].ctx_len, b.row_tokens[j]) for j in range(bt.n_decode)]
         picks = ctypes.string_at(b.picks, b.n_picks).decode() if b.n_picks else ""
         n_tok = sum(c[2] for c in emb) + sum(c[2] for c in gen) + len(dec)
+        adapters = ([bt.chunk_adapter[i] for i in range(bt.n_chunks)] if bt.chunk_adapter
+                    else [-1] * bt.n_chunks)
         return {
             "emb_chunks": emb, "gen_chunks": gen, "decodes": dec, "order": list(picks),
+            "emb_adapters": adapters,
             "used": b.tokens_used, "logit_ids": [b.logit_ids[i] for i in range(b.n_logit_rows)],
             "finished": [b.finishing_ids[i] for i in range(b.n_finishing)],
             "credits": (b.credit_e, b.credit_g),

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = P.load()
     names = header_functions()
     assert [os.path.basename(h) for h in HEADERS] == ["orthrus.h", "orthrus_sched.h"]
-    assert len(names) == 11 + 13
+    assert len(names) == 12 + 12
     for n in names:
         assert hasattr(lib, n), n
         assert n in A.SIGNATURES, n
@@ -50,12 +50,13 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(A.orthrus_kv) == 3 * 8 + 3 * 4 + 4
     assert ctypes.sizeof(A.orthrus_gen_chunk) == 16
     # n_chunks, n_decode, 3 pointers, n_gen_chunks (+4 bytes of padding), 3 pointers,
-    # hidden_stride (+4 bytes of padding)
-    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8 + 8 + 3 * 8 + 8
+    # hidden_stride (+4 bytes of padding), 1 pointer
+    assert ctypes.sizeof(A.orthrus_batch) == 8 + 3 * 8 + 8 + 3 * 8 + 8 + 8
     assert A.orthrus_batch.gen_chunks.offset == 40
 
 
-STRUCTS = ["orthrus_config", "orthrus_layer_weights", "orthrus_weights", "orthrus_emb_chunk",
+STRUCTS = ["orthrus_config", "orthrus_layer_weights", "orthrus_weights", "orthrus_lora_layer",
+           "orthrus_lora", "orthrus_emb_chunk",
            "orthrus_decode_row", "orthrus_gen_chunk", "orthrus_batch", "orthrus_kv",
            "orthrus_kernel_time", "orthrus_sched_config", "orthrus_sched_batch",
            "orthrus_runner_buffers", "orthrus_runner_output"]
@@ -360,3 +361,44 @@ def test_unknown_pooling_codes_and_missing_hidden_buffer():
     with pytest.raises(A.OrthrusError) as e:
         R.step(m, m, b, kv, kv, acc, accw, None, emb, ws)
     assert e.value.code == A.ORTHRUS_EINVAL
+
+
+def test_adapter_registration_and_host_validation():
+    from workload import make_lora
+    cfg = tiny_config()
+    W = make_weights(cfg, 2)
+    W["adapters"] = [make_lora(cfg, 2, 16, tag=t) for t in range(6)]
+    m = R.DeviceModel(cfg, W, device="cpu")
+    for bad_ad, code in (([make_lora(cfg, 2, 8)], A.ORTHRUS_EUNSUPPORTED),          # qkv rank 24
+                         ([make_lora(cfg, 2, 16), make_lora(cfg, 2, 32, tag=1)], A.ORTHRUS_EUNSUPPORTED),
+                         ([make_lora(cfg, 2, 160)], A.ORTHRUS_EUNSUPPORTED)):        # qkv rank 480
+        with pytest.raises(A.OrthrusError) as e:
+            R.DeviceModel(cfg, dict(W, adapters=bad_ad), device="cpu")
+        assert e.value.code == code
+    pk = PagedKV(cfg, 64, 6, 8, 3)
+    for s in range(6):
+        pk.reserve(s, 40)
+    kv = R.DeviceKV.from_paged(pk, device="cpu")
+    okv = OracleKV.from_paged(pk)
+    ids = draw_tokens(1, 0, 12, cfg.vocab)
+    t = R.torch
+    acc, accw = t.zeros((6, cfg.d_model)), t.zeros(6)
+    emb = t.zeros((6, cfg.d_model))
+    ws = type("WS", (), {"buf": t.zeros(64, dtype=t.uint8), "nbytes": 64})()
+    We = dict(W)
+    bad = [
+        Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[6]),
+        Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[-3]),
+        Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[0, 1]),
+        Batch([EmbChunk(s, 0, 2, True) for s in range(5)], [], ids[:10], chunk_adapter=[0, 1, 2, 3, 4]),
+    ]
+    for b in bad:
+        with pytest.raises(StepError) as e:
+            step_oracle((cfg, We), (cfg, We), b, okv, okv, np.zeros((6, cfg.d_model)), np.zeros(6))
+        want = KIND_CODE[e.value.kind]
+        with pytest.raises(A.OrthrusError) as g:
+            R.step(m, m, b, kv, kv, acc, accw, None, emb, ws)
+        assert g.value.code == want, (b.chunk_adapter, e.value.kind, g.value.code)
+    # four distinct adapters (one of them twice) plan fine
+    ok = Batch([EmbChunk(s, 0, 2, True) for s in range(5)], [], ids[:10], chunk_adapter=[3, 1, 3, 0, 5])
+    R.plan(m, m, ok, kv, kv)

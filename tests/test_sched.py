@@ -18,7 +18,7 @@ from paper_2609_25405_amd import runtime as R
 from paper_2609_25405_amd import _abi as A
 from workload import Batch, DecodeRow, EmbChunk, GenChunk, tiny_config
 
-POOLS = ("mean", "last", "cls")
+POOLS = ("mean", "last", "cls", "wmean")
 
 
 class _KVShape:
@@ -36,7 +36,7 @@ def _as_step_batch(b, pools):
     return Batch(chunks, rows, b["token_ids"], gen)
 
 
-def _run_pair(seed, cfg: SchedConfig, iters=80, eos_rate=0.0, vocab=50):
+def _run_pair(seed, cfg: SchedConfig, iters=80, eos_rate=0.0, vocab=50, adapters=False):
     rng = random.Random(seed)
     o = IBSOracle(cfg)
     caches = [cfg.emb_cache] if cfg.shared_cache else [cfg.emb_cache, cfg.gen_cache]
@@ -44,27 +44,30 @@ def _run_pair(seed, cfg: SchedConfig, iters=80, eos_rate=0.0, vocab=50):
                     atomic_embeddings=cfg.atomic_embeddings, decode_tokens=cfg.decode_tokens,
                     page_size=cfg.page_size, eos=cfg.eos)
     mcfg = tiny_config().replace(vocab=vocab)
-    model = (mcfg, {"lm_head": np.zeros(1)})
+    model = (mcfg, {"lm_head": np.zeros(1), "adapters": [None] * 7})
     kv_e = _KVShape(cfg.emb_cache[0], cfg.emb_cache[2])
     kv_g = kv_e if cfg.shared_cache else _KVShape(cfg.gen_cache[0], cfg.gen_cache[2])
     rid = 0
-    pools, toks, history = {}, {}, {}
+    pools, toks, history, weights = {}, {}, {}, {}
     for it in range(iters):
         for _ in range(rng.randrange(0, 4)):
             if rng.random() < 0.5:
                 ln = rng.randrange(1, 300)
                 pools[rid] = rng.choice(POOLS)
                 toks[rid] = [rng.randrange(vocab) for _ in range(ln)]
+                ad = rng.randrange(-1, 7) if adapters else -1
+                wts = [rng.random() for _ in range(ln)] if pools[rid] == "wmean" else None
+                weights[rid] = wts
                 try:
-                    o.submit_embedding(rid, ln)
+                    o.submit_embedding(rid, ln, adapter=ad)
                     ok = True
                 except SchedError:
                     ok = False
                 if ok:
-                    n.submit_embedding(rid, ln, toks[rid], pools[rid])
+                    n.submit_embedding(rid, ln, toks[rid], pools[rid], weights=wts, adapter=ad)
                 else:
                     with pytest.raises(A.OrthrusError):
-                        n.submit_embedding(rid, ln, toks[rid], pools[rid])
+                        n.submit_embedding(rid, ln, toks[rid], pools[rid], weights=wts, adapter=ad)
             else:
                 ln, mx = rng.randrange(1, 200), rng.randrange(1, 30)
                 toks[rid] = [rng.randrange(vocab) for _ in range(ln)]
@@ -83,6 +86,8 @@ def _run_pair(seed, cfg: SchedConfig, iters=80, eos_rate=0.0, vocab=50):
         ob = o.schedule()
         nb = n.next()
         assert nb["emb_chunks"] == ob.emb_chunks
+        assert nb["emb_adapters"] == ob.emb_adapters
+        assert len({a for a in nb["emb_adapters"] if a >= 0}) <= A.ORTHRUS_MAX_STEP_ADAPTERS
         assert nb["gen_chunks"] == ob.gen_chunks
         assert nb["decodes"] == ob.decodes
         assert nb["order"] == ob.order
@@ -92,6 +97,11 @@ def _run_pair(seed, cfg: SchedConfig, iters=80, eos_rate=0.0, vocab=50):
         assert nb["credits"] == (o.a_e, o.a_g)
         # the batch satisfies the step's host contract and carries the requests' tokens
         sb = _as_step_batch(nb, pools)
+        sb.chunk_adapter = nb["emb_adapters"]
+        if any(pools[c[0]] == "wmean" for c in nb["emb_chunks"]):
+            sb.token_weights = np.concatenate(
+                [np.asarray(weights[c[0]][c[1]:c[1] + c[2]], np.float32) if weights[c[0]] else
+                 np.ones(c[2], np.float32) for c in nb["emb_chunks"]])
         validate(model, model, sb, kv_e, kv_g)
         want = []
         for rid_, off, ln, _ in nb["emb_chunks"] + nb["gen_chunks"]:
@@ -129,6 +139,13 @@ def _check_tables(n: R.Scheduler, cfg: SchedConfig):
 def test_native_scheduler_matches_reference_model(seed):
     cfg = SchedConfig(budget=256, chunk=64, emb_cache=(12, 300, 40), eos=-1)
     _run_pair(seed, cfg)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_native_scheduler_matches_with_adapters(seed):
+    """Embedding requests naming LoRA adapters 0..5: no batch takes chunks of more than four."""
+    cfg = SchedConfig(budget=256, chunk=32, emb_cache=(20, 400, 40))
+    _run_pair(seed, cfg, adapters=True)
 
 
 @pytest.mark.parametrize("seed", range(4))

@@ -250,3 +250,17 @@ def test_running_requests_are_served_first_in_order():
     s2.submit_embedding(99, 4)
     b = s2.schedule()
     assert [d[0] for d in b.decodes] == [0, 1, 2, 3, 4] and b.emb_chunks == [] and b.used == 5
+
+
+def test_at_most_four_adapters_per_batch_in_arrival_order():
+    """Six embedding requests on six adapters: the first four are admitted; the fifth would add
+    a fifth adapter, so the embedding queue stops there (the sixth does not overtake it)."""
+    s = IBSOracle(SchedConfig(budget=1000, chunk=64, emb_cache=(10, 400, 40)))
+    for i in range(6):
+        s.submit_embedding(i, 10, adapter=i)
+    s.submit_embedding(6, 10, adapter=1)      # an adapter already in the batch, but behind id 4
+    b = s.schedule()
+    assert [c[0] for c in b.emb_chunks] == [0, 1, 2, 3] and b.emb_adapters == [0, 1, 2, 3]
+    s.commit()
+    b = s.schedule()
+    assert [c[0] for c in b.emb_chunks] == [4, 5, 6]
