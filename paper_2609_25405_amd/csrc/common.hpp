@@ -194,5 +194,8 @@ hipError_t launch_argmax(const float *logits, int rows, int vocab, int32_t *out,
 // their row's final norm themselves (adding npend slabs); with any_rows, mean, weighted-mean and
 // buffered chunks are handled too and need launch_final_rows over the embedding rows first.
 hipError_t launch_pool(const PoolArgs &a, bool any_rows, hipStream_t s);
+// both at once when no chunk needs every embedding row's norm (n_emb_rows == 0): the LM rows'
+// final norm and the single-row pooler in one launch
+hipError_t launch_final_and_pool(int dtype, const PoolArgs &a, hipStream_t s);
 
 }  // namespace orthrus

@@ -142,11 +142,10 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
 // lm_rows and write them, normalised with the generator's gain, as consecutive rows of the LM
 // head's input.
 template <typename T>
-__global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
-    __shared__ float red[4];
-    const bool emb_row = (int)blockIdx.x < a.n_emb_rows;
-    const int lm = (int)blockIdx.x - a.n_emb_rows;
-    const int r = emb_row ? (int)blockIdx.x : a.lm_rows[lm];
+__device__ void final_row_block(const PoolArgs &a, int b, float *red) {
+    const bool emb_row = b < a.n_emb_rows;
+    const int lm = b - a.n_emb_rows;
+    const int r = emb_row ? b : a.lm_rows[lm];
     const int nv = a.d / 4;
     float *x = const_cast<float *>(a.x) + (size_t)r * a.d;
     float ss = 0.f;
@@ -180,6 +179,12 @@ __global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
         const float4 q = load4(x + 4 * v), g = load4(a.gen_gain + 4 * v);
         store4(y + 4 * v, float4{q.x * inv * g.x, q.y * inv * g.y, q.z * inv * g.z, q.w * inv * g.w});
     }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
+    __shared__ float red[4];
+    final_row_block<T>(a, blockIdx.x, red);
 }
 
 __device__ __forceinline__ bool chunk_state_ok(const int32_t *ch, const float *acc_w) {
@@ -256,9 +261,7 @@ __global__ __launch_bounds__(256) void pool_finish_kernel(PoolArgs a) {
 // gets its final RMSNorm here (after the pending split-K slabs, if any), S of Eq. (1) takes
 // that row (last: an offset-0 chunk without it clears S), W of Eq. (2) grows by the chunk
 // length, and a final chunk writes S / max(||S||, 1e-12).
-__global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
-    __shared__ float red[4];
-    const int ci = blockIdx.x;
+__device__ void pool_rows_block(const PoolArgs &a, int ci, float *red) {
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], len = ch[2], flags = ch[3], t0 = ch[4];
     const int pool = (flags >> ORTHRUS_POOL_SHIFT) & ORTHRUS_POOL_MASK;
@@ -309,6 +312,21 @@ __global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
         const float4 q = load4(S + 4 * v);
         store4(out + 4 * v, float4{q.x * sc, q.y * sc, q.z * sc, q.w * sc});
     }
+}
+
+__global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
+    __shared__ float red[4];
+    pool_rows_block(a, blockIdx.x, red);
+}
+
+// With no head that needs every embedding row's norm, the final norm of the rows that get
+// logits and the single-row pooler are independent: one launch, blocks [0, n_lm) normalise the
+// LM rows, the following n_chunks blocks pool one chunk each.
+template <typename T>
+__global__ __launch_bounds__(256) void final_and_pool_rows_kernel(PoolArgs a) {
+    __shared__ float red[4];
+    if ((int)blockIdx.x < a.n_lm) final_row_block<T>(a, blockIdx.x, red);
+    else pool_rows_block(a, (int)blockIdx.x - a.n_lm, red);
 }
 
 // ------------------------------------------------------------------------- greedy sampler
@@ -388,6 +406,15 @@ hipError_t launch_final_rows(int dtype, const PoolArgs &a, hipStream_t s) {
     if (rows <= 0) return hipSuccess;
     if (dtype == 1) hipLaunchKernelGGL(final_rows_kernel<bf16>, dim3(rows), dim3(256), 0, s, a);
     else hipLaunchKernelGGL(final_rows_kernel<float>, dim3(rows), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_final_and_pool(int dtype, const PoolArgs &a, hipStream_t s) {
+    if (a.n_emb_rows != 0) return hipErrorInvalidValue;
+    const int blocks = a.n_lm + a.n_chunks;
+    if (blocks <= 0) return hipSuccess;
+    if (dtype == 1) hipLaunchKernelGGL(final_and_pool_rows_kernel<bf16>, dim3(blocks), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(final_and_pool_rows_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -572,10 +572,15 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     pa.hidden = batch->hidden;
     pa.n_emb_rows = any_rows ? Te : 0;
     pa.n_lm = p.n_lm;
-    if (pa.n_emb_rows + pa.n_lm > 0) RUN("final_norm", launch_final_rows(dt, pa, s));
-    // the embedding rows' pending slabs were added by the final norm when it covered them
-    if (any_rows) pa.npend = 0;
-    if (p.n_chunks > 0) RUN("pool", launch_pool(pa, any_rows, s));
+    if (!any_rows && p.n_chunks > 0 && p.n_lm > 0) {
+        // independent work: LM rows' final norm and the single-row pooler in one launch
+        RUN("final_norm_pool", launch_final_and_pool(dt, pa, s));
+    } else {
+        if (pa.n_emb_rows + pa.n_lm > 0) RUN("final_norm", launch_final_rows(dt, pa, s));
+        // the embedding rows' pending slabs were added by the final norm when it covered them
+        if (any_rows) pa.npend = 0;
+        if (p.n_chunks > 0) RUN("pool", launch_pool(pa, any_rows, s));
+    }
     if (p.n_lm > 0) {
         GemmArgs ga{};
         ga.A = act;
