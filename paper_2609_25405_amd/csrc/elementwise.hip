@@ -30,6 +30,11 @@ __device__ __forceinline__ void store4(bf16 *p, float4 v) {
     *(uint2 *)p = uint2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
 }
 
+// Rows of up to kRegV * 256 float4 (d <= 8192) are held in registers between the sum of squares
+// and the scaled write: every load of the row is issued before the first one is used (one memory
+// latency per row instead of one per 256-float4 piece) and nothing is read twice.
+constexpr int kRegV = 8;
+
 // y = x / sqrt(mean(x^2) + eps) * gain over one row per block (d a multiple of 4); gather mode
 // first sets x = table[tok] (the fp32 copy is kept as the residual stream)
 template <typename T, bool GATHER>
@@ -39,6 +44,62 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
     const int nv = a.d / 4;
     float *xrow = (GATHER ? a.x_out : const_cast<float *>(a.x)) + (size_t)r * a.d;
     float ss = 0.f;
+    if (nv <= kRegV * 256) {
+        float4 xv[kRegV];
+        if (GATHER) {
+            const T *src = (const T *)a.table + (size_t)a.tok[r] * a.d;
+#pragma unroll
+            for (int i = 0; i < kRegV; ++i) {
+                const int v = threadIdx.x + i * 256;
+                if (v < nv) xv[i] = load4(src + 4 * v);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < kRegV; ++i) {
+                const int v = threadIdx.x + i * 256;
+                if (v < nv) xv[i] = load4(xrow + 4 * v);
+            }
+            // finish a split-K residual add: x += slab 0 + slab 1 + ... in order
+            for (int sp = 0; sp < a.npend; ++sp) {
+                const float *slab = a.pend + sp * a.pend_stride + (size_t)r * a.d;
+#pragma unroll
+                for (int i = 0; i < kRegV; ++i) {
+                    const int v = threadIdx.x + i * 256;
+                    if (v < nv) {
+                        const float4 p = load4(slab + 4 * v);
+                        xv[i] = float4{xv[i].x + p.x, xv[i].y + p.y, xv[i].z + p.z, xv[i].w + p.w};
+                    }
+                }
+            }
+        }
+        if (GATHER && a.cs && threadIdx.x < a.hd / 2) {
+            // rotation table of this token for the QKV epilogue (angle evaluated in double)
+            const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
+            double sv, cv;
+            sincos((double)a.pos[r] * inv_freq, &sv, &cv);
+            a.cs[(size_t)r * (a.hd / 2) + threadIdx.x] = float2{(float)cv, (float)sv};
+        }
+#pragma unroll
+        for (int i = 0; i < kRegV; ++i) {
+            const int v = threadIdx.x + i * 256;
+            if (v < nv) {
+                if (GATHER || a.npend > 0) store4(xrow + 4 * v, xv[i]);
+                ss += xv[i].x * xv[i].x + xv[i].y * xv[i].y + xv[i].z * xv[i].z + xv[i].w * xv[i].w;
+            }
+        }
+        const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
+        T *y = (T *)a.y + (size_t)r * a.d;
+#pragma unroll
+        for (int i = 0; i < kRegV; ++i) {
+            const int v = threadIdx.x + i * 256;
+            if (v < nv) {
+                const float4 g = load4(a.gain + 4 * v);
+                store4(y + 4 * v, float4{xv[i].x * inv * g.x, xv[i].y * inv * g.y, xv[i].z * inv * g.z,
+                                         xv[i].w * inv * g.w});
+            }
+        }
+        return;
+    }
     if (GATHER && a.cs && threadIdx.x < a.hd / 2) {
         // rotation table of this token for the QKV epilogue (angle evaluated in double)
         const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
@@ -149,6 +210,50 @@ __device__ void final_row_block(const PoolArgs &a, int b, float *red) {
     const int nv = a.d / 4;
     float *x = const_cast<float *>(a.x) + (size_t)r * a.d;
     float ss = 0.f;
+    if (nv <= kRegV * 256) {
+        // the row in registers (see kRegV)
+        float4 xv[kRegV];
+#pragma unroll
+        for (int i = 0; i < kRegV; ++i) {
+            const int v = threadIdx.x + i * 256;
+            if (v < nv) xv[i] = load4(x + 4 * v);
+        }
+        for (int sp = 0; sp < a.npend; ++sp) {
+            const float *slab = a.pend + sp * a.pend_stride + (size_t)r * a.d;
+#pragma unroll
+            for (int i = 0; i < kRegV; ++i) {
+                const int v = threadIdx.x + i * 256;
+                if (v < nv) {
+                    const float4 p = load4(slab + 4 * v);
+                    xv[i] = float4{xv[i].x + p.x, xv[i].y + p.y, xv[i].z + p.z, xv[i].w + p.w};
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kRegV; ++i) {
+            const int v = threadIdx.x + i * 256;
+            if (v < nv) {
+                if (a.npend > 0) store4(x + 4 * v, xv[i]);
+                ss += xv[i].x * xv[i].x + xv[i].y * xv[i].y + xv[i].z * xv[i].z + xv[i].w * xv[i].w;
+            }
+        }
+        const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
+        if (emb_row && threadIdx.x == 0) a.inv_rms[r] = inv;
+        const int hr = emb_row && a.hid_rows ? a.hid_rows[r] : -1;
+        if (emb_row && hr < 0) return;
+        const float *gain = emb_row ? a.gain : a.gen_gain;
+#pragma unroll
+        for (int i = 0; i < kRegV; ++i) {
+            const int v = threadIdx.x + i * 256;
+            if (v < nv) {
+                const float4 g = load4(gain + 4 * v);
+                const float4 o{xv[i].x * inv * g.x, xv[i].y * inv * g.y, xv[i].z * inv * g.z, xv[i].w * inv * g.w};
+                if (emb_row) store4(a.hidden + (size_t)hr * a.d + 4 * v, o);
+                else store4((T *)a.act + (size_t)lm * a.d + 4 * v, o);
+            }
+        }
+        return;
+    }
     for (int v = threadIdx.x; v < nv; v += 256) {
         float4 q = load4(x + 4 * v);
         if (a.npend > 0) {
