@@ -91,6 +91,13 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="BLAS threads for the oracle (0 = all)")
+    ap.add_argument("--workload", default="7b-layer-mixed",
+                    choices=["7b-layer-mixed", "retrieval-sweep-32l", "long-docs-32l", "decode-heavy-32l"],
+                    help="7b-layer-mixed (default): the headline one-layer step with roofline and CPU "
+                         "baseline.  The others run the full 32-layer configurations on device-drawn "
+                         "weights and caches: two models over an embedding-fraction sweep, 16 documents "
+                         "of 8192 tokens chunked by 512 next to 32 decode rows, and 256 decode rows at "
+                         "contexts 4096-8192 next to 8 short queries")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three plain 1 GiB device copies (the reference kernel for scaling "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -109,6 +116,9 @@ def main() -> int:
               "(independent replicas per GPU; no collective in the method). Use --gpus 1.",
               file=sys.stderr)
         return 2
+    if args.workload != "7b-layer-mixed":
+        print(json.dumps(full_model_bench(args)), flush=True)
+        return 0
 
     import numpy as np
     import torch
@@ -216,6 +226,143 @@ def main() -> int:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def full_model_bench(args) -> dict:
+    """The 32-layer configurations: seeded weights and caches drawn on the device (their host
+    images would not fit), batches from the workload module's scenario generators.  Parity at
+    these sizes is covered by the one-layer tests of the same kernels; no CPU baseline here (the
+    float64 oracle would take hours per step)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_25405_amd import runtime as R
+    from workload import (decode_heavy_scenario, device_weights, fill_device_pools, llm7b_config,
+                          long_document_scenario, retrieval_mix_scenario)
+
+    L = 32
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    def device_kv(cfg, n_pages, n_seq, max_blocks, block_table, seed):
+        need = 2 * cfg.n_layers * n_pages * cfg.n_kv_heads * cfg.page_size * cfg.head_dim * 2
+        free = torch.cuda.mem_get_info()[0]
+        if need > 0.9 * free:
+            raise SystemExit(f"cache of {need / 2**30:.1f} GiB does not fit ({free / 2**30:.1f} GiB free)")
+        kv = R.DeviceKV(cfg, n_pages, n_seq, max_blocks, fill=0.0)
+        kv.set_block_table(block_table)
+        fill_device_pools(kv.k, kv.v, seed)
+        torch.cuda.synchronize()
+        log(f"cache {need / 2**30:.1f} GiB drawn")
+        return kv
+
+    def model(cfg, seed, tag):
+        W = device_weights(cfg, seed, tag)
+        torch.cuda.synchronize()
+        dm = R.DeviceModel(cfg, W)
+        del W
+        log(f"model (tag {tag}) drawn: {cfg.n_layers} layers")
+        return dm
+
+    def time_steps(dm_e, dm_g, kv_e, kv_g, batches, ws, n_seq_e, repeat):
+        """Each batch run `repeat` times back to back (a repeated step rewrites the same cache
+        slots and restarts its offset-0 chunks, so every repetition is a valid step)."""
+        acc_sum = torch.zeros((n_seq_e, dm_e.cfg.d_model), device="cuda")
+        acc_w = torch.zeros(n_seq_e, device="cuda")
+        D_max = max(b.n_logit_rows for b in batches)
+        logits = torch.empty((max(1, D_max), dm_g.cfg.vocab), device="cuda")
+        out_emb = torch.empty((max(1, max(len(b.chunks) for b in batches)), dm_e.cfg.d_model), device="cuda")
+        packed = [R.PackedBatch(b) for b in batches]
+        times = []
+        for b, pb in zip(batches, packed):
+            st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            st.record()
+            for _ in range(repeat):
+                R.step(dm_e, dm_g, b, kv_e, kv_g, acc_sum, acc_w, logits, out_emb, ws, packed=pb)
+            en.record()
+            torch.cuda.synchronize()
+            times.append(st.elapsed_time(en) / repeat)
+        assert ws.device_error() == 0, "device error"
+        return times
+
+    def attention_gbs(dm, kv_e, kv_g, batch, ws, n_seq_e):
+        acc_sum = torch.zeros((n_seq_e, dm.cfg.d_model), device="cuda")
+        acc_w = torch.zeros(n_seq_e, device="cuda")
+        logits = torch.empty((max(1, batch.n_logit_rows), dm.cfg.vocab), device="cuda")
+        out_emb = torch.empty((max(1, len(batch.chunks)), dm.cfg.d_model), device="cuda")
+        R.profile_begin(dm)
+        R.step(dm, dm, batch, kv_e, kv_g, acc_sum, acc_w, logits, out_emb, ws)
+        prof = R.profile_end(dm)
+        n, tot = prof["attention"]
+        per_launch = algorithmic_work(dm.cfg, batch)["attention"][1]
+        return per_launch / (tot / n * 1e-3) / 1e9, {k: round(v[1] / v[0] * 1e3, 1) for k, v in prof.items()}
+
+    rep = max(1, args.steps // 4)
+    base = {"metric": METRIC, "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded N(0,0.02) weights and N(0,1) bf16 caches drawn on the device, "
+                    "uniform token ids)"}
+    if args.workload == "decode-heavy-32l":
+        _, _, batch, rec = decode_heavy_scenario(n_layers=1)
+        cfg = llm7b_config(n_layers=L)
+        dm = model(cfg, rec.seed, 0)
+        kv = device_kv(cfg, rec.n_pages, rec.n_seq, rec.max_blocks, rec.block_table, rec.seed)
+        ws = R.Workspace(dm, dm, batch.n_tokens, len(batch.chunks), len(batch.rows), 8192)
+        time_steps(dm, dm, kv, kv, [batch], ws, rec.n_seq, 2)
+        (ms,) = time_steps(dm, dm, kv, kv, [batch], ws, rec.n_seq, rep)
+        gbs, kern = attention_gbs(dm, kv, kv, batch, ws, rec.n_seq)
+        Te, D = batch.n_emb_tokens, len(batch.rows)
+        return dict(base, value=(Te + D) / (ms * 1e-3), steps=rep, warmup=2, ms_per_step=ms,
+                    config={"workload": "decode-heavy-32l: 32 layers 7B shape bf16 vocab 32000; 256 decode "
+                                        "rows ctx U[4096,8192] + 8 queries x16 tokens (mean pooling), page 16",
+                            "embed_tokens": Te, "decode_tokens": D, "layers": L},
+                    embed_tokens_per_s=Te / (ms * 1e-3), decode_tokens_per_s=D / (ms * 1e-3),
+                    attention_gbs=gbs, attention_frac_hbm=gbs / PEAK_HBM_GBS, kernel_avg_us=kern)
+    if args.workload == "retrieval-sweep-32l":
+        cfg_e1, _, cfg_g1, _, paged_e, paged_g, steps = retrieval_mix_scenario(n_layers=1)
+        cfg_e, cfg_g = llm7b_config(n_layers=L, has_lm_head=False), llm7b_config(n_layers=L)
+        dm_e, dm_g = model(cfg_e, 1003, 1), model(cfg_g, 1003, 2)
+        kv_e = device_kv(cfg_e, paged_e.n_pages, paged_e.n_seq, paged_e.max_blocks, paged_e.block_table, 1)
+        kv_g = device_kv(cfg_g, paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
+        ws = R.Workspace(dm_e, dm_g, max(b.n_tokens for b in steps), max(1, max(len(b.chunks) for b in steps)),
+                         max(len(b.rows) for b in steps), 4096)
+        time_steps(dm_e, dm_g, kv_e, kv_g, steps, ws, paged_e.n_seq, 1)
+        times = time_steps(dm_e, dm_g, kv_e, kv_g, steps, ws, paged_e.n_seq, rep)
+        sweep = []
+        for f, b, t in zip((0.0, 0.25, 0.5, 0.75, 1.0), steps, times):
+            sweep.append({"embedding_fraction": f, "embed_tokens": b.n_emb_tokens, "decode_rows": len(b.rows),
+                          "ms_per_step": t, "tokens_per_s": (b.n_emb_tokens + len(b.rows)) / (t * 1e-3)})
+        tok = sum(b.n_emb_tokens + len(b.rows) for b in steps)
+        ms = sum(times) / len(times)
+        return dict(base, value=tok / (sum(times) * 1e-3), steps=rep * len(steps), warmup=len(steps),
+                    ms_per_step=ms,
+                    config={"workload": "retrieval-sweep-32l: two 32-layer 7B-shape models (embedding: mean "
+                                        "pooling, no LM head; generator: vocab 32000), 2048-token budget, "
+                                        "embedding fraction 0/.25/.5/.75/1, queries lognormal mean 64, up to "
+                                        "256 decode rows with contexts lognormal mean 512",
+                            "layers": L},
+                    embed_tokens_per_s=sum(b.n_emb_tokens for b in steps) / (sum(times) * 1e-3),
+                    decode_tokens_per_s=sum(len(b.rows) for b in steps) / (sum(times) * 1e-3),
+                    sweep=sweep)
+    # long documents
+    _, _, paged, steps = long_document_scenario(n_layers=1, n_docs=16, doc_len=8192, chunk=512, per_step=3,
+                                                n_dec=32, ctx0=2048)
+    cfg = llm7b_config(n_layers=L)
+    dm = model(cfg, 1004, 0)
+    kv = device_kv(cfg, paged.n_pages, paged.n_seq, paged.max_blocks, paged.block_table, 4)
+    ws = R.Workspace(dm, dm, max(b.n_tokens for b in steps), 3, 32, paged.max_blocks * 16)
+    time_steps(dm, dm, kv, kv, steps[:1], ws, paged.n_seq, 2)
+    times = time_steps(dm, dm, kv, kv, steps, ws, paged.n_seq, 1)
+    Te = sum(b.n_emb_tokens for b in steps)
+    D = sum(len(b.rows) for b in steps)
+    tsum = sum(times) * 1e-3
+    return dict(base, value=(Te + D) / tsum, steps=len(steps), warmup=2, ms_per_step=sum(times) / len(times),
+                config={"workload": "long-docs-32l: 32 layers 7B shape bf16 vocab 32000; 16 documents x8192 "
+                                    "tokens chunked by 512 (mean pooling), 3 chunks per step, + 32 decode rows "
+                                    "from context 2048", "layers": L, "steps": len(steps)},
+                embed_tokens_per_s=Te / tsum, decode_tokens_per_s=D / tsum,
+                ms_per_step_first_last=[times[0], times[-1]])
 
 
 def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):

@@ -46,6 +46,8 @@ class DeviceModel:
         dt = torch_dtype(cfg)
 
         def up(a, dtype=dt):
+            if isinstance(a, torch.Tensor):      # already on the device (drawn there)
+                return a.to(device=device, dtype=dtype).contiguous()
             return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(device=device, dtype=dtype)
 
         self.tok_emb = up(weights["tok_emb"])

@@ -601,6 +601,44 @@ def decode_heavy_scenario(seed: int = 1005, n_layers: int = 1, n_dec: int = 256,
     return cfg, W, Batch(chunks=chunks, rows=rows, token_ids=ids), DeviceKVRecipe(n_pages, n_seq, max_blocks, bt, seed)
 
 
+def device_weights(cfg: ModelConfig, seed: int, model_tag: int = 0, std: float = 0.02, device="cuda") -> Dict:
+    """Seeded N(0, std) weights drawn on the device in the model dtype (torch tensors), same
+    layout as make_weights, for shapes whose host image would be too large (32-layer 7B models).
+    Each tensor has its own generator seed, derived from (seed, model_tag, layer, tensor)."""
+    import torch
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    d, F = cfg.d_model, cfg.d_ff
+
+    def draw(layer, name, shape):
+        key = np.random.SeedSequence(seed, spawn_key=(model_tag, layer, _TENSOR_IDS[name])).generate_state(1)[0]
+        g = torch.Generator(device=device)
+        g.manual_seed(int(key))
+        out = torch.empty(shape, dtype=dt, device=device)
+        flat = out.view(-1)
+        step = 1 << 26
+        for i in range(0, flat.numel(), step):
+            part = flat[i:i + step]
+            part.copy_((torch.randn(part.numel(), generator=g, device=device) * std).to(dt))
+        return out
+
+    ones = lambda: torch.ones(d, dtype=torch.float32, device=device)
+    W = {"tok_emb": draw(_GLOBAL_LAYER, "tok_emb", (cfg.vocab, d)), "final_norm": ones(),
+         "lm_head": draw(_GLOBAL_LAYER, "lm_head", (cfg.vocab, d)) if cfg.has_lm_head else None,
+         "layers": []}
+    for l in range(cfg.n_layers):
+        W["layers"].append({
+            "attn_norm": ones(),
+            "w_qkv": torch.cat([draw(l, "w_q", (cfg.q_dim, d)), draw(l, "w_k", (cfg.kv_dim, d)),
+                                draw(l, "w_v", (cfg.kv_dim, d))]),
+            "w_o": draw(l, "w_o", (d, cfg.q_dim)),
+            "mlp_norm": ones(),
+            "w_gate": draw(l, "w_gate", (F, d)),
+            "w_up": draw(l, "w_up", (F, d)),
+            "w_down": draw(l, "w_down", (d, F)),
+        })
+    return W
+
+
 def fill_device_pools(k, v, seed: int) -> None:
     """Fill device key/value pools with N(0, 1) values of their dtype from a seeded device
     generator (torch tensors; values, not a method step)."""
