@@ -517,18 +517,27 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //  - residual-add projections with split-K slabs: 192x256 over 8 waves, split 2 (o 58 -> 46 us,
 //    down 177 -> 135 us against 128x128 tiles);
 //  - otherwise 128x128 (64 KiB of LDS, two workgroups per CU hide each other's waits).
+//  - medium M (64 < M <= 896: decode-heavy and small mixed batches, where the weights stream):
+//    more, smaller workgroups and deeper split-K for the residual-add projections (down at
+//    M = 384: 124 -> 57 us; o: 42 -> 23 us), 64x128 tiles for QKV up to M = 512, and for
+//    gate/up up to M = 896 the 128- or 192-row tile that pads M least (M = 512: 162 -> 129 us).
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
     if constexpr (EPI == EPI_QKV_ROPE) {
         if (a.M <= 64) return run_bf16<64, 128, 2, 2, EPI, 64, 4>(a, s);
+        if (a.M <= 512) return run_bf16<64, 128, 1, 4, EPI, 64, 3>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else if constexpr (EPI == EPI_SWIGLU) {
         if (a.M <= 64) return run_bf16<64, 256, 1, 4, EPI, 64, 3>(a, s);
-        if (a.M > 128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        const int pad128 = (a.M + 127) / 128 * 128 - a.M, pad192 = (a.M + 191) / 192 * 192 - a.M;
+        if (a.M > 896 || (a.M > 128 && pad192 <= pad128)) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else {
         if (a.M <= 64) return run_bf16<64, 64, 2, 2, EPI, 64, 4>(a, s);
-        if (EPI == EPI_ADD_F32 && a.partial && a.splits > 1) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        const bool split = EPI == EPI_ADD_F32 && a.partial && a.splits > 1;
+        if (split && a.M <= 192) return run_bf16<64, 64, 2, 2, EPI, 64, 4>(a, s);
+        if (split && a.M <= 896) return run_bf16<128, 128, 2, 2, EPI>(a, s);
+        if (split) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         if (EPI == EPI_ADD_F32) return run_bf16<128, 128, 4, 2, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     }
@@ -536,18 +545,25 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
 
 }  // namespace
 
-// Split-K factor for a residual-add projection on the bf16 path, for the tiles dispatch_bf16
-// uses with it (64x64 for M <= 64, else 192x256, one workgroup per CU): the factor whose
-// workgroups fill the last round over 256 CUs best, the smaller one on a tie, each split a whole
-// number of 64-deep stages and at least 512 deep.  1 = no split.
+// Split-K factor for a residual-add projection on the bf16 path, matched to the tiles
+// dispatch_bf16 uses with it.  M <= 64 (64x64 tiles): the factor whose workgroups fill the last
+// round over 256 CUs best, the smaller one on a tie.  Larger M, from measurements of the 7B
+// projections: 4 up to M = 640 (64x64 or 128x128 tiles; weight streaming wants many workgroups),
+// then 2 (128x128 up to M = 896, 192x256 beyond), where more slabs cost more traffic than they
+// gain.  Every split is a whole number of 64-deep stages and at least 512 deep.  1 = no split.
 int gemm_add_splits(int M, int N, int K, int max_splits) {
-    const int bm = M <= 64 ? 64 : 192, bn = M <= 64 ? 64 : 256;
-    const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    auto valid = [&](int s) { return s <= max_splits && K % (s * BK) == 0 && K / s >= 512; };
+    if (M > 64) {
+        int s = M <= 640 ? 4 : 2;
+        while (s > 1 && !valid(s)) s /= 2;
+        return s;
+    }
+    const long tiles = (long)((M + 63) / 64) * ((N + 63) / 64);
     auto fill = [](long w) { const long rounds = (w + 255) / 256; return (double)w / (double)(rounds * 256); };
     int best = 1;
-    double best_fill = M <= 64 ? fill(tiles) : 0.0;   // M > 64 without a split uses other tiles
+    double best_fill = fill(tiles);
     for (int s = 2; s <= max_splits; ++s) {
-        if (K % (s * BK) || K / s < 512) continue;
+        if (!valid(s)) continue;
         const double f = fill(tiles * s);
         if (f > best_fill + 1e-9) { best = s; best_fill = f; }
     }

@@ -389,9 +389,13 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.lora = lg;
         return launch_gemm(dt, epi, ga, s);
     };
-    // residual-add projection into x; one model and bf16: split K when the tile count is low and
-    // leave the slabs for the next row-wise kernel (returns the split count)
-    auto add_proj = [&](const Group &g, const char *A, int lda, const void *B, int K, int &splits,
+    // residual-add projection into x; bf16: split K when the tile count is low and leave the
+    // slabs for the next row-wise kernel.  `splits` is chosen once per projection for the largest
+    // row group and used by every group, so the pending slab count is the same for all rows.
+    int max_rows = 0;
+    for (int gi = 0; gi < n_groups; ++gi) max_rows = std::max(max_rows, groups[gi].r1 - groups[gi].r0);
+    auto add_splits = [&](int K) { return slabs ? gemm_add_splits(max_rows, d, K, kMaxSplits) : 1; };
+    auto add_proj = [&](const Group &g, const char *A, int lda, const void *B, int K, int splits,
                         const LoraGemm &lg) -> hipError_t {
         GemmArgs ga{};
         ga.A = A + (size_t)g.r0 * lda * es;
@@ -402,9 +406,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.K = K;
         ga.lda = lda;
         ga.ldo = d;
-        splits = (slabs && n_groups == 1) ? gemm_add_splits(ga.M, d, K, kMaxSplits) : 1;
         ga.splits = splits;
-        ga.partial = slabs;
+        ga.partial = slabs ? slabs + (size_t)g.r0 * d : nullptr;  // the group's rows of each slab
         ga.split_stride = slab_stride;
         ga.lora = lg;
         return launch_gemm(dt, EPI_ADD_F32, ga, s);
@@ -518,7 +521,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         }
         RUN("attention", launch_attention(dt, aa, s));
         if (p.n_split_rows > 0) RUN("attn_combine", launch_attn_combine(dt, aa, p.D, s));
-        int splits = 1;
+        int splits = add_splits(qd);
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             LoraGemm lg{};
@@ -534,6 +537,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
             if (lora_on(2, groups[gi])) RUN("lora_shrink", lora(2, l, groups[gi], act, d, d, lg));
             RUN("gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d, lg));
         }
+        splits = add_splits(F);
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             LoraGemm lg{};
