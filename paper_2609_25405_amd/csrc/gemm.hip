@@ -178,8 +178,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
     // with the next k-step's fragments read under the current k-step's.  (Spreading the copies
     // between the MFMAs, or L2 prefetches further ahead, measured slower on MI355X.)
     constexpr int NMF = FM * FN, NFR = FM + FN;
-    const int nk = a.K / BKS / splits;
-    const int kt0 = split * nk;
+    // this split's stages: [kt0, kt0 + nk), the K stages dealt as evenly as the count allows
+    const int nk_all = a.K / BKS;
+    const int kt0 = split * nk_all / splits;
+    const int nk = (split + 1) * nk_all / splits - kt0;
     for (int i = -(SDD - 1); i < 0; ++i) issue(i, kt0, nk);
     for (int kt = 0; kt < nk; ++kt) {
         __builtin_amdgcn_s_waitcnt(vmcnt_imm<IN_FLIGHT>());
@@ -501,7 +503,7 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
     const int cols = EPI == EPI_SWIGLU ? BN / 2 : BN;
     const int nt = (a.N + cols - 1) / cols;
     const int splits =
-        (EPI == EPI_ADD_F32 && a.partial && a.splits > 1 && a.K % (a.splits * BK) == 0) ? a.splits : 1;
+        (EPI == EPI_ADD_F32 && a.partial && a.splits > 1 && a.K % BKS == 0 && a.K / BKS >= a.splits) ? a.splits : 1;
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, BKS, STAGES, BSTAGES>), dim3(mt * nt * splits),
                        dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
@@ -514,8 +516,10 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //    workgroups) with a 4-deep copy ring keep enough bytes in flight per CU (LM head
 //    64 x 32000 x 4096: 70 -> 43 us with warm caches; decode-batch QKV 35 -> 25 us);
 //  - gate/up: 192x256 tiles over 8 waves;
-//  - residual-add projections with split-K slabs: 192x256 over 8 waves, split 2 (o 58 -> 46 us,
-//    down 177 -> 135 us against 128x128 tiles);
+//  - residual-add projections of M > 896 rows: 256x256 tiles over 8 waves with the split-K
+//    count gemm_add_splits picks (o 58 -> 46 us, down 177 -> 135 us against 128x128 tiles at
+//    M = 1088; down at M = 1568 264 -> 195 us, at M = 2048 275 -> 211 us against 192x256
+//    tiles split 2, whose 288 or 352 workgroups spill into a second round);
 //  - otherwise 128x128 (64 KiB of LDS, two workgroups per CU hide each other's waits).
 //  - medium M (64 < M <= 896: decode-heavy and small mixed batches, where the weights stream):
 //    more, smaller workgroups and deeper split-K for the residual-add projections (down at
@@ -537,7 +541,7 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
         const bool split = EPI == EPI_ADD_F32 && a.partial && a.splits > 1;
         if (split && a.M <= 192) return run_bf16<64, 64, 2, 2, EPI, 64, 4>(a, s);
         if (split && a.M <= 896) return run_bf16<128, 128, 2, 2, EPI>(a, s);
-        if (split) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        if (EPI == EPI_ADD_F32 && a.partial && a.M > 896) return run_bf16<256, 256, 2, 4, EPI>(a, s);
         if (EPI == EPI_ADD_F32) return run_bf16<128, 128, 4, 2, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     }
@@ -546,13 +550,30 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 // Split-K factor for a residual-add projection on the bf16 path, matched to the tiles
-// dispatch_bf16 uses with it.  M <= 64 (64x64 tiles): the factor whose workgroups fill the last
-// round over 256 CUs best, the smaller one on a tie.  Larger M, from measurements of the 7B
-// projections: 4 up to M = 640 (64x64 or 128x128 tiles; weight streaming wants many workgroups),
-// then 2 (128x128 up to M = 896, 192x256 beyond), where more slabs cost more traffic than they
-// gain.  Every split is a whole number of 64-deep stages and at least 512 deep.  1 = no split.
+// dispatch_bf16 uses with it.  Each split takes a run of whole 64-deep stages (the stages dealt
+// as evenly as the count allows), at least 512 deep.  1 = no split.
+//  - M <= 64 (64x64 tiles): the factor whose workgroups fill the last round over 256 CUs best,
+//    the smaller one on a tie;
+//  - 64 < M <= 896, from measurements of the 7B projections: 4 up to M = 640 (64x64 or 128x128
+//    tiles; weight streaming wants many workgroups), then 2;
+//  - M > 896 (256x256 tiles, one workgroup per CU): the factor with the least (rounds of
+//    workgroups over 256 CUs) x (stages per split), the smaller one on a tie.  The copies of a
+//    round's stages bound these launches, so a second round that is only partly full costs as
+//    much as the first (M = 1568: split 2 fills one round with 224 workgroups).
 int gemm_add_splits(int M, int N, int K, int max_splits) {
-    auto valid = [&](int s) { return s <= max_splits && K % (s * BK) == 0 && K / s >= 512; };
+    const int stages = K / BK;
+    auto valid = [&](int s) { return s <= max_splits && K % BK == 0 && K / s >= 512; };
+    if (M > 896) {
+        const long tiles = (long)((M + 255) / 256) * ((N + 255) / 256);
+        int best = 1;
+        long best_cost = -1;
+        for (int s = 1; s <= max_splits; ++s) {
+            if (s > 1 && !valid(s)) continue;
+            const long cost = (tiles * s + 255) / 256 * ((stages + s - 1) / s);
+            if (best_cost < 0 || cost < best_cost) { best = s; best_cost = cost; }
+        }
+        return best;
+    }
     if (M > 64) {
         int s = M <= 640 ? 4 : 2;
         while (s > 1 && !valid(s)) s /= 2;
