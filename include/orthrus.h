@@ -247,7 +247,10 @@ int orthrus_device_error(void *workspace, void *stream, int32_t *bits);
  * and split).  If `items` is non-NULL it receives up to `cap` items of 8 int32 each:
  *   {kind (0 prefill, 1 decode), chunk or row index, kv head, q_begin or split index,
  *    q_count or n_splits, key_begin, key_end (exclusive), partial slot or -1}.
- * Chunk indices count the embedding chunks first, then the generation prefill chunks. */
+ * Chunk indices count the embedding chunks first, then the generation prefill chunks.  On the
+ * bf16 path a prefill tile over a long cached prefix may be cut along its keys into pieces (one
+ * item each, cuts on 64-key boundaries at or before the tile's first query): a piece has a
+ * partial slot, the first of 128 / group consecutive slots holding its rows. */
 int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, int32_t *n_prefill_items,
                  int32_t *n_decode_items, int32_t *items, int32_t cap);

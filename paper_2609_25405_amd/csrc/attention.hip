@@ -13,7 +13,10 @@
 //     and walks the keys of its request in 32-key blocks, with operands loaded straight from
 //     the cache (L2-resident, shared by the group's waves) one block ahead of the MFMAs, an
 //     online softmax in fp32 (exp2 domain) and causal masking on the diagonal blocks.  Waves
-//     never synchronise, so each stops at its own causal bound.
+//     never synchronise, so each stops at its own causal bound.  A tile over a long cached
+//     prefix comes as several items, one per run of keys (the walk is serial, about a
+//     microsecond per 32-key block, so one long tile would otherwise set the launch's length);
+//     those write partials like split decode rows, merged by attn_combine.
 //   * decode items: one (decode row, KV head, key-range split), walked in 128-key chunks.  Each
 //     wave owns two pages of a chunk, scores with v_dot2_f32_bf16 for all `group` query heads
 //     at once, keeps an online softmax, and accumulates P V from registers; the next chunk's K
@@ -445,7 +448,10 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     constexpr int KS = HD / 16, DB = HD / 32;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int ci = it[IT_INDEX], g = it[IT_KVHEAD], qb = it[IT_A], qn = it[IT_B];
-    const int kend = it[IT_KEY_END];               // causal bound of the whole tile
+    // keys [k0, kend) of the tile: all of them up to its causal bound, or one piece of a
+    // key-split tile (pieces start on 64-key boundaries, so block k0 / 32 is even; only the last
+    // piece reaches the diagonal), whose (max, sum, unnormalised output) go to partial slots
+    const int k0 = it[IT_KEY_BEGIN], kend = it[IT_KEY_END], pslot = it[IT_PARTIAL];
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], tok0 = ch[4];
     const int sb = wave / G;
@@ -458,7 +464,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     const PoolView pv = pool_view(a, chunk_pool(ch));
     const size_t page_bytes = (size_t)a.nkv * kPage * HD * 2;
     const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks;
-    const int nkb = (kend + 31) / 32;
+    const int kb0 = k0 / 32, nkb = (kend + 31) / 32;
     const int last_block = (kend - 1) / kPage;      // last page index the tile reads
 
     // page ids of the tile's keys, staged in LDS a window at a time (validated there, -1 = bad)
@@ -473,7 +479,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         }
         if (bad) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
     };
-    int w0 = 0;
+    int w0 = 2 * kb0;
     auto page_of = [&](int blk) -> int2 {  // pages of the block's two halves; -1 = bad
         const int p0 = min(2 * blk, last_block), p1 = min(2 * blk + 1, last_block);
         return int2{pg_lds[p0 - w0], pg_lds[p1 - w0]};
@@ -638,19 +644,19 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
                 }
         }
     };
-    load_window(0);
+    load_window(w0);
     __syncthreads();
-    int2 pg_b0 = page_of(0);
+    int2 pg_b0 = page_of(kb0);
     issue(stg0, pg_b0);
-    stash(stg0, smem, 0, pg_b0);
-    int2 pg_b1 = nkb > 1 ? page_of(1) : int2{-1, -1};
-    int2 pg_b2 = nkb > 2 ? page_of(2) : int2{-1, -1};
-    if (nkb > 1) issue(stg1, pg_b1);
-    if (nkb > 2) issue(stg0, pg_b2);
+    stash(stg0, smem, kb0, pg_b0);
+    int2 pg_b1 = kb0 + 1 < nkb ? page_of(kb0 + 1) : int2{-1, -1};
+    int2 pg_b2 = kb0 + 2 < nkb ? page_of(kb0 + 2) : int2{-1, -1};
+    if (kb0 + 1 < nkb) issue(stg1, pg_b1);
+    if (kb0 + 2 < nkb) issue(stg0, pg_b2);
     __syncthreads();
     // iteration kb: compute block kb, stash block kb + 1 from its stage, reuse that stage for
     // block kb + 3; stage of block b is stg1 for odd b, stg0 for even b
-    for (int kb = 0; kb < nkb; kb += 2) {
+    for (int kb = kb0; kb < nkb; kb += 2) {
         compute(kb);
         if (kb + 1 < nkb) stash(stg1, smem + St::BYTES, kb + 1, pg_b1);
         int2 pg_b3 = {-1, -1};
@@ -672,6 +678,23 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         pg_b2 = pg_b4;
     }
     if (col >= rows) return;
+    if (pslot >= 0) {
+        // piece of a split tile: row r of the tile is slot pslot + r, holding the group's heads
+        float *pp = a.partials + ((size_t)(pslot + sb * 32 + col) * G + (wave % G)) * (HD + 2);
+        if (half == 0) {
+            pp[0] = m;
+            pp[1] = l;
+        }
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                float2 *dst = (float2 *)(pp + 2 + d * 32 + q4 * 8 + half * 4);
+                dst[0] = float2{acc[d][q4 * 4 + 0], acc[d][q4 * 4 + 1]};
+                dst[1] = float2{acc[d][q4 * 4 + 2], acc[d][q4 * 4 + 3]};
+            }
+        return;
+    }
     const float inv = l > 0.f ? 1.f / l : 0.f;
     bf16 *op = (bf16 *)a.o + ((size_t)tok * a.nq + h) * HD;
 #pragma unroll
@@ -708,37 +731,85 @@ __global__ __launch_bounds__(256, BF16 ? 2 : 1) void attn_kernel(AttnArgs a) {
     }
 }
 
-// Merge the key-range splits of one (decode row, KV head) for its `group` query heads, in split
-// order: M = max m_s, L = sum l_s 2^(m_s - M), o = sum acc_s 2^(m_s - M) / L.
-template <typename T, int HD, int G>
-__global__ __launch_bounds__(G * HD) void attn_combine_kernel(AttnArgs a) {
-    const int j = blockIdx.x, g = blockIdx.y;
-    const int h = threadIdx.x / HD, d = threadIdx.x % HD;
-    const int32_t *row = a.rows + kRowInts * j;
-    const int nsplit = row[3], base = row[4], tok = row[2];
-    if (nsplit <= 1) return;
-    constexpr int STRIDE = G * (HD + 2);  // floats between consecutive splits of one head
-    const float *pp = a.partials + ((size_t)(base + g * nsplit) * G + h) * (HD + 2);
+// Merge key-range partials in split order: M = max m_s, L = sum l_s 2^(m_s - M),
+// o = sum acc_s 2^(m_s - M) / L.  Blocks [0, n_dec_blocks): one (decode row, KV head) each, for
+// its `group` query heads; then kCombineRows rows of one key-split prefill tile per block.  Up to
+// kCombineSplits splits are loaded in one round before any arithmetic (a block is a single
+// memory round trip), longer decode rows loop.
+constexpr int kCombineRows = 4;
+constexpr int kCombineSplits = 8;
+static_assert(kMaxPrefillSplits <= kCombineSplits, "prefill pieces load in one round");
+
+template <typename T>
+__device__ __forceinline__ void merge_splits(const AttnArgs &a, const float *pp, size_t stride, int nsplit,
+                                             int d, size_t out) {
+    float m[kCombineSplits], l[kCombineSplits], v[kCombineSplits];
+#pragma unroll
+    for (int s = 0; s < kCombineSplits; ++s) {
+        if (s < nsplit) {
+            const float *q = pp + (size_t)s * stride;
+            m[s] = q[0];
+            l[s] = q[1];
+            v[s] = q[2 + d];
+        }
+    }
     float M = -INFINITY;
-#pragma unroll 8
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pp[(size_t)s * STRIDE]);
+#pragma unroll
+    for (int s = 0; s < kCombineSplits; ++s)
+        if (s < nsplit) M = fmaxf(M, m[s]);
+    for (int s = kCombineSplits; s < nsplit; ++s) M = fmaxf(M, pp[(size_t)s * stride]);
     float L = 0.f, acc = 0.f;
-#pragma unroll 8
-    for (int s = 0; s < nsplit; ++s) {
-        const float *q = pp + (size_t)s * STRIDE;
+#pragma unroll
+    for (int s = 0; s < kCombineSplits; ++s) {
+        if (s < nsplit) {
+            const float w = (m[s] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[s] - M);
+            L += l[s] * w;
+            acc += v[s] * w;
+        }
+    }
+    for (int s = kCombineSplits; s < nsplit; ++s) {
+        const float *q = pp + (size_t)s * stride;
         const float w = (q[0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(q[0] - M);
         L += q[1] * w;
         acc += q[2 + d] * w;
     }
-    ((T *)a.o)[((size_t)tok * a.nq + g * G + h) * HD + d] = from_f32<T>(L > 0.f ? acc / L : 0.f);
+    ((T *)a.o)[out] = from_f32<T>(L > 0.f ? acc / L : 0.f);
+}
+
+template <typename T, int HD, int G>
+__global__ __launch_bounds__(G * HD) void attn_combine_kernel(AttnArgs a, int n_dec_blocks) {
+    const int h = threadIdx.x / HD, d = threadIdx.x % HD;
+    if ((int)blockIdx.x < n_dec_blocks) {
+        const int j = blockIdx.x / a.nkv, g = blockIdx.x % a.nkv;
+        const int32_t *row = a.rows + kRowInts * j;
+        const int nsplit = row[3];
+        if (nsplit <= 1) return;
+        const float *pp = a.partials + ((size_t)(row[4] + g * nsplit) * G + h) * (HD + 2);
+        merge_splits<T>(a, pp, (size_t)G * (HD + 2), nsplit, d, ((size_t)row[2] * a.nq + g * G + h) * HD + d);
+        return;
+    }
+    constexpr int QR = kPrefillRows / G, BPM = QR / kCombineRows;   // blocks per merge entry
+    const int b = blockIdx.x - n_dec_blocks;
+    const int32_t *mg = a.combine + kCombineInts * (b / BPM);
+    const int r0 = (b % BPM) * kCombineRows;
+#pragma unroll
+    for (int i = 0; i < kCombineRows; ++i) {
+        const int r = r0 + i;
+        if (r < mg[1]) {
+            const float *pp = a.partials + ((size_t)(mg[4] + r) * G + h) * (HD + 2);
+            merge_splits<T>(a, pp, (size_t)QR * G * (HD + 2), mg[3], d,
+                            ((size_t)(mg[0] + r) * a.nq + mg[2] * G + h) * HD + d);
+        }
+    }
 }
 
 template <bool BF16, int HD, int G>
 hipError_t run(const AttnArgs &a, int n_decode, bool combine, hipStream_t s) {
     if (combine) {
-        if (n_decode <= 0) return hipSuccess;
-        if (BF16) hipLaunchKernelGGL((attn_combine_kernel<bf16, HD, G>), dim3(n_decode, a.nkv), dim3(G * HD), 0, s, a);
-        else hipLaunchKernelGGL((attn_combine_kernel<float, HD, G>), dim3(n_decode, a.nkv), dim3(G * HD), 0, s, a);
+        const int n_dec = n_decode * a.nkv, blocks = n_dec + a.n_combine * (kPrefillRows / G / kCombineRows);
+        if (blocks <= 0) return hipSuccess;
+        if (BF16) hipLaunchKernelGGL((attn_combine_kernel<bf16, HD, G>), dim3(blocks), dim3(G * HD), 0, s, a, n_dec);
+        else hipLaunchKernelGGL((attn_combine_kernel<float, HD, G>), dim3(blocks), dim3(G * HD), 0, s, a, n_dec);
         return hipGetLastError();
     }
     if (a.n_items <= 0) return hipSuccess;

@@ -158,11 +158,14 @@ struct AttnArgs {
     const int32_t *block_table[2];
     int n_pages[2], max_blocks[2];
     const int32_t *chunks, *rows, *items;
+    const int32_t *combine;   // merge entries of key-split prefill tiles
     float *partials;          // [slot][group][hd + 2]
-    int n_prefill, n_items, Te, nq, nkv, hd, page;
+    int n_prefill, n_items, n_combine, Te, nq, nkv, hd, page;
     int *err;
 };
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
+// merges the partials of split decode rows (the first n_decode rows' entries; 0 = none) and of
+// the a.n_combine key-split prefill tiles
 hipError_t launch_attn_combine(int dtype, const AttnArgs &a, int n_decode, hipStream_t s);
 
 struct PoolArgs {

@@ -151,33 +151,63 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     const int qrows = kPrefillRows / group;  // tokens per prefill item
 
     // --- attention work list: prefill query tiles (heaviest first), then decode splits
-    struct Pre { long long work; int chunk, kvh, qb, qn, kend; };
-    std::vector<Pre> pre;
+    struct Pre { long long work; int chunk, kvh, qb, qn, k0, k1, piece; };
+    std::vector<Pre> tiles;
     for (int i = 0; i < n_all; ++i) {
         const int32_t *ch = &chunks[kChunkInts * i];
         const int off = ch[1], len = ch[2];
         for (int qb = 0; qb < len; qb += qrows) {
             const int qn = std::min(qrows, len - qb);
             const int kend = off + qb + qn;
-            for (int g = 0; g < nkv; ++g) pre.push_back({(long long)kend * qn, i, g, qb, qn, kend});
+            for (int g = 0; g < nkv; ++g) tiles.push_back({(long long)kend * qn, i, g, qb, qn, 0, kend, -1});
         }
     }
-    std::stable_sort(pre.begin(), pre.end(), [](const Pre &a, const Pre &b2) { return a.work > b2.work; });
+    std::stable_sort(tiles.begin(), tiles.end(), [](const Pre &a, const Pre &b2) { return a.work > b2.work; });
+    // key splits of the longest tiles (bf16): cuts on 64-key boundaries at or before the tile's
+    // first query position, so only the last piece reaches the causal diagonal; heaviest tiles
+    // first while the piece budget lasts
+    std::vector<Pre> pre;
+    struct Merge { int tok, qn, kvh, n, piece0; };
+    std::vector<Merge> merges;
+    int n_pieces = 0;
+    {
+        long long keys = 0;
+        for (const Pre &t : tiles) keys += t.k1;
+        // a tile is cut only when it is more than twice the mean keys per workgroup slot (else
+        // the launch is bound by its total work, and pieces only add partial traffic), into
+        // pieces of about that mean, at least kPrefillSplitKeys keys
+        const long long mean = (keys + kAttnSlots - 1) / kAttnSlots;
+        const long long target = std::max<long long>(kPrefillSplitKeys, mean);
+        const bool may_split = emb.cfg.dtype == ORTHRUS_BF16;
+        for (const Pre &t : tiles) {
+            const int first_q = t.k1 - t.qn;                    // keys below it are seen by every row
+            int n = may_split && t.k1 > 2 * mean
+                        ? (int)std::min<long long>(kMaxPrefillSplits, (t.k1 + target - 1) / target)
+                        : 1;
+            std::vector<int> cuts{0};
+            for (int k = 1; k < n; ++k) {
+                const int c = std::min((int)((long long)k * t.k1 / n) / 64 * 64, first_q / 64 * 64);
+                if (c > cuts.back()) cuts.push_back(c);
+            }
+            n = (int)cuts.size();
+            if (n < 2 || n_pieces + n > kMaxPrefillPieces) {
+                pre.push_back(t);
+                continue;
+            }
+            cuts.push_back(t.k1);
+            const int32_t *ch = &chunks[kChunkInts * t.chunk];
+            merges.push_back({ch[4] + t.qb, t.qn, t.kvh, n, n_pieces});
+            for (int k = 0; k < n; ++k)
+                pre.push_back({(long long)(cuts[k + 1] - cuts[k]) * t.qn, t.chunk, t.kvh, t.qb, t.qn, cuts[k],
+                               cuts[k + 1], n_pieces + k});
+            n_pieces += n;
+        }
+        std::stable_sort(pre.begin(), pre.end(), [](const Pre &a, const Pre &b2) { return a.work > b2.work; });
+    }
     p.n_prefill = (int)pre.size();
+    p.n_split_prefill = (int)merges.size();
 
     std::vector<int32_t> rows(kRowInts * p.D);
-    std::vector<int32_t> items(kItemInts * pre.size());
-    for (size_t k = 0; k < pre.size(); ++k) {
-        int32_t *it = &items[kItemInts * k];
-        it[IT_KIND] = 0;
-        it[IT_INDEX] = pre[k].chunk;
-        it[IT_KVHEAD] = pre[k].kvh;
-        it[IT_A] = pre[k].qb;
-        it[IT_B] = pre[k].qn;
-        it[IT_KEY_BEGIN] = 0;
-        it[IT_KEY_END] = pre[k].kend;
-        it[IT_PARTIAL] = -1;
-    }
     // decode splits: whole chunks of kSplitPages pages, up to `cps` chunks per split, the
     // row's chunks dealt out evenly over its splits
     const int cps = gen.cfg.dtype == ORTHRUS_BF16 ? kDecodeChunksBf16 : 1;
@@ -219,9 +249,32 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
                                                 const std::array<int32_t, kItemInts> &y) {
         return x[IT_KEY_END] - x[IT_KEY_BEGIN] > y[IT_KEY_END] - y[IT_KEY_BEGIN];
     });
+    // prefill pieces take partial slots after the decode rows': piece k of a split tile holds
+    // its qrows tokens in consecutive slots, pieces of one tile qrows slots apart
+    std::vector<int32_t> items(kItemInts * pre.size());
+    std::vector<int32_t> combine(kCombineInts * merges.size());
+    for (size_t k = 0; k < pre.size(); ++k) {
+        int32_t *it = &items[kItemInts * k];
+        it[IT_KIND] = 0;
+        it[IT_INDEX] = pre[k].chunk;
+        it[IT_KVHEAD] = pre[k].kvh;
+        it[IT_A] = pre[k].qb;
+        it[IT_B] = pre[k].qn;
+        it[IT_KEY_BEGIN] = pre[k].k0;
+        it[IT_KEY_END] = pre[k].k1;
+        it[IT_PARTIAL] = pre[k].piece < 0 ? -1 : partial + pre[k].piece * qrows;
+    }
+    for (size_t i = 0; i < merges.size(); ++i) {
+        int32_t *m = &combine[kCombineInts * i];
+        m[0] = merges[i].tok;
+        m[1] = merges[i].qn;
+        m[2] = merges[i].kvh;
+        m[3] = merges[i].n;
+        m[4] = partial + merges[i].piece0 * qrows;
+    }
     for (const auto &it : dec) items.insert(items.end(), it.begin(), it.end());
     p.n_decode_items = (int)(items.size() / kItemInts) - p.n_prefill;
-    p.n_partials = partial;
+    p.n_partials = partial + n_pieces * qrows;
 
     // --- pack
     p.off_tok = 0;
@@ -231,7 +284,8 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     p.off_rows = p.off_chunks + kChunkInts * n_all;
     p.off_items = p.off_rows + kRowInts * p.D;
     p.off_lm = p.off_items + (int)items.size();
-    int end = p.off_lm + p.n_lm;
+    p.off_combine = p.off_lm + p.n_lm;
+    int end = p.off_combine + (int)combine.size();
     if (p.any_wmean) {
         p.off_wts = end;
         end += p.Te;
@@ -281,6 +335,7 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     std::copy(chunks.begin(), chunks.end(), p.meta.begin() + p.off_chunks);
     std::copy(rows.begin(), rows.end(), p.meta.begin() + p.off_rows);
     std::copy(items.begin(), items.end(), p.meta.begin() + p.off_items);
+    std::copy(combine.begin(), combine.end(), p.meta.begin() + p.off_combine);
     return ORTHRUS_OK;
 }
 

@@ -18,6 +18,20 @@ constexpr int kSplitPages = 16;
 // Chunks per decode split on the bf16 path (its items pipeline one chunk's loads under the
 // previous chunk's arithmetic, so longer splits keep the memory pipe busier).
 constexpr int kDecodeChunksBf16 = 4;
+// Key splits of prefill items on the bf16 path.  A prefill item walks its keys one 32-key
+// block after another, so an item over a long cached prefix can outlast the rest of the launch
+// however many CUs are idle.  Items with more than twice the batch's mean prefill keys per
+// workgroup slot (kAttnSlots = 256 CUs x two 256-thread workgroups) are cut into pieces of
+// whole 64-key runs, about that mean long and at least kPrefillSplitKeys, at most
+// kMaxPrefillSplits per item and kMaxPrefillPieces per step (their partials fit a fixed part of
+// the workspace).
+constexpr int kPrefillSplitKeys = 2048;
+constexpr int kMaxPrefillSplits = 8;
+constexpr int kMaxPrefillPieces = 1024;
+constexpr int kAttnSlots = 512;
+// int32 fields of one merge entry of a split prefill item: first token, tokens, kv head,
+// pieces, first partial slot (piece k of row r: slot + k * (kPrefillRows / group) + r)
+constexpr int kCombineInts = 5;
 
 struct Model {
     orthrus_config cfg;
@@ -49,6 +63,7 @@ struct StepPlan {
     int T = 0, Te = 0, Tg = 0, D = 0, n_chunks = 0, n_gen = 0;
     bool shared_kv = true;
     int n_prefill = 0, n_decode_items = 0, n_partials = 0, n_split_rows = 0;
+    int n_split_prefill = 0;  // prefill items cut along keys (merge entries at off_combine)
     int n_lm = 0;  // rows that get logits: last rows of final prompt chunks, then decode rows
     // heads in the batch that need every embedding row's final norm (mean, weighted mean,
     // buffered), and the optional per-token arrays they read
@@ -58,11 +73,11 @@ struct StepPlan {
     int n_used = 0;
     int used[ORTHRUS_MAX_STEP_ADAPTERS] = {0, 0, 0, 0};
     int off_radp = -1;
-    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows, then
+    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows combine, then
     // (weighted mean) fp32 weights[Te] and (buffered head) hidden-buffer row[Te] (-1: none)
     std::vector<int32_t> meta;
     int off_tok = 0, off_pos = 0, off_seq = 0, off_chunks = 0, off_rows = 0, off_items = 0,
-        off_lm = 0, off_wts = -1, off_hid = -1;
+        off_lm = 0, off_combine = 0, off_wts = -1, off_hid = -1;
 };
 
 int validate_config(const orthrus_config &c);

@@ -222,11 +222,17 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
     const size_t splits = max_splits_for_ctx(max_ctx, m.cfg.page_size);
     const size_t pre_items = ((size_t)max_tokens / qrows + max_chunks) * nkv;
     const size_t dec_items = (size_t)max_decode * nkv * splits;
+    // key-split prefill tiles (bf16): each piece adds at most one item and holds qrows partial
+    // slots; a split tile has at least two pieces, so merge entries number at most pieces / 2
+    const size_t pieces = m.cfg.dtype == ORTHRUS_BF16
+                              ? std::min<size_t>(kMaxPrefillPieces, (size_t)kMaxPrefillSplits * pre_items)
+                              : 0;
     const size_t meta = 3 * (size_t)max_tokens + kChunkInts * (size_t)max_chunks +
-                        kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items) +
+                        kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items + pieces) +
+                        kCombineInts * (pieces / 2) +
                         (size_t)max_chunks + max_decode +  // rows that get logits
                         2 * (size_t)max_tokens;            // token weights, hidden-buffer rows
-    return make_layout(m, max_tokens, meta, dec_items).total;
+    return make_layout(m, max_tokens, meta, dec_items + pieces * qrows).total;
 }
 
 int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
@@ -426,6 +432,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     aa.chunks = meta + p.off_chunks;
     aa.rows = meta + p.off_rows;
     aa.items = meta + p.off_items;
+    aa.combine = meta + p.off_combine;
+    aa.n_combine = p.n_split_prefill;
     aa.partials = (float *)(ws + L.partials);
     aa.n_prefill = p.n_prefill;
     aa.n_items = p.n_prefill + p.n_decode_items;
@@ -520,7 +528,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
             aa.v_cache[i] = ra.v_cache[i];
         }
         RUN("attention", launch_attention(dt, aa, s));
-        if (p.n_split_rows > 0) RUN("attn_combine", launch_attn_combine(dt, aa, p.D, s));
+        if (p.n_split_rows > 0 || p.n_split_prefill > 0)
+            RUN("attn_combine", launch_attn_combine(dt, aa, p.n_split_rows > 0 ? p.D : 0, s));
         int splits = add_splits(qd);
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];

@@ -189,23 +189,43 @@ def test_undersized_workspace_is_rejected_before_launch():
 
 
 def _check_coverage(batch, cfg, npre, ndec, items):
-    """Every (chunk token, kv head) in exactly one prefill tile with the causal key bound, and
-    every (decode row, kv head, key) in exactly one decode split."""
+    """Every (chunk token, kv head) in exactly one prefill tile, whose keys up to the causal bound
+    are covered once (whole, or in key pieces cut on 64-key boundaries at or before the tile's
+    first query, each with its own block of partial slots), and every (decode row, kv head, key)
+    in exactly one decode split."""
     P_ = cfg.page_size
     group = cfg.n_q_heads // cfg.n_kv_heads
+    qrows = 128 // group
     seen_q = {}
+    pieces = {}
     work = []
+    piece_slots = []
     for it in items[:npre]:
         kind, ci, g, qb, qn, kb, ke, ps = it
-        assert kind == 0 and ps == -1 and kb == 0
+        assert kind == 0
         c = batch.chunks[ci]
-        assert 1 <= qn <= 128 // group and qb + qn <= c.len
-        assert ke == c.offset + qb + qn
+        assert 1 <= qn <= qrows and qb + qn <= c.len
+        pieces.setdefault((ci, g, qb, qn), []).append((kb, ke, ps))
+        work.append((ke - kb) * qn)
+    for (ci, g, qb, qn), ps_ in pieces.items():
+        c = batch.chunks[ci]
+        ps_.sort()
+        assert ps_[0][0] == 0 and ps_[-1][1] == c.offset + qb + qn
+        if len(ps_) == 1:
+            assert ps_[0][2] == -1
+        else:
+            assert 2 <= len(ps_) <= 8 and cfg.dtype == "bf16"
+            for (kb, ke, ps), nxt in zip(ps_, ps_[1:] + [None]):
+                assert kb % 64 == 0 and ps >= 0
+                if nxt is not None:
+                    assert ke == nxt[0] and ke <= c.offset + qb      # every row sees the piece
+            base = ps_[0][2]
+            assert [x[2] for x in ps_] == [base + k * qrows for k in range(len(ps_))]
+            piece_slots += [(base + k * qrows, qrows) for k in range(len(ps_))]
         for r in range(qb, qb + qn):
             key = (ci, g, r)
             assert key not in seen_q
             seen_q[key] = True
-        work.append(ke * qn)
     assert len(seen_q) == sum(c.len for c in batch.chunks) * cfg.n_kv_heads
     assert work == sorted(work, reverse=True)  # heaviest first
     seen_k = {}
@@ -234,20 +254,38 @@ def _check_coverage(batch, cfg, npre, ndec, items):
     assert lengths == sorted(lengths, reverse=True)
     if slots:
         assert slots == set(range(len(slots)))
+    # prefill pieces: disjoint blocks of qrows slots after the decode rows' slots
+    taken = set(slots)
+    for base, n in piece_slots:
+        block = set(range(base, base + n))
+        assert min(block) >= len(slots) and not (block & taken)
+        taken |= block
+    return len(piece_slots)
 
 
-@pytest.mark.parametrize("cfgname", ["tiny", "7b"])
+@pytest.mark.parametrize("cfgname", ["tiny", "7b", "7b-long-prefix", "7b-three-long"])
 def test_plan_covers_every_key_exactly_once(cfgname):
+    rng = np.random.default_rng(0)
     if cfgname == "tiny":
         cfg = tiny_config()
         chunks = [EmbChunk(0, 0, 128, False), EmbChunk(1, 256, 44, True)]
         rows = [DecodeRow(2, 0), DecodeRow(3, 255), DecodeRow(4, 256), DecodeRow(5, 1000)]
-    else:
+    elif cfgname == "7b":
         cfg = llm7b_config(n_layers=1)
         chunks = [EmbChunk(0, 0, 512, False, "last"), EmbChunk(1, 1536, 512, True, "last")]
-        rng = np.random.default_rng(0)
         rows = [DecodeRow(2 + i, int(c)) for i, c in enumerate(rng.integers(1024, 4097, 64))]
-    n_seq = 2 + len(rows)
+    elif cfgname == "7b-long-prefix":
+        # one chunk at the end of an 8192-token document: 128 tiles of ~8000 keys, each cut in 4
+        cfg = llm7b_config(n_layers=1)
+        chunks = [EmbChunk(0, 7680, 512, True, "mean")]
+        rows = [DecodeRow(2 + i, 2100) for i in range(32)]
+    else:
+        # three chunks at 4096: 384 tiles of at most 4608 keys, under twice the mean keys per
+        # workgroup slot (the launch is bound by its total work): no cuts
+        cfg = llm7b_config(n_layers=1)
+        chunks = [EmbChunk(i, 4096, 512, False, "mean") for i in range(3)]
+        rows = [DecodeRow(3 + i, 2100) for i in range(32)]
+    n_seq = 1 + max([c.seq for c in chunks] + [r.seq for r in rows])
     # planning reads no weight memory: tiny stand-in tensors carry the shapes' pointers
     small = cfg.replace(n_layers=0, vocab=64) if cfgname == "7b" else cfg
     W = make_weights(small, 0)
@@ -257,7 +295,10 @@ def test_plan_covers_every_key_exactly_once(cfgname):
     ids = np.zeros(sum(c.len for c in chunks) + len(rows), np.int32)
     b = Batch(chunks, rows, ids)
     npre, ndec, items = R.plan(m, m, b, kv, kv)
-    _check_coverage(b, cfg if cfgname == "tiny" else small, npre, ndec, items)
+    n_pieces = _check_coverage(b, cfg if cfgname == "tiny" else small, npre, ndec, items)
+    # cuts only on the bf16 path, for tiles over twice the mean keys per slot, into pieces of
+    # about that mean and at least 2048 keys
+    assert n_pieces == {"tiny": 0, "7b": 0, "7b-long-prefix": 128 * 4, "7b-three-long": 0}[cfgname]
 
 
 def test_prompt_chunks_need_an_lm_head_only_for_logits():

@@ -53,6 +53,37 @@ def _gqa_config(dtype="bf16", n_layers=2):
                        d_ff=1024, vocab=512, dtype=dtype)
 
 
+def test_long_prefix_prefill_key_splits():
+    """Chunks over long cached prefixes (bf16): the planner cuts their query tiles along the keys
+    into pieces whose partials the combine merges in piece order.  Two resuming chunks with
+    ragged query tails (6000 and 2500 cached tokens), a chunk with no prefix and a decode row;
+    embeddings, pooling state, logits and every cache write match the oracle."""
+    cfg = _gqa_config("bf16")
+    W = make_weights(cfg, 11, qk_std=0.06)
+    n_seq, max_blocks = 4, 400
+    pk = PagedKV(cfg, n_seq * max_blocks + 3, n_seq, max_blocks, 11)
+    pk.fill_random(0, 6000, 11)
+    pk.reserve(0, 6070)
+    pk.fill_random(1, 2500, 12)
+    pk.reserve(1, 2540)
+    pk.reserve(2, 50)
+    pk.fill_random(3, 3000, 13)
+    pk.reserve(3, 3001)
+    acc_w = np.zeros(n_seq)
+    acc_w[0], acc_w[1] = 6000, 2500
+    pair = Pair(cfg, W, pk, acc_w=acc_w)
+    pair.workspace(max_tokens=256, max_chunks=3, max_decode=1, max_ctx=4096)
+    chunks = [EmbChunk(0, 6000, 70, True, "mean"), EmbChunk(1, 2500, 40, False, "mean"),
+              EmbChunk(2, 0, 50, True, "last")]
+    b = Batch(chunks, [DecodeRow(3, 3000)], draw_tokens(11, 1, 70 + 40 + 50 + 1, cfg.vocab))
+    npre, _, items = R.plan(pair.dm_e, pair.dm_e, b, pair.dkv_e, pair.dkv_e)
+    pieces = items[:npre][items[:npre, 7] >= 0]
+    # chunk 0's tiles in 3 pieces (6032..6070 keys, 2048-key target), chunk 1's in 2
+    assert len(pieces) == 2 * (3 * 3 + 2 * 2), pieces
+    pair.step(b)
+    print(pair.report, flush=True)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_gqa_long_context_splits(dtype):
     """Grouped-query shape (group 4, head_dim 128) with multi-split decode rows, chunk offsets
