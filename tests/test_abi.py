@@ -200,15 +200,16 @@ def _check_coverage(batch, cfg, npre, ndec, items):
     pieces = {}
     work = []
     piece_slots = []
+    allc = list(batch.chunks) + list(getattr(batch, "gen_chunks", None) or [])
     for it in items[:npre]:
         kind, ci, g, qb, qn, kb, ke, ps = it
         assert kind == 0
-        c = batch.chunks[ci]
+        c = allc[ci]
         assert 1 <= qn <= qrows and qb + qn <= c.len
         pieces.setdefault((ci, g, qb, qn), []).append((kb, ke, ps))
         work.append((ke - kb) * qn)
     for (ci, g, qb, qn), ps_ in pieces.items():
-        c = batch.chunks[ci]
+        c = allc[ci]
         ps_.sort()
         assert ps_[0][0] == 0 and ps_[-1][1] == c.offset + qb + qn
         if len(ps_) == 1:
@@ -226,7 +227,7 @@ def _check_coverage(batch, cfg, npre, ndec, items):
             key = (ci, g, r)
             assert key not in seen_q
             seen_q[key] = True
-    assert len(seen_q) == sum(c.len for c in batch.chunks) * cfg.n_kv_heads
+    assert len(seen_q) == sum(c.len for c in allc) * cfg.n_kv_heads
     assert work == sorted(work, reverse=True)  # heaviest first
     seen_k = {}
     slots = set()
@@ -299,6 +300,56 @@ def test_plan_covers_every_key_exactly_once(cfgname):
     # cuts only on the bf16 path, for tiles over twice the mean keys per slot, into pieces of
     # about that mean and at least 2048 keys
     assert n_pieces == {"tiny": 0, "7b": 0, "7b-long-prefix": 128 * 4, "7b-three-long": 0}[cfgname]
+
+
+def _random_plan(seed):
+    """Plan of a random batch checked by _check_coverage; returns the number of key pieces."""
+    rng = np.random.default_rng(seed)
+    if seed % 2 == 0:
+        cfg = llm7b_config(n_layers=1)
+        small = cfg.replace(n_layers=0, vocab=64)
+    else:
+        cfg = ModelConfig(n_layers=1, d_model=512, n_q_heads=8, n_kv_heads=4, head_dim=64, d_ff=512,
+                          vocab=64, dtype="bf16")
+        small = cfg
+    W = make_weights(small, 0)
+    m = R.DeviceModel(small, W, device="cpu")
+    seqs = iter(range(1000))
+    def offset():
+        return int(rng.choice([0, rng.integers(1, 600), rng.integers(2000, 12000)]))
+    chunks = [EmbChunk(next(seqs), offset(), int(rng.integers(1, 600)), bool(rng.integers(0, 2)), "mean")
+              for _ in range(int(rng.integers(0, 5)))]
+    gen = [GenChunk(next(seqs), offset(), int(rng.integers(1, 300)), bool(rng.integers(0, 2)))
+           for _ in range(int(rng.integers(0, 3)))]
+    rows = [DecodeRow(next(seqs), int(rng.integers(0, 9000))) for _ in range(int(rng.integers(0, 40)))]
+    if not (chunks or gen or rows):
+        rows = [DecodeRow(next(seqs), 5)]
+    n_seq = next(seqs)
+    kv = type("KV", (), {})()
+    kv.struct = lambda: A.orthrus_kv(1, 1, 1, 1 << 22, n_seq, 1024)
+    n_tok = sum(c.len for c in chunks) + sum(c.len for c in gen) + len(rows)
+    b = Batch(chunks, rows, np.zeros(n_tok, np.int32), gen)
+    npre, ndec, items = R.plan(m, m, b, kv, kv)
+    n_pieces = _check_coverage(b, small, npre, ndec, items)
+    assert n_pieces <= 1024
+    for it in items[:npre]:
+        if it[7] >= 0:
+            assert it[6] - it[5] >= 64
+    return n_pieces
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_plan_invariants_on_random_batches(seed):
+    """Random mixes of fresh and resuming chunks (some after long cached prefixes), prompt chunks
+    and decode rows on the 7B shape and a group-2 bf16 shape: every query row and key is covered
+    once, key pieces follow their rules, slot blocks are disjoint, pieces stay within budget."""
+    _random_plan(seed)
+
+
+def test_random_batches_exercise_key_pieces():
+    """The random batches above include tiles cut into key pieces (most seeds) and plans without."""
+    n = [_random_plan(s) for s in range(24)]
+    assert sum(1 for x in n if x) >= 12 and 0 in n
 
 
 def test_prompt_chunks_need_an_lm_head_only_for_logits():
