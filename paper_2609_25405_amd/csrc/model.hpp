@@ -11,10 +11,15 @@
 #include "plan.hpp"
 
 struct orthrus_model : public orthrus::Model {
-    // pinned host staging for the per-step metadata upload, double-buffered with events
+    // pinned host staging for the per-step metadata upload, double-buffered with events:
+    // fine-grained (coherent) host memory that the upload kernel reads through its device
+    // address; buffers outgrown by a larger batch are retired, not freed, until the handle is
+    // destroyed
     std::mutex mu;
     void *stage[2] = {nullptr, nullptr};
+    void *stage_dev[2] = {nullptr, nullptr};
     size_t stage_bytes[2] = {0, 0};
+    std::vector<void *> retired;
     hipEvent_t ev[2] = {nullptr, nullptr};
     int next = 0;
     // kernel timing (orthrus_profile_begin / _end)

@@ -73,22 +73,37 @@ bool kv_ok(const orthrus_kv *kv) {
         if ((expr) != hipSuccess) return ORTHRUS_EHIP;  \
     } while (0)
 
+// The step's metadata goes from pinned host memory to the workspace through this kernel on the
+// step's stream, which reads the fine-grained host buffer itself.  An asynchronous host-to-device
+// copy hands off to a copy engine and back: 30-50 us of idle GPU per step for a 6.8 us transfer
+// of 64 KB, against a few microseconds here.
+__global__ __launch_bounds__(256) void meta_upload_kernel(const int4 *src, int4 *dst, int n16) {
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < n16; i += gridDim.x * 256) dst[i] = src[i];
+}
+
 int upload_meta(orthrus_model *m, const StepPlan &p, void *dst, hipStream_t s) {
     std::lock_guard<std::mutex> lk(m->mu);
     const int i = m->next;
     m->next ^= 1;
     const size_t bytes = p.meta.size() * 4;
+    const size_t n16 = (bytes + 15) / 16;  // the destination region is rounded up to 256 bytes
     if (m->ev[i]) HIP_TRY(hipEventSynchronize(m->ev[i]));
     else HIP_TRY(hipEventCreateWithFlags(&m->ev[i], hipEventDisableTiming));
-    if (m->stage_bytes[i] < bytes) {
-        if (m->stage[i]) HIP_TRY(hipHostFree(m->stage[i]));
-        m->stage[i] = nullptr;
+    if (m->stage_bytes[i] < n16 * 16) {
+        if (m->stage[i]) m->retired.push_back(m->stage[i]);
+        m->stage[i] = m->stage_dev[i] = nullptr;
         m->stage_bytes[i] = 0;
-        HIP_TRY(hipHostMalloc(&m->stage[i], bytes * 2, hipHostMallocDefault));
-        m->stage_bytes[i] = bytes * 2;
+        void *h = nullptr;
+        HIP_TRY(hipHostMalloc(&h, n16 * 32, hipHostMallocCoherent));
+        m->stage[i] = h;
+        m->stage_bytes[i] = n16 * 32;
+        HIP_TRY(hipHostGetDevicePointer(&m->stage_dev[i], h, 0));
     }
     std::memcpy(m->stage[i], p.meta.data(), bytes);
-    HIP_TRY(hipMemcpyAsync(dst, m->stage[i], bytes, hipMemcpyHostToDevice, s));
+    const int blocks = (int)std::min<size_t>((n16 + 255) / 256, 128);
+    hipLaunchKernelGGL(meta_upload_kernel, dim3(blocks), dim3(256), 0, s, (const int4 *)m->stage_dev[i],
+                       (int4 *)dst, (int)n16);
+    HIP_TRY(hipGetLastError());
     HIP_TRY(hipEventRecord(m->ev[i], s));
     return ORTHRUS_OK;
 }
@@ -209,6 +224,7 @@ void orthrus_model_destroy(orthrus_model *m) {
         }
         if (m->stage[i]) (void)hipHostFree(m->stage[i]);
     }
+    for (void *r : m->retired) (void)hipHostFree(r);
     delete m;
 }
 
