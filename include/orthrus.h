@@ -175,7 +175,9 @@ typedef struct orthrus_batch {
  * (keys stored after rotation, position-major inside a page); v_cache:
  * [n_layers][n_pages][n_kv_heads][hd][page] (dim-major inside a page, so that 8 consecutive
  * positions of one value dim are contiguous).  block_table: int32 [n_seq][max_blocks]; position
- * p of request s lives in page block_table[s][p / page] at in-page position p % page. */
+ * p of request s lives in page block_table[s][p / page] at in-page position p % page.  For a
+ * model without layers the pools are never touched and may be NULL (the block table is still
+ * validated). */
 typedef struct orthrus_kv {
     void *k_cache;
     void *v_cache;

@@ -63,9 +63,10 @@ bool same_shape(const orthrus_config &a, const orthrus_config &b) {
            a.rms_eps == b.rms_eps;
 }
 
-bool kv_ok(const orthrus_kv *kv) {
-    return kv && kv->k_cache && kv->v_cache && kv->block_table && kv->n_pages > 0 && kv->n_seq > 0 &&
-           kv->max_blocks > 0;
+// a model without layers never reads or writes its cache: its pools may be NULL
+bool kv_ok(const orthrus_kv *kv, const orthrus_model *m) {
+    return kv && (m->cfg.n_layers == 0 || (kv->k_cache && kv->v_cache)) && kv->block_table && kv->n_pages > 0 &&
+           kv->n_seq > 0 && kv->max_blocks > 0;
 }
 
 #define HIP_TRY(expr)                                   \
@@ -254,7 +255,7 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
 int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, int32_t *n_prefill_items,
                  int32_t *n_decode_items, int32_t *items, int32_t cap) {
-    if (!emb || !gen || !batch || !kv_ok(emb_kv) || !kv_ok(gen_kv)) return ORTHRUS_EINVAL;
+    if (!emb || !gen || !batch || !kv_ok(emb_kv, emb) || !kv_ok(gen_kv, gen)) return ORTHRUS_EINVAL;
     if (gen != emb && !same_shape(emb->cfg, gen->cfg)) return ORTHRUS_EUNSUPPORTED;
     StepPlan p;
     const int rc = plan_step(*emb, *gen, *batch, *emb_kv, *gen_kv, p);
@@ -271,7 +272,7 @@ int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthr
 int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
                  float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream) {
-    if (!emb || !gen || !batch || !workspace || !kv_ok(emb_kv) || !kv_ok(gen_kv)) return ORTHRUS_EINVAL;
+    if (!emb || !gen || !batch || !workspace || !kv_ok(emb_kv, emb) || !kv_ok(gen_kv, gen)) return ORTHRUS_EINVAL;
     if (gen != emb && !same_shape(emb->cfg, gen->cfg)) return ORTHRUS_EUNSUPPORTED;
     if (batch->n_chunks > 0 && (!acc_sum || !acc_w || !out_emb)) return ORTHRUS_EINVAL;
     if (batch->n_decode > 0 && !out_logits) return ORTHRUS_EINVAL;

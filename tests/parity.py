@@ -155,6 +155,8 @@ class Pair:
         slots = written_slots(batch, self.bt, P, self.shared_kv)
         pools = [(self.dkv_e, self.okv_e)] + ([] if self.shared_kv else [(self.dkv_g, self.okv_g)])
         for pi, (dkv, okv) in enumerate(pools):
+            if dkv.k.shape[0] == 0:
+                continue          # a model without layers has an empty cache
             mine = [(pg, off) for (pool, pg, off) in slots if pool == pi]
             mask = torch.zeros(dkv.k.shape[1:4], dtype=torch.bool, device="cuda")  # page, kvh, off
             if mine:

@@ -352,6 +352,29 @@ def test_random_batches_exercise_key_pieces():
     assert sum(1 for x in n if x) >= 12 and 0 in n
 
 
+def test_null_cache_pools_only_for_a_model_without_layers():
+    """A model without layers never touches its cache pools, so they may be NULL; with layers a
+    NULL pool is rejected before any device work (the block table is required either way)."""
+    for n_layers, want in ((0, None), (2, A.ORTHRUS_EINVAL)):
+        cfg = tiny_config().replace(n_layers=n_layers)
+        m = R.DeviceModel(cfg, make_weights(cfg, 3), device="cpu")
+        bt = np.zeros((2, 4), np.int32)
+        kv = type("KV", (), {})()
+        kv.struct = lambda: A.orthrus_kv(None, None, bt.ctypes.data, 8, 2, 4)
+        b = Batch([EmbChunk(0, 0, 5, True)], [DecodeRow(1, 3)], np.zeros(6, np.int32))
+        if want is None:
+            npre, ndec, _ = R.plan(m, m, b, kv, kv)
+            assert npre == cfg.n_kv_heads and ndec == cfg.n_kv_heads
+        else:
+            with pytest.raises(A.OrthrusError) as e:
+                R.plan(m, m, b, kv, kv)
+            assert e.value.code == want
+        kv.struct = lambda: A.orthrus_kv(None, None, None, 8, 2, 4)
+        with pytest.raises(A.OrthrusError) as e:
+            R.plan(m, m, b, kv, kv)
+        assert e.value.code == A.ORTHRUS_EINVAL
+
+
 def test_prompt_chunks_need_an_lm_head_only_for_logits():
     """A final prompt chunk asks for logits; the oracle and the library both refuse it on a model
     without an LM head, and both accept a non-final prompt chunk there."""
