@@ -84,6 +84,38 @@ def algorithmic_work(cfg, batch):
     return work
 
 
+def step_roofline(cfg, batch, t_step_ms):
+    """Ideal step time if every kernel class ran at its own roofline, one after another:
+    sum over classes of max(F / bf16 MFMA peak, B / HBM peak), with F the algorithmic flops and
+    B the least HBM bytes the class must move (weights, activations in and out, the KV it reads
+    and writes, the residual stream read and written once; split-K slabs, partials and
+    metadata are implementation traffic and not counted).  Returns (ideal_ms, ideal / measured)."""
+    T, Te, D = batch.n_tokens, batch.n_emb_tokens, len(batch.rows)
+    d, F, V = cfg.d_model, cfg.d_ff, cfg.vocab
+    qd, kvd, qkv = cfg.q_dim, cfg.kv_dim, cfg.qkv_dim
+    es = 2 if cfg.dtype == "bf16" else 4
+    L = cfg.n_layers
+    pairs = sum(sum(c.offset + i + 1 for i in range(c.len)) for c in batch.chunks)
+    dec_keys = sum(r.ctx_len + 1 for r in batch.rows)
+    chunk_keys = sum(c.offset + c.len for c in batch.chunks)       # each chunk reads its keys once
+    kv_per_key = 2 * kvd * es
+    n_lm = D + sum(1 for c in getattr(batch, "gen_chunks", None) or [] if c.last)
+    classes = {
+        "gather_norm": (0.0, T * d * (es + 4 + es)),
+        "gemm_qkv_rope": (2.0 * T * d * qkv * L, (d * qkv * es + T * d * es + T * qd * es + T * kv_per_key) * L),
+        "attention": (4.0 * pairs * cfg.head_dim * cfg.n_q_heads * L,
+                      ((dec_keys + chunk_keys) * kv_per_key + 2 * T * qd * es) * L),
+        "gemm_o": (2.0 * T * qd * d * L, (qd * d * es + T * qd * es + 2 * T * d * 4) * L),
+        "rmsnorm": (0.0, T * d * (4 + es) * (2 * L - 1)),
+        "gemm_gate_up": (2.0 * T * d * 2 * F * L, (2 * F * d * es + T * d * es + T * F * es) * L),
+        "gemm_down": (2.0 * T * F * d * L, (F * d * es + T * F * es + 2 * T * d * 4) * L),
+        "final_norm_pool": (0.0, (n_lm + len(batch.chunks)) * d * (4 + es)),
+        "lm_head": (2.0 * n_lm * d * V, d * V * es + n_lm * d * es + n_lm * V * 4),
+    }
+    ideal_s = sum(max(f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)) for f, b in classes.values())
+    return ideal_s * 1e3, ideal_s * 1e3 / t_step_ms
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -222,6 +254,27 @@ def main() -> int:
         "roofline": roof,
         "kernels": kernels,
     }
+    ideal_ms, frac = step_roofline(cfg, batch, ms)
+    result["step_roofline"] = {"ideal_ms": ideal_ms, "frac": frac,
+                               "definition": "sum over kernel classes of max(algorithmic flops / 2.5 PFLOP/s, "
+                                             "least HBM bytes / 8 TB/s), divided by the measured step time"}
+    # the decode rows alone (no chunk tiles in the attention launch): HBM figure of the decode
+    # attention without the chunk tiles that share its CUs in the mixed step
+    from workload import Batch
+    dec_batch = Batch([], batch.rows, batch.token_ids[Te:])
+    dec_packed = R.PackedBatch(dec_batch)
+    for _ in range(3):
+        R.step(dm, dm, dec_batch, kv, kv, acc_sum, acc_w, logits, out_emb, ws, packed=dec_packed)
+    R.profile_begin(dm)
+    for _ in range(20):
+        R.step(dm, dm, dec_batch, kv, kv, acc_sum, acc_w, logits, out_emb, ws, packed=dec_packed)
+    prof_dec = R.profile_end(dm)
+    torch.cuda.synchronize()
+    assert ws.device_error() == 0, "device error during the decode-only pass"
+    n_a, tot_a = prof_dec["attention"]
+    dec_bytes = algorithmic_work(cfg, dec_batch)["attention"][1]
+    result["attention_decode_only"] = {"avg_ms": tot_a / n_a, "gbs": dec_bytes / (tot_a / n_a * 1e-3) / 1e9,
+                                       "frac_hbm": dec_bytes / (tot_a / n_a * 1e-3) / 1e9 / PEAK_HBM_GBS}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
     print(json.dumps(result), flush=True)
