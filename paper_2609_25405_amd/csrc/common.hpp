@@ -138,7 +138,10 @@ struct NormArgs {
 hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t s);
 
 struct RopeArgs {
-    const float *qkv;        // fp32 [T][qkv_dim]
+    const float *qkv;        // fp32 [T][qkv_dim]: nslab partial sums slab_stride floats apart,
+    int nslab;               // added in order (split-K of the QKV projection); 1 = plain rows
+    size_t slab_stride;
+    const float2 *cs;        // per-token (cos, sin) table [T][hd/2], or null: computed here
     void *q_out;             // [T][nq][hd] model dtype
     const int32_t *pos, *seq;
     void *k_cache[2], *v_cache[2];          // layer base per pool

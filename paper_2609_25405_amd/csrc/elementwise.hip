@@ -141,33 +141,68 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
 // pos % page of page block_table[seq][pos / page] (keys [kv head][slot][dim], values
 // [kv head][dim][slot]).
 template <typename T>
+// One token per blockIdx.x; its work items (rotation quads of the q and k heads, then value
+// quads) are dealt over gridDim.y blocks.  Angles come from the per-token table when the step
+// built one (the same values the fused GEMM epilogue uses), else in double here.
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
     __shared__ __attribute__((aligned(16))) float cs[64], sn[64];
     const int t = blockIdx.x;
     const int half = a.hd / 2;
     const int pos = a.pos[t];
     if (threadIdx.x < half) {
-        const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
-        double sv, cv;
-        sincos((double)pos * inv_freq, &sv, &cv);
-        cs[threadIdx.x] = (float)cv;
-        sn[threadIdx.x] = (float)sv;
+        if (a.cs) {
+            const float2 v = a.cs[(size_t)t * half + threadIdx.x];
+            cs[threadIdx.x] = v.x;
+            sn[threadIdx.x] = v.y;
+        } else {
+            const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
+            double sv, cv;
+            sincos((double)pos * inv_freq, &sv, &cv);
+            cs[threadIdx.x] = (float)cv;
+            sn[threadIdx.x] = (float)sv;
+        }
     }
     __syncthreads();
     const int p = t < a.Te ? 0 : 1;
     const int seq = a.seq[t];
     const int page = a.block_table[p][(size_t)seq * a.max_blocks[p] + pos / a.page];
     const bool ok = page >= 0 && page < a.n_pages[p];
-    if (!ok && threadIdx.x == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
+    if (!ok && threadIdx.x == 0 && blockIdx.y == 0) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
     const int qkv_dim = (a.nq + 2 * a.nkv) * a.hd;
     const float *src = a.qkv + (size_t)t * qkv_dim;
+    // four values of the row: the sum of the split-K partials, in split order
+    auto slab4 = [&](const float *p) {
+        float4 v = *(const float4 *)p;
+        for (int k = 1; k < a.nslab; ++k) {
+            const float4 w = *(const float4 *)(p + k * a.slab_stride);
+            v.x += w.x;
+            v.y += w.y;
+            v.z += w.z;
+            v.w += w.w;
+        }
+        return v;
+    };
     const size_t slot = ok ? (((size_t)page * a.nkv) * a.page + pos % a.page) * a.hd : 0;
-    // rotations: (nq + nkv) heads x (half / 4) quads of pairs (i..i+3, i+half..i+half+3)
+    // rotations: (nq + nkv) heads x (half / 4) quads of pairs (i..i+3, i+half..i+half+3); then
+    // values, stored dim-major inside a page: [kv head][dim][slot]
     const int quads = half / 4;
-    for (int w = threadIdx.x; w < (a.nq + a.nkv) * quads; w += 256) {
+    const int n_rot = (a.nq + a.nkv) * quads, n_all = n_rot + a.nkv * a.hd / 4;
+    const float *vs = src + (size_t)(a.nq + a.nkv) * a.hd;
+    T *v = ok ? (T *)a.v_cache[p] + (size_t)page * a.nkv * a.hd * a.page + pos % a.page : nullptr;
+    for (int w = blockIdx.y * 256 + threadIdx.x; w < n_all; w += gridDim.y * 256) {
+        if (w >= n_rot) {
+            if (!ok) continue;
+            const int u = w - n_rot;
+            const float4 x = slab4(vs + 4 * u);
+            v[(size_t)(4 * u + 0) * a.page] = from_f32<T>(x.x);
+            v[(size_t)(4 * u + 1) * a.page] = from_f32<T>(x.y);
+            v[(size_t)(4 * u + 2) * a.page] = from_f32<T>(x.z);
+            v[(size_t)(4 * u + 3) * a.page] = from_f32<T>(x.w);
+            continue;
+        }
         const int head = w / quads, i = 4 * (w % quads);
-        const float4 x1 = *(const float4 *)(src + head * a.hd + i);
-        const float4 x2 = *(const float4 *)(src + head * a.hd + i + half);
+        const float4 x1 = slab4(src + head * a.hd + i);
+        const float4 x2 = slab4(src + head * a.hd + i + half);
         const float4 c = *(const float4 *)(cs + i), sn4 = *(const float4 *)(sn + i);
         const float4 y1 = {x1.x * c.x - x2.x * sn4.x, x1.y * c.y - x2.y * sn4.y, x1.z * c.z - x2.z * sn4.z,
                            x1.w * c.w - x2.w * sn4.w};
@@ -182,18 +217,6 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
         }
         store4(dst + i, y1);
         store4(dst + i + half, y2);
-    }
-    if (ok) {
-        // values are stored dim-major inside a page: [kv head][dim][slot]
-        const float *vs = src + (size_t)(a.nq + a.nkv) * a.hd;
-        T *v = (T *)a.v_cache[p] + (size_t)page * a.nkv * a.hd * a.page + pos % a.page;
-        for (int w = threadIdx.x; w < a.nkv * a.hd / 4; w += 256) {
-            const float4 x = *(const float4 *)(vs + 4 * w);
-            v[(size_t)(4 * w + 0) * a.page] = from_f32<T>(x.x);
-            v[(size_t)(4 * w + 1) * a.page] = from_f32<T>(x.y);
-            v[(size_t)(4 * w + 2) * a.page] = from_f32<T>(x.z);
-            v[(size_t)(4 * w + 3) * a.page] = from_f32<T>(x.w);
-        }
     }
 }
 
@@ -501,8 +524,12 @@ hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t
 
 hipError_t launch_rope_append(int dtype, const RopeArgs &a, hipStream_t s) {
     if (a.T <= 0) return hipSuccess;
-    if (dtype == 1) hipLaunchKernelGGL(rope_append_kernel<bf16>, dim3(a.T), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(rope_append_kernel<float>, dim3(a.T), dim3(256), 0, s, a);
+    // enough blocks per token to spread its work items over the CUs (at least 4 x 256 blocks)
+    const int items = (a.nq + a.nkv) * (a.hd / 8) + a.nkv * a.hd / 4;
+    const int per_tok = std::max(1, std::min((items + 255) / 256, (1024 + a.T - 1) / std::max(a.T, 1)));
+    const dim3 grid(a.T, per_tok);
+    if (dtype == 1) hipLaunchKernelGGL(rope_append_kernel<bf16>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(rope_append_kernel<float>, grid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

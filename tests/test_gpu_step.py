@@ -173,6 +173,18 @@ def test_layer7b_mixed_step():
     print(pair.report, flush=True)
 
 
+def test_layer7b_decode_rows_alone():
+    """The 7B-layer step's 64 decode rows without its chunks: a 64-row batch, whose QKV
+    projection splits K into fp32 partials that the rotation/append kernel sums (and whose
+    other projections stream their weights once).  Logits and every cache write compared."""
+    wl = layer7b_mixed_workload()
+    pair = Pair(wl.cfg, wl.weights, wl.kv, acc_w=wl.acc_w)
+    pair.workspace(max_tokens=wl.batch.n_tokens, max_chunks=2, max_decode=64, max_ctx=4096)
+    Te = wl.batch.n_emb_tokens
+    pair.step(Batch([], wl.batch.rows, wl.batch.token_ids[Te:]))
+    print(pair.report, flush=True)
+
+
 def test_device_errors_are_flagged_not_faulted():
     """A chunk whose pooling state does not match its offset, and a block-table entry past the
     pool, raise device error bits; the step still completes and nothing outside is written."""
