@@ -35,11 +35,17 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_25405_amd", "csrc", f) for f in
 
 
 def kernel_source_hash() -> str:
+    """SHA-256 of the dominant kernel's sources with comments and whitespace removed: a change of
+    code invalidates the committed counter summary, a change of comments does not."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)   # block comments
+        text = re.sub(r"//[^\n]*", " ", text)                # line comments (no '//' in strings here)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

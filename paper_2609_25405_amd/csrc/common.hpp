@@ -99,8 +99,9 @@ struct GemmArgs {
     LoraGemm lora;   // adds the low-rank update before the epilogue (split 0 of a split-K launch)
 };
 hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
-// split-K factor (<= max_splits, dividing K into whole stages) for a bf16 residual-add
-// projection of this shape; launch_gemm ignores a requested split that does not divide K
+// split-K factor (<= max_splits; each split a run of whole 64-deep stages, the stages dealt as
+// evenly as the count allows) for a bf16 residual-add projection of this shape; launch_gemm
+// ignores a requested split count larger than K's number of stages
 int gemm_add_splits(int M, int N, int K, int max_splits);
 
 // LoRA shrink: u[row][j*r + k] = scale[j] * sum_i x[row][i] a_j[k][i] for the adapter j of the
