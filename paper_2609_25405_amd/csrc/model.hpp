@@ -22,6 +22,12 @@ struct orthrus_model : public orthrus::Model {
     std::vector<void *> retired;
     hipEvent_t ev[2] = {nullptr, nullptr};
     int next = 0;
+    // steps with two row groups (two models) run the generator group's launches on `aux`
+    // (default priority), forked from and joined to the step's stream around each attention
+    // launch; step_mu serialises the host side of such steps on this handle
+    hipStream_t aux = nullptr;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+    std::mutex step_mu;
     // kernel timing (orthrus_profile_begin / _end)
     bool profiling = false;
     struct Mark { int name; hipEvent_t a, b; };

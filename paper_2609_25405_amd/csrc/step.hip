@@ -235,6 +235,12 @@ void orthrus_model_destroy(orthrus_model *m) {
         if (m->stage[i]) (void)hipHostFree(m->stage[i]);
     }
     for (void *r : m->retired) (void)hipHostFree(r);
+    if (m->aux) {
+        (void)hipStreamSynchronize(m->aux);
+        (void)hipStreamDestroy(m->aux);
+    }
+    if (m->ev_fork) (void)hipEventDestroy(m->ev_fork);
+    if (m->ev_join) (void)hipEventDestroy(m->ev_join);
     delete m;
 }
 
@@ -297,16 +303,23 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 
     hipStream_t s = (hipStream_t)stream;
     Prof prof{const_cast<orthrus_model *>(emb), s};
-    auto timed = [&](const char *name, auto &&launch) -> int {
+    auto timed = [&](hipStream_t st, const char *name, auto &&launch) -> int {
+        prof.s = st;
         int r = prof.begin(name);
         if (r) return r;
         if (launch() != hipSuccess) return ORTHRUS_EHIP;
         return prof.end();
     };
-#define RUN(name, expr)                                          \
-    do {                                                         \
-        const int r_ = timed(name, [&]() { return (expr); });    \
-        if (r_) return r_;                                       \
+    // RUN: a launch on the step's stream; RUNG: a launch of row group g on the group's stream
+#define RUN(name, expr)                                             \
+    do {                                                            \
+        const int r_ = timed(s, name, [&]() { return (expr); });    \
+        if (r_) return r_;                                          \
+    } while (0)
+#define RUNG(g, name, expr)                                         \
+    do {                                                            \
+        const int r_ = timed((g).st, name, [&]() { return (expr); }); \
+        if (r_) return r_;                                          \
     } while (0)
     char *ws = (char *)workspace;
     int *err = (int *)(ws + L.err);
@@ -328,14 +341,47 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 
     // row groups: [0, Te) through the embedding model, [Te, T) (prompt chunks, then decode rows)
     // through the generator
-    struct Group { const orthrus_model *m; int r0, r1; };
+    struct Group { const orthrus_model *m; int r0, r1; hipStream_t st; };
     Group groups[2];
     int n_groups = 0;
-    if (one_model) groups[n_groups++] = {emb, 0, T};
+    if (one_model) groups[n_groups++] = {emb, 0, T, s};
     else {
-        if (Te > 0) groups[n_groups++] = {emb, 0, Te};
-        if (T > Te) groups[n_groups++] = {gen, Te, T};
+        if (Te > 0) groups[n_groups++] = {emb, 0, Te, s};
+        if (T > Te) groups[n_groups++] = {gen, Te, T, s};
     }
+    // Two row groups touch disjoint rows, weights and cache slots between one attention launch
+    // and the next, so the second group's launches run on the handle's auxiliary stream,
+    // concurrently with the first's: forked after the plan upload and after each attention
+    // launch, joined before each launch over all rows (measured on the two-model retrieval steps)
+    orthrus_model *mh = const_cast<orthrus_model *>(emb);
+    const bool concurrent = n_groups == 2;
+    std::unique_lock<std::mutex> step_lock(mh->step_mu, std::defer_lock);
+    if (concurrent) {
+        step_lock.lock();
+        if (!mh->aux) {
+            HIP_TRY(hipStreamCreateWithFlags(&mh->aux, hipStreamNonBlocking));
+            HIP_TRY(hipEventCreateWithFlags(&mh->ev_fork, hipEventDisableTiming));
+            HIP_TRY(hipEventCreateWithFlags(&mh->ev_join, hipEventDisableTiming));
+        }
+        groups[1].st = mh->aux;
+    }
+    auto fork = [&]() -> int {
+        if (!concurrent) return ORTHRUS_OK;
+        HIP_TRY(hipEventRecord(mh->ev_fork, s));
+        HIP_TRY(hipStreamWaitEvent(mh->aux, mh->ev_fork, 0));
+        return ORTHRUS_OK;
+    };
+    auto join = [&]() -> int {
+        if (!concurrent) return ORTHRUS_OK;
+        HIP_TRY(hipEventRecord(mh->ev_join, mh->aux));
+        HIP_TRY(hipStreamWaitEvent(s, mh->ev_join, 0));
+        return ORTHRUS_OK;
+    };
+#define SYNC_GROUPS(call)            \
+    do {                             \
+        const int r_ = (call);       \
+        if (r_) return r_;           \
+    } while (0)
 
     // split-K slabs of the last residual-add projection, not yet added to x
     float *slabs = dt == ORTHRUS_BF16 ? (float *)(ws + L.split_slabs) : nullptr;
@@ -362,7 +408,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
             n.hd = c.head_dim;
             n.rope_base = c.rope_base;
         }
-        return launch_rmsnorm(dt, gather, n, s);
+        return launch_rmsnorm(dt, gather, n, g.st);
     };
     // LoRA: the shrink of site `site` (0 qkv, 1 o, 2 gate/up, 3 down) for the embedding rows of
     // group g in layer l, launched now on the GEMM input X; returns the GEMM's update arguments
@@ -403,7 +449,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
             lg.b0[j] = site == 0 ? ll.qkv_b : site == 1 ? ll.o_b : site == 2 ? ll.gate_b : ll.down_b;
             lg.b1[j] = site == 2 ? ll.up_b : nullptr;
         }
-        return launch_lora_shrink(dt, sh, s);
+        return launch_lora_shrink(dt, sh, g.st);
     };
     auto gemm = [&](int epi, const Group &g, const char *A, int lda, const void *B0, const void *B1,
                     void *out, int ldo, size_t out_es, int N, int K, const LoraGemm &lg) -> hipError_t {
@@ -419,7 +465,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.ldo = ldo;
         ga.splits = 1;
         ga.lora = lg;
-        return launch_gemm(dt, epi, ga, s);
+        return launch_gemm(dt, epi, ga, g.st);
     };
     // residual-add projection into x; bf16: split K when the tile count is low and leave the
     // slabs for the next row-wise kernel.  `splits` is chosen once per projection for the largest
@@ -442,14 +488,15 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         ga.partial = slabs ? slabs + (size_t)g.r0 * d : nullptr;  // the group's rows of each slab
         ga.split_stride = slab_stride;
         ga.lora = lg;
-        return launch_gemm(dt, EPI_ADD_F32, ga, s);
+        return launch_gemm(dt, EPI_ADD_F32, ga, g.st);
     };
 
     // token gather fused with the first RMSNorm (the final norm when there are no layers)
+    SYNC_GROUPS(fork());
     for (int gi = 0; gi < n_groups; ++gi) {
         const Group &g = groups[gi];
         const float *gain = c.n_layers > 0 ? g.m->layers[0].attn_norm : g.m->w.final_norm;
-        RUN("gather_norm", norm(true, g, gain));
+        RUNG(g, "gather_norm", norm(true, g, gain));
     }
 
     AttnArgs aa{};
@@ -501,7 +548,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 
     for (int l = 0; l < c.n_layers; ++l) {
         if (l > 0) {
-            for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].attn_norm));
+            for (int gi = 0; gi < n_groups; ++gi)
+                RUNG(groups[gi], "rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].attn_norm));
             pending = 0;
         }
         ra.k_cache[0] = (char *)emb_kv->k_cache + l * e_stride;
@@ -530,11 +578,12 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
                 ga.splits = qkv_splits;
                 ga.partial = qkv + (size_t)g.r0 * qkvd;
                 ga.split_stride = (size_t)T * qkvd;
-                if (lora_on(0, g)) RUN("lora_shrink", lora(0, l, g, act, d, d, ga.lora));
-                RUN("gemm_qkv", launch_gemm(dt, EPI_ADD_F32, ga, s));
+                if (lora_on(0, g)) RUNG(g, "lora_shrink", lora(0, l, g, act, d, d, ga.lora));
+                RUNG(g, "gemm_qkv", launch_gemm(dt, EPI_ADD_F32, ga, g.st));
             }
             ra.nslab = qkv_splits;
             ra.slab_stride = (size_t)T * qkvd;
+            SYNC_GROUPS(join());
             RUN("rope_append", launch_rope_append(dt, ra, s));
         } else if (dt == ORTHRUS_BF16) {
             // QKV projection with rotation and cache append in its epilogue
@@ -567,51 +616,56 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
                 q.hd = c.head_dim;
                 q.page = c.page_size;
                 q.err = err;
-                if (lora_on(0, g)) RUN("lora_shrink", lora(0, l, g, act, d, d, ga.lora));
-                RUN("gemm_qkv_rope", launch_gemm(dt, EPI_QKV_ROPE, ga, s));
+                if (lora_on(0, g)) RUNG(g, "lora_shrink", lora(0, l, g, act, d, d, ga.lora));
+                RUNG(g, "gemm_qkv_rope", launch_gemm(dt, EPI_QKV_ROPE, ga, g.st));
             }
         } else {
             for (int gi = 0; gi < n_groups; ++gi) {
                 const orthrus_layer_weights &lw = groups[gi].m->layers[l];
                 LoraGemm lg{};
-                if (lora_on(0, groups[gi])) RUN("lora_shrink", lora(0, l, groups[gi], act, d, d, lg));
-                RUN("gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d, lg));
+                if (lora_on(0, groups[gi])) RUNG(groups[gi], "lora_shrink", lora(0, l, groups[gi], act, d, d, lg));
+                RUNG(groups[gi], "gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d, lg));
             }
+            SYNC_GROUPS(join());
             RUN("rope_append", launch_rope_append(dt, ra, s));
         }
         for (int i = 0; i < 2; ++i) {
             aa.k_cache[i] = ra.k_cache[i];
             aa.v_cache[i] = ra.v_cache[i];
         }
+        SYNC_GROUPS(join());
         RUN("attention", launch_attention(dt, aa, s));
         if (p.n_split_rows > 0 || p.n_split_prefill > 0)
             RUN("attn_combine", launch_attn_combine(dt, aa, p.n_split_rows > 0 ? p.D : 0, s));
+        SYNC_GROUPS(fork());
         int splits = add_splits(qd);
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             LoraGemm lg{};
-            if (lora_on(1, groups[gi])) RUN("lora_shrink", lora(1, l, groups[gi], ob, qd, qd, lg));
-            RUN("gemm_o", add_proj(groups[gi], ob, qd, lw.w_o, qd, splits, lg));
+            if (lora_on(1, groups[gi])) RUNG(groups[gi], "lora_shrink", lora(1, l, groups[gi], ob, qd, qd, lg));
+            RUNG(groups[gi], "gemm_o", add_proj(groups[gi], ob, qd, lw.w_o, qd, splits, lg));
         }
         pending = splits > 1 ? splits : 0;
-        for (int gi = 0; gi < n_groups; ++gi) RUN("rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].mlp_norm));
+        for (int gi = 0; gi < n_groups; ++gi)
+            RUNG(groups[gi], "rmsnorm", norm(false, groups[gi], groups[gi].m->layers[l].mlp_norm));
         pending = 0;
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             LoraGemm lg{};
-            if (lora_on(2, groups[gi])) RUN("lora_shrink", lora(2, l, groups[gi], act, d, d, lg));
-            RUN("gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d, lg));
+            if (lora_on(2, groups[gi])) RUNG(groups[gi], "lora_shrink", lora(2, l, groups[gi], act, d, d, lg));
+            RUNG(groups[gi], "gemm_gate_up", gemm(EPI_SWIGLU, groups[gi], act, d, lw.w_gate, lw.w_up, ub, F, es, F, d, lg));
         }
         splits = add_splits(F);
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
             LoraGemm lg{};
-            if (lora_on(3, groups[gi])) RUN("lora_shrink", lora(3, l, groups[gi], ub, F, F, lg));
-            RUN("gemm_down", add_proj(groups[gi], ub, F, lw.w_down, F, splits, lg));
+            if (lora_on(3, groups[gi])) RUNG(groups[gi], "lora_shrink", lora(3, l, groups[gi], ub, F, F, lg));
+            RUNG(groups[gi], "gemm_down", add_proj(groups[gi], ub, F, lw.w_down, F, splits, lg));
         }
         pending = splits > 1 ? splits : 0;  // added by the next layer's norm or the final norm
     }
 
+    SYNC_GROUPS(join());
     // final RMSNorm (scale of the embedding rows; LM-head input of the rows that get logits),
     // then the incremental pooler on the embedding slice and the LM head on the listed rows
     PoolArgs pa{};
@@ -665,6 +719,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     }
     return ORTHRUS_OK;
 #undef RUN
+#undef RUNG
+#undef SYNC_GROUPS
 }
 
 int orthrus_profile_begin(orthrus_model *m) {
