@@ -221,7 +221,11 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
  *            (weighted mean, last, CLS).
  *   workspace: device buffer of ws_bytes >= orthrus_workspace_bytes(...) for this batch.
  * Host-side validation (EINVAL, EDESC, EDUPSEQ, ECAPACITY) runs before anything is enqueued.
- * One step in flight per workspace.  Outputs are valid once the stream has synchronised. */
+ * One step in flight per workspace.  Outputs are valid once the stream has synchronised.  With
+ * two distinct models, the generator rows' launches run on a second stream owned by `emb`
+ * (default priority), forked from and joined back to `stream` inside the enqueued work, so
+ * ordering against `stream` is as for a single-stream step; calls sharing `emb` that use it
+ * this way are serialised on the host. */
 int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
                  float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream);
