@@ -551,6 +551,8 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
         if (split && a.M <= 896) return run_bf16<128, 128, 2, 2, EPI>(a, s);
         if (EPI == EPI_ADD_F32 && a.partial && a.M > 896) return run_bf16<256, 256, 2, 4, EPI>(a, s);
         if (EPI == EPI_ADD_F32) return run_bf16<128, 128, 4, 2, EPI>(a, s);
+        // fp32 rows of a large QKV projection (rotated by a row kernel): one round of big tiles
+        if (a.M > 1280) return a.M <= 1728 ? run_bf16<192, 256, 2, 4, EPI>(a, s) : run_bf16<256, 256, 2, 4, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     }
 }

@@ -36,6 +36,11 @@ constexpr int kMaxSplits = 4;
 // rows the fused projection is faster (54.5 us against 46.2 + 15.4 us with 4 splits)
 constexpr int kQkvSplitRows = 64;
 constexpr int kQkvSplits = 2;
+// QKV projections of more than kQkvFusedMaxRows rows per model (bf16 path) store fp32 rows
+// from one round of 192x256 or 256x256 tiles and rotate them in the row kernel: whole-head
+// 128x128 tiles with the fused epilogue need more than one round there (7B shape: 1568 rows
+// 138 us fused against 86 + ~12 us; 2048 rows 173 us against 104 + ~15 us)
+constexpr int kQkvFusedMaxRows = 1280;
 size_t qkv_slab_rows(size_t T) { return (size_t)kQkvSplits * std::min<size_t>(T, 2 * kQkvSplitRows); }
 
 Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials) {
@@ -49,7 +54,7 @@ Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials
     L.act = o; o += up(T * d * es);
     // fp32 QKV rows for the separate rotation kernel: every row on the fp32 path; on the bf16
     // path (which rotates in the GEMM epilogue) the split-K partials of small projections
-    L.qkv = o; o += up((m.cfg.dtype == ORTHRUS_BF16 ? qkv_slab_rows(T) : T) * (size_t)m.qkv_dim() * 4);
+    L.qkv = o; o += up((m.cfg.dtype == ORTHRUS_BF16 ? std::max(T, qkv_slab_rows(T)) : T) * (size_t)m.qkv_dim() * 4);
     L.q = o; o += up(T * (size_t)m.q_dim() * es);
     L.o = o; o += up(T * (size_t)m.q_dim() * es);
     L.u = o; o += up(T * (size_t)m.cfg.d_ff * es);
@@ -585,7 +590,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
             ra.slab_stride = (size_t)T * qkvd;
             SYNC_GROUPS(join());
             RUN("rope_append", launch_rope_append(dt, ra, s));
-        } else if (dt == ORTHRUS_BF16) {
+        } else if (dt == ORTHRUS_BF16 && max_rows <= kQkvFusedMaxRows) {
             // QKV projection with rotation and cache append in its epilogue
             for (int gi = 0; gi < n_groups; ++gi) {
                 const Group &g = groups[gi];
@@ -626,6 +631,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
                 if (lora_on(0, groups[gi])) RUNG(groups[gi], "lora_shrink", lora(0, l, groups[gi], act, d, d, lg));
                 RUNG(groups[gi], "gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d, lg));
             }
+            ra.nslab = 1;
             SYNC_GROUPS(join());
             RUN("rope_append", launch_rope_append(dt, ra, s));
         }
