@@ -130,7 +130,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="BLAS threads for the oracle (0 = all)")
     ap.add_argument("--workload", default="7b-layer-mixed",
-                    choices=["7b-layer-mixed", "retrieval-sweep-32l", "long-docs-32l", "decode-heavy-32l"],
+                    choices=["7b-layer-mixed", "retrieval-sweep-32l", "long-docs-32l", "decode-heavy-32l",
+                             "serving-32l"],
                     help="7b-layer-mixed (default): the headline one-layer step with roofline and CPU "
                          "baseline.  The others run the full 32-layer configurations on device-drawn "
                          "weights and caches: two models over an embedding-fraction sweep, 16 documents "
@@ -404,6 +405,8 @@ def full_model_bench(args) -> dict:
                     embed_tokens_per_s=sum(b.n_emb_tokens for b in steps) / (sum(times) * 1e-3),
                     decode_tokens_per_s=sum(len(b.rows) for b in steps) / (sum(times) * 1e-3),
                     sweep=sweep)
+    if args.workload == "serving-32l":
+        return serving_bench(args, model, log, L)
     # long documents
     _, _, paged, steps = long_document_scenario(n_layers=1, n_docs=16, doc_len=8192, chunk=512, per_step=3,
                                                 n_dec=32, ctx0=2048)
@@ -422,6 +425,94 @@ def full_model_bench(args) -> dict:
                                     "from context 2048", "layers": L, "steps": len(steps)},
                 embed_tokens_per_s=Te / tsum, decode_tokens_per_s=D / tsum,
                 ms_per_step_first_last=[times[0], times[-1]])
+
+
+def serving_bench(args, model, log, L: int) -> dict:
+    """The serving loop on the GPU: the native intra-batch scheduler and the runner (schedule,
+    step, sample, commit; one host synchronisation per iteration) serve a closed set of
+    requests to completion on a 32-layer 7B-shape model.  Value: every token the model processed
+    (embedding inputs, prompts, generated tokens) per second of wall time."""
+    import numpy as np
+    import torch
+
+    from paper_2609_25405_amd import runtime as R
+    from workload import llm7b_config
+
+    cfg = llm7b_config(n_layers=L)
+    dm = model(cfg, 1005, 0)
+    rng = np.random.default_rng(1005)
+    n_emb, n_gen, prompt, new = 384, 96, 512, 128
+    sigma = 0.6
+    emb_len = np.clip(np.round(rng.lognormal(np.log(512) - sigma * sigma / 2, sigma, n_emb)), 16, 4096).astype(int)
+    budget, chunk, n_seq, page = 2048, 512, 512, cfg.page_size
+    max_blocks = (max(int(emb_len.max()), prompt + new) + page - 1) // page + 1
+    n_pages = 16384                                   # 2 MiB per page over 32 layers: 32 GiB
+    kv = R.DeviceKV(cfg, n_pages, n_seq, max_blocks, fill=0.0)
+    # untimed warm-up: one embedding and one short generation through a scheduler of their own
+    w_sched = R.Scheduler(budget, chunk, [(n_seq, n_pages, max_blocks)])
+    w_run = R.Runner(dm, dm, kv, kv, w_sched)
+    w_sched.submit_embedding(0, 600, rng.integers(0, cfg.vocab, 600).tolist(), "mean")
+    w_sched.submit_generation(1, 600, 4, rng.integers(0, cfg.vocab, 600).tolist())
+    for _ in range(16):
+        w_run.iterate()
+        c = w_sched.counts()
+        if c["queued_emb"] == 0 and c["queued_gen"] == 0 and c["running"] == 0:
+            break
+    w_run.close()
+    w_sched.close()
+    del w_run, w_sched
+    sched = R.Scheduler(budget, chunk, [(n_seq, n_pages, max_blocks)])
+    run = R.Runner(dm, dm, kv, kv, sched)
+    rid = 0
+    for i in range(max(n_emb, n_gen)):                # interleaved arrivals, all at time 0
+        if i < n_gen:
+            sched.submit_generation(rid, prompt, new, rng.integers(0, cfg.vocab, prompt).tolist())
+            rid += 1
+        if i < n_emb:
+            n = int(emb_len[i])
+            sched.submit_embedding(rid, n, rng.integers(0, cfg.vocab, n).tolist(), "mean")
+            rid += 1
+    log(f"serving: {n_emb} embedding requests ({int(emb_len.sum())} tokens), {n_gen} generations "
+        f"({prompt}-token prompts, {new} new tokens)")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    it, used, gen_tokens, n_embs, fills, iter_s = 0, 0, 0, 0, [], []
+    while True:
+        t1 = time.perf_counter()
+        out = run.iterate()                           # synchronises the stream
+        iter_s.append(time.perf_counter() - t1)
+        it += 1
+        used += out["used"]
+        fills.append(out["used"] / budget)
+        gen_tokens += len(out["tokens"])
+        n_embs += len(out["embeddings"])
+        c = sched.counts()
+        if c["queued_emb"] == 0 and c["queued_gen"] == 0 and c["running"] == 0:
+            break
+        if it >= 2000:
+            raise SystemExit("serving run did not drain in 2000 iterations")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert n_embs == n_emb, (n_embs, n_emb)
+    emb_tokens, prompt_tokens = int(emb_len.sum()), n_gen * prompt
+    processed = emb_tokens + prompt_tokens + n_gen * (new - 1)   # the last sampled token is never fed back
+    return {"metric": METRIC, "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded N(0,0.02) weights drawn on the device, uniform token ids)",
+            "value": processed / wall, "steps": it, "warmup": 1, "ms_per_step": wall / it * 1e3,
+            "config": {"workload": "serving-32l: 32 layers 7B shape bf16 vocab 32000; native scheduler (budget "
+                                   "2048, chunk 512) and runner serve 384 embedding requests (lognormal lengths, "
+                                   "mean 512, mean pooling) and 96 generations (512-token prompts, 128 new tokens, "
+                                   "greedy) to completion, one synchronisation per iteration",
+                       "layers": L},
+            "embed_tokens_per_s": emb_tokens / wall, "prompt_tokens_per_s": prompt_tokens / wall,
+            "generated_tokens_per_s": n_gen * new / wall, "iterations": it,
+            "mean_budget_fill": float(np.mean(fills)), "budget_tokens_used": used,
+            "full_budget_iterations": int(sum(f >= 1.0 for f in fills)),
+            "full_budget_ms_mean": float(np.mean([t for t, f in zip(iter_s, fills) if f >= 1.0] or [0])) * 1e3,
+            "decode_only_iterations": int(sum(f * budget <= n_gen for f in fills)),
+            "decode_only_ms_mean": float(np.mean([t for t, f in zip(iter_s, fills) if f * budget <= n_gen]
+                                                 or [0])) * 1e3}
 
 
 def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):

@@ -30,47 +30,71 @@ __device__ __forceinline__ void store4(bf16 *p, float4 v) {
     *(uint2 *)p = uint2{pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
 }
 
-// Rows of up to kRegV * 256 float4 (d <= 8192) are held in registers between the sum of squares
-// and the scaled write: every load of the row is issued before the first one is used (one memory
-// latency per row instead of one per 256-float4 piece) and nothing is read twice.
-constexpr int kRegV = 8;
+// Rows of up to RV * 256 float4 (RV = 4 for d <= 4096, 8 for d <= 8192) are held in registers
+// between the sum of squares and the scaled write; longer rows take a strided loop.
+constexpr int kMaxPend = 4;  // split-K slabs a row kernel adds (the step splits K at most 4 ways)
+
+// x row plus its pending split-K slabs into registers, x + slab 0 + slab 1 + ... in that order:
+// every load is issued before the first add, so the row costs one memory latency whatever the
+// number of slabs (a loop that adds each slab as it arrives waits once per slab)
+template <int RV>
+__device__ __forceinline__ void load_row_pend(float4 (&xv)[RV], const float *xrow, const float *pend,
+                                              size_t pend_stride, int npend, int nv) {
+    float4 p[kMaxPend][RV];
+#pragma unroll
+    for (int i = 0; i < RV; ++i) {
+        const int v = threadIdx.x + i * 256;
+        if (v < nv) xv[i] = load4(xrow + 4 * v);
+    }
+#pragma unroll
+    for (int sp = 0; sp < kMaxPend; ++sp) {
+        if (sp < npend) {
+#pragma unroll
+            for (int i = 0; i < RV; ++i) {
+                const int v = threadIdx.x + i * 256;
+                if (v < nv) p[sp][i] = load4(pend + sp * pend_stride + 4 * v);
+            }
+        }
+    }
+#pragma unroll
+    for (int sp = 0; sp < kMaxPend; ++sp) {
+        if (sp < npend) {
+#pragma unroll
+            for (int i = 0; i < RV; ++i) {
+                const int v = threadIdx.x + i * 256;
+                if (v < nv) xv[i] = float4{xv[i].x + p[sp][i].x, xv[i].y + p[sp][i].y, xv[i].z + p[sp][i].z,
+                                           xv[i].w + p[sp][i].w};
+            }
+        }
+    }
+}
 
 // y = x / sqrt(mean(x^2) + eps) * gain over one row per block (d a multiple of 4); gather mode
 // first sets x = table[tok] (the fp32 copy is kept as the residual stream)
-template <typename T, bool GATHER>
+template <typename T, bool GATHER, int RV>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
     __shared__ float red[4];
     const int r = blockIdx.x;
     const int nv = a.d / 4;
     float *xrow = (GATHER ? a.x_out : const_cast<float *>(a.x)) + (size_t)r * a.d;
     float ss = 0.f;
-    if (nv <= kRegV * 256) {
-        float4 xv[kRegV];
+    if (nv <= RV * 256) {
+        float4 xv[RV], gv[RV];
+        // the gain first: its loads complete under the row's
+#pragma unroll
+        for (int i = 0; i < RV; ++i) {
+            const int v = threadIdx.x + i * 256;
+            if (v < nv) gv[i] = load4(a.gain + 4 * v);
+        }
         if (GATHER) {
             const T *src = (const T *)a.table + (size_t)a.tok[r] * a.d;
 #pragma unroll
-            for (int i = 0; i < kRegV; ++i) {
+            for (int i = 0; i < RV; ++i) {
                 const int v = threadIdx.x + i * 256;
                 if (v < nv) xv[i] = load4(src + 4 * v);
             }
         } else {
-#pragma unroll
-            for (int i = 0; i < kRegV; ++i) {
-                const int v = threadIdx.x + i * 256;
-                if (v < nv) xv[i] = load4(xrow + 4 * v);
-            }
-            // finish a split-K residual add: x += slab 0 + slab 1 + ... in order
-            for (int sp = 0; sp < a.npend; ++sp) {
-                const float *slab = a.pend + sp * a.pend_stride + (size_t)r * a.d;
-#pragma unroll
-                for (int i = 0; i < kRegV; ++i) {
-                    const int v = threadIdx.x + i * 256;
-                    if (v < nv) {
-                        const float4 p = load4(slab + 4 * v);
-                        xv[i] = float4{xv[i].x + p.x, xv[i].y + p.y, xv[i].z + p.z, xv[i].w + p.w};
-                    }
-                }
-            }
+            load_row_pend<RV>(xv, xrow, a.pend + (size_t)r * a.d, a.pend_stride, a.npend, nv);
         }
         if (GATHER && a.cs && threadIdx.x < a.hd / 2) {
             // rotation table of this token for the QKV epilogue (angle evaluated in double)
@@ -80,7 +104,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
             a.cs[(size_t)r * (a.hd / 2) + threadIdx.x] = float2{(float)cv, (float)sv};
         }
 #pragma unroll
-        for (int i = 0; i < kRegV; ++i) {
+        for (int i = 0; i < RV; ++i) {
             const int v = threadIdx.x + i * 256;
             if (v < nv) {
                 if (GATHER || a.npend > 0) store4(xrow + 4 * v, xv[i]);
@@ -90,10 +114,10 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
         const float inv = rsqrtf(block_sum(ss, red) / (float)a.d + a.eps);
         T *y = (T *)a.y + (size_t)r * a.d;
 #pragma unroll
-        for (int i = 0; i < kRegV; ++i) {
+        for (int i = 0; i < RV; ++i) {
             const int v = threadIdx.x + i * 256;
             if (v < nv) {
-                const float4 g = load4(a.gain + 4 * v);
+                const float4 g = gv[i];
                 store4(y + 4 * v, float4{xv[i].x * inv * g.x, xv[i].y * inv * g.y, xv[i].z * inv * g.z,
                                          xv[i].w * inv * g.w});
             }
@@ -225,7 +249,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
 // only the scale 1/rms (the pooler applies it); the following blocks take the rows listed in
 // lm_rows and write them, normalised with the generator's gain, as consecutive rows of the LM
 // head's input.
-template <typename T>
+template <typename T, int RV>
 __device__ void final_row_block(const PoolArgs &a, int b, float *red) {
     const bool emb_row = b < a.n_emb_rows;
     const int lm = b - a.n_emb_rows;
@@ -233,27 +257,19 @@ __device__ void final_row_block(const PoolArgs &a, int b, float *red) {
     const int nv = a.d / 4;
     float *x = const_cast<float *>(a.x) + (size_t)r * a.d;
     float ss = 0.f;
-    if (nv <= kRegV * 256) {
-        // the row in registers (see kRegV)
-        float4 xv[kRegV];
+    if (nv <= RV * 256) {
+        float4 xv[RV], gv[RV];
+        // an LM row's gain first: its loads complete under the row's
+        if (!emb_row) {
 #pragma unroll
-        for (int i = 0; i < kRegV; ++i) {
-            const int v = threadIdx.x + i * 256;
-            if (v < nv) xv[i] = load4(x + 4 * v);
-        }
-        for (int sp = 0; sp < a.npend; ++sp) {
-            const float *slab = a.pend + sp * a.pend_stride + (size_t)r * a.d;
-#pragma unroll
-            for (int i = 0; i < kRegV; ++i) {
+            for (int i = 0; i < RV; ++i) {
                 const int v = threadIdx.x + i * 256;
-                if (v < nv) {
-                    const float4 p = load4(slab + 4 * v);
-                    xv[i] = float4{xv[i].x + p.x, xv[i].y + p.y, xv[i].z + p.z, xv[i].w + p.w};
-                }
+                if (v < nv) gv[i] = load4(a.gen_gain + 4 * v);
             }
         }
+        load_row_pend<RV>(xv, x, a.pend + (size_t)r * a.d, a.pend_stride, a.npend, nv);
 #pragma unroll
-        for (int i = 0; i < kRegV; ++i) {
+        for (int i = 0; i < RV; ++i) {
             const int v = threadIdx.x + i * 256;
             if (v < nv) {
                 if (a.npend > 0) store4(x + 4 * v, xv[i]);
@@ -264,12 +280,18 @@ __device__ void final_row_block(const PoolArgs &a, int b, float *red) {
         if (emb_row && threadIdx.x == 0) a.inv_rms[r] = inv;
         const int hr = emb_row && a.hid_rows ? a.hid_rows[r] : -1;
         if (emb_row && hr < 0) return;
-        const float *gain = emb_row ? a.gain : a.gen_gain;
+        if (emb_row) {
 #pragma unroll
-        for (int i = 0; i < kRegV; ++i) {
+            for (int i = 0; i < RV; ++i) {
+                const int v = threadIdx.x + i * 256;
+                if (v < nv) gv[i] = load4(a.gain + 4 * v);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RV; ++i) {
             const int v = threadIdx.x + i * 256;
             if (v < nv) {
-                const float4 g = load4(gain + 4 * v);
+                const float4 g = gv[i];
                 const float4 o{xv[i].x * inv * g.x, xv[i].y * inv * g.y, xv[i].z * inv * g.z, xv[i].w * inv * g.w};
                 if (emb_row) store4(a.hidden + (size_t)hr * a.d + 4 * v, o);
                 else store4((T *)a.act + (size_t)lm * a.d + 4 * v, o);
@@ -309,10 +331,10 @@ __device__ void final_row_block(const PoolArgs &a, int b, float *red) {
     }
 }
 
-template <typename T>
+template <typename T, int RV>
 __global__ __launch_bounds__(256) void final_rows_kernel(PoolArgs a) {
     __shared__ float red[4];
-    final_row_block<T>(a, blockIdx.x, red);
+    final_row_block<T, RV>(a, blockIdx.x, red);
 }
 
 __device__ __forceinline__ bool chunk_state_ok(const int32_t *ch, const float *acc_w) {
@@ -450,10 +472,10 @@ __global__ __launch_bounds__(256) void pool_rows_kernel(PoolArgs a) {
 // With no head that needs every embedding row's norm, the final norm of the rows that get
 // logits and the single-row pooler are independent: one launch, blocks [0, n_lm) normalise the
 // LM rows, the following n_chunks blocks pool one chunk each.
-template <typename T>
+template <typename T, int RV>
 __global__ __launch_bounds__(256) void final_and_pool_rows_kernel(PoolArgs a) {
     __shared__ float red[4];
-    if ((int)blockIdx.x < a.n_lm) final_row_block<T>(a, blockIdx.x, red);
+    if ((int)blockIdx.x < a.n_lm) final_row_block<T, RV>(a, blockIdx.x, red);
     else pool_rows_block(a, (int)blockIdx.x - a.n_lm, red);
 }
 
@@ -512,12 +534,15 @@ hipError_t launch_argmax(const float *logits, int rows, int vocab, int32_t *out,
 
 hipError_t launch_rmsnorm(int dtype, bool gather, const NormArgs &a, hipStream_t s) {
     if (a.rows <= 0) return hipSuccess;
+    if (a.npend < 0 || a.npend > kMaxPend) return hipErrorInvalidValue;
+    const bool rv4 = a.d <= 4096;
+    auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(a.rows), dim3(256), 0, s, a); };
     if (dtype == 1) {
-        if (gather) hipLaunchKernelGGL((rmsnorm_kernel<bf16, true>), dim3(a.rows), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((rmsnorm_kernel<bf16, false>), dim3(a.rows), dim3(256), 0, s, a);
+        if (gather) rv4 ? go(rmsnorm_kernel<bf16, true, 4>) : go(rmsnorm_kernel<bf16, true, 8>);
+        else rv4 ? go(rmsnorm_kernel<bf16, false, 4>) : go(rmsnorm_kernel<bf16, false, 8>);
     } else {
-        if (gather) hipLaunchKernelGGL((rmsnorm_kernel<float, true>), dim3(a.rows), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((rmsnorm_kernel<float, false>), dim3(a.rows), dim3(256), 0, s, a);
+        if (gather) rv4 ? go(rmsnorm_kernel<float, true, 4>) : go(rmsnorm_kernel<float, true, 8>);
+        else rv4 ? go(rmsnorm_kernel<float, false, 4>) : go(rmsnorm_kernel<float, false, 8>);
     }
     return hipGetLastError();
 }
@@ -536,17 +561,23 @@ hipError_t launch_rope_append(int dtype, const RopeArgs &a, hipStream_t s) {
 hipError_t launch_final_rows(int dtype, const PoolArgs &a, hipStream_t s) {
     const int rows = a.n_emb_rows + a.n_lm;
     if (rows <= 0) return hipSuccess;
-    if (dtype == 1) hipLaunchKernelGGL(final_rows_kernel<bf16>, dim3(rows), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(final_rows_kernel<float>, dim3(rows), dim3(256), 0, s, a);
+    if (a.npend < 0 || a.npend > kMaxPend) return hipErrorInvalidValue;
+    const bool rv4 = a.d <= 4096;
+    auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(rows), dim3(256), 0, s, a); };
+    if (dtype == 1) rv4 ? go(final_rows_kernel<bf16, 4>) : go(final_rows_kernel<bf16, 8>);
+    else rv4 ? go(final_rows_kernel<float, 4>) : go(final_rows_kernel<float, 8>);
     return hipGetLastError();
 }
 
 hipError_t launch_final_and_pool(int dtype, const PoolArgs &a, hipStream_t s) {
     if (a.n_emb_rows != 0) return hipErrorInvalidValue;
+    if (a.npend < 0 || a.npend > kMaxPend) return hipErrorInvalidValue;
     const int blocks = a.n_lm + a.n_chunks;
     if (blocks <= 0) return hipSuccess;
-    if (dtype == 1) hipLaunchKernelGGL(final_and_pool_rows_kernel<bf16>, dim3(blocks), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(final_and_pool_rows_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
+    const bool rv4 = a.d <= 4096;
+    auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, s, a); };
+    if (dtype == 1) rv4 ? go(final_and_pool_rows_kernel<bf16, 4>) : go(final_and_pool_rows_kernel<bf16, 8>);
+    else rv4 ? go(final_and_pool_rows_kernel<float, 4>) : go(final_and_pool_rows_kernel<float, 8>);
     return hipGetLastError();
 }
 
