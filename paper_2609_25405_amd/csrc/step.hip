@@ -32,9 +32,10 @@ constexpr int kMaxSplits = 4;
 // QKV projections of at most kQkvSplitRows rows per model split K in two (bf16 path): their fp32
 // partial sums [2][T][qkv_dim] get a region of qkv_slab_rows(T) rows (two such groups).
 // Measured on the 7B shape at 64 rows: the split projection and the rotation kernel take
-// 18.6 + 6.9 us against 42.6 us fused (48 whole-head tiles); 8 splits 22.1 + 10.3 us; at 384
-// rows the fused projection is faster (54.5 us against 46.2 + 15.4 us with 4 splits)
-constexpr int kQkvSplitRows = 64;
+// 18.6 + 6.9 us against 42.6 us fused (48 whole-head tiles); 8 splits 22.1 + 10.3 us; at 96
+// rows 23.9 + 8.2 us against 44.0 us, at 128 rows 25.8 + 8.4 against 45.1 us; at 384 rows the
+// fused projection is faster (54.5 us against 46.2 + 15.4 us with 4 splits)
+constexpr int kQkvSplitRows = 128;
 constexpr int kQkvSplits = 2;
 // QKV projections of more than kQkvFusedMaxRows rows per model (bf16 path) store fp32 rows
 // from one round of 192x256 or 256x256 tiles and rotate them in the row kernel: whole-head

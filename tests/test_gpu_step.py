@@ -185,6 +185,31 @@ def test_layer7b_decode_rows_alone():
     print(pair.report, flush=True)
 
 
+@pytest.mark.parametrize("n_dec", [96, 128])
+def test_layer7b_decode_batches_up_to_128_rows(n_dec):
+    """Decode-only 7B-layer batches of 65..128 rows: the QKV projection splits K in two into
+    fp32 partials the rotation/append kernel sums, gate/up and the LM head stream their weights
+    through one 128-row tile, O and down split K four ways on 128x64 tiles.  Contexts U[256,
+    1024]; logits and every cache write compared."""
+    cfg = ModelConfig(n_layers=1, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128, d_ff=14336,
+                      vocab=32000, dtype="bf16")
+    seed = 1006
+    W = make_weights(cfg, seed)
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(n_dec,)))
+    ctx = rng.integers(256, 1024, size=n_dec, endpoint=True)
+    P = cfg.page_size
+    max_blocks = 1024 // P + 1
+    pk = PagedKV(cfg, sum(-(-(int(c) + 1) // P) for c in ctx) + 8, n_dec, max_blocks, seed)
+    rows = [DecodeRow(seq=i, ctx_len=int(c)) for i, c in enumerate(ctx)]
+    for r in rows:
+        pk.fill_random(r.seq, r.ctx_len, seed)
+        pk.reserve(r.seq, r.ctx_len + 1)
+    pair = Pair(cfg, W, pk)
+    pair.workspace(max_tokens=n_dec, max_chunks=1, max_decode=n_dec, max_ctx=max_blocks * P)
+    pair.step(Batch([], rows, draw_tokens(seed, 1, n_dec, cfg.vocab)))
+    print(pair.report, flush=True)
+
+
 def test_device_errors_are_flagged_not_faulted():
     """A chunk whose pooling state does not match its offset, and a block-table entry past the
     pool, raise device error bits; the step still completes and nothing outside is written."""
