@@ -535,7 +535,15 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //    gate/up up to M = 896 the 128- or 192-row tile that pads M least (M = 512: 162 -> 129 us);
 //  - 64 < M <= 128 (decode batches of up to 128 rows): one row tile of 128 rows and a 4-deep
 //    ring (128 KiB of LDS), weights streamed: gate/up 66.5 -> 47.3 us, LM head 74.6 -> 66.5 us,
-//    down split 4 ways on 128x64 tiles 38.8 -> 32.7 us (M = 96, cold weights).
+//    down split 4 ways on 128x64 tiles 38.8 -> 32.7 us (M = 96, cold weights);
+//  - split-K residual-add projections of 128 < M <= 256: 128x128 tiles with 4-deep rings (one
+//    workgroup per CU; down at M = 192 57.1 -> 45.7 us, o at M = 256 27.1 -> 21.8 us); above 256
+//    rows two 64 KiB workgroups per CU win again (down at M = 384: 71 against 86 us);
+//  - gate/up of 128 < M <= 896, measured on the 7B shape with cold weights: 128x128 up to
+//    M = 256 (192x256 tiles would leave most CUs idle: M = 192 75 against 97 us); above, 192x256
+//    when 128x128 tiles need more than the 512 slots of one round and 192x256 tiles fit in
+//    one (M = 640: 172 against 195 us), else the tile that pads M least (M = 384 98 against
+//    130 us, M = 512 147 against 174 us, M = 896 240 against 256 us).
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
     if constexpr (EPI == EPI_QKV_ROPE) {
@@ -545,15 +553,17 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
     } else if constexpr (EPI == EPI_SWIGLU) {
         if (a.M <= 64) return run_bf16<64, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
         if (a.M <= 128) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
+        if (a.M <= 256) return run_bf16<128, 128, 2, 2, EPI>(a, s);
         const int pad128 = (a.M + 127) / 128 * 128 - a.M, pad192 = (a.M + 191) / 192 * 192 - a.M;
-        if (a.M > 896 || (a.M > 128 && pad192 <= pad128)) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        const int w128 = (a.M + 127) / 128 * ((a.N + 127) / 128), w192 = (a.M + 191) / 192 * ((a.N + 255) / 256);
+        if (a.M > 896 || (w128 > 512 && w192 <= 256) || pad192 <= pad128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else {
         if (a.M <= 64) return run_bf16<64, 64, 2, 2, EPI, 64, 4, 4, true>(a, s);
         const bool split = EPI == EPI_ADD_F32 && a.partial && a.splits > 1;
         if (split && a.M <= 128) return run_bf16<128, 64, 2, 2, EPI, 64, 4, 4, true>(a, s);
         if (EPI != EPI_ADD_F32 && a.M <= 128) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
-        if (split && a.M <= 192) return run_bf16<64, 64, 2, 2, EPI, 64, 4>(a, s);
+        if (split && a.M <= 256) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, false>(a, s);
         if (split && a.M <= 896) return run_bf16<128, 128, 2, 2, EPI>(a, s);
         if (EPI == EPI_ADD_F32 && a.partial && a.M > 896) return run_bf16<256, 256, 2, 4, EPI>(a, s);
         if (EPI == EPI_ADD_F32) return run_bf16<128, 128, 4, 2, EPI>(a, s);

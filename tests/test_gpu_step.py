@@ -185,12 +185,13 @@ def test_layer7b_decode_rows_alone():
     print(pair.report, flush=True)
 
 
-@pytest.mark.parametrize("n_dec", [96, 128])
-def test_layer7b_decode_batches_up_to_128_rows(n_dec):
-    """Decode-only 7B-layer batches of 65..128 rows: the QKV projection splits K in two into
-    fp32 partials the rotation/append kernel sums, gate/up and the LM head stream their weights
-    through one 128-row tile, O and down split K four ways on 128x64 tiles.  Contexts U[256,
-    1024]; logits and every cache write compared."""
+@pytest.mark.parametrize("n_dec", [96, 128, 192])
+def test_layer7b_decode_batches_up_to_192_rows(n_dec):
+    """Decode-only 7B-layer batches of 65..192 rows.  Up to 128 rows the QKV projection splits
+    K in two into fp32 partials the rotation/append kernel sums, gate/up and the LM head stream
+    their weights through one 128-row tile, O and down split K four ways on 128x64 tiles; at 192
+    rows QKV takes the fused rotation epilogue and O and down 4-deep 128x128 tiles.  Contexts
+    U[256, 1024]; logits and every cache write compared."""
     cfg = ModelConfig(n_layers=1, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128, d_ff=14336,
                       vocab=32000, dtype="bf16")
     seed = 1006
