@@ -321,10 +321,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
                     *(u32x4 *)(dst + half + g * 8) = w2;
                 }
             } else {
-                // v: items (dim, group of 8 rows); a dim of one page holds `page` slots contiguously
+                // v: items (dim, group of 8 rows); a dim of one page holds `page` slots contiguously.
+                // Adjacent lanes take the two 8-row halves of one dim's 16 rows, so a page-aligned
+                // run of 16 rows leaves as whole 32-byte runs of consecutive dims (7B-layer mixed
+                // step: 80.3 -> 78.8 us against lanes along the dims)
+                static_assert(BM % 16 == 0, "16-row groups");
                 const int kvh = head - q.nq - q.nkv;
                 for (int it = tid; it < hd * (BM / 8); it += 64 * NW) {
-                    const int d = it % hd, r0 = (it / hd) * 8;
+                    const int d = (it >> 1) % hd, r0 = ((it >> 1) / hd) * 16 + (it & 1) * 8;
                     const int4 m0d = meta[r0];
                     bool run = m0d.x >= 0 && m0d.z >= 0 && (m0d.y & 7) == 0;
 #pragma unroll
