@@ -431,7 +431,9 @@ def serving_bench(args, model, log, L: int) -> dict:
     """The serving loop on the GPU: the native intra-batch scheduler and the runner (schedule,
     step, sample, commit; one host synchronisation per iteration) serve a closed set of
     requests to completion on a 32-layer 7B-shape model.  Value: every token the model processed
-    (embedding inputs, prompts, generated tokens) per second of wall time."""
+    (embedding inputs, prompts, generated tokens) per second of wall time.  The run length is
+    the request set's (244 iterations), so --steps and --warmup do not apply: one short
+    embedding and one short generation go through a scheduler of their own first, untimed."""
     import numpy as np
     import torch
 
