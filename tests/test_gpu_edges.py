@@ -1,6 +1,8 @@
 """GPU parity at the edges of the batch descriptor, against the float64 oracle: one-token chunks
 on page boundaries, decode rows at context 0 and on page edges, batches of one item kind, an
-empty batch, and a model without layers (token gather, final norm, pooling and LM head only).
+empty batch, a model without layers (token gather, final norm, pooling and LM head only), and a
+bf16 batch of more than 1280 rows (the rotation/append kernel of large batches, with and
+without a bad page).
 """
 import numpy as np
 import pytest
@@ -83,3 +85,61 @@ def test_model_without_layers(dtype):
     rows = [DecodeRow(2, 5), DecodeRow(3, 0)]
     pair.step(Batch(chunks, rows, draw_tokens(51, 1, 20 + 9 + 2, cfg.vocab)))
     print(pair.report, flush=True)
+
+
+def _over_1280_rows(seed=61):
+    """Tiny bf16 model, one batch of 1302 rows: chunks at offsets and of lengths that are not
+    multiples of 8 (a resumed one among them) and two decode rows."""
+    cfg = tiny_config("bf16")
+    W = make_weights(cfg, seed, qk_std=0.09)
+    n_seq, max_blocks = 5, 1400 // 16 + 1
+    pk = PagedKV(cfg, n_seq * max_blocks + 3, n_seq, max_blocks, seed)
+    pk.reserve(0, 700)
+    pk.fill_random(1, 37, seed + 1)
+    pk.reserve(1, 37 + 555)
+    pk.reserve(2, 45)
+    pk.fill_random(3, 100, seed + 3)
+    pk.reserve(3, 101)
+    pk.fill_random(4, 16, seed + 4)
+    pk.reserve(4, 17)
+    chunks = [EmbChunk(0, 0, 700, True, "mean"), EmbChunk(1, 37, 555, False, "mean"),
+              EmbChunk(2, 0, 45, True, "last")]
+    rows = [DecodeRow(3, 100), DecodeRow(4, 16)]
+    batch = Batch(chunks, rows, draw_tokens(seed, 1, 700 + 555 + 45 + 2, cfg.vocab))
+    acc_w = np.zeros(n_seq)
+    acc_w[1] = 37
+    return cfg, W, pk, batch, acc_w
+
+
+def test_bf16_batch_over_1280_rows():
+    """More than 1280 rows of one bf16 model: the QKV projection stores fp32 rows, which the
+    16-token x one-head rotation/append kernel rotates and appends (values both as 16-byte runs
+    of 8 slots and one at a time where rows do not fill them).  Every output against the oracle."""
+    cfg, W, pk, batch, acc_w = _over_1280_rows()
+    pair = Pair(cfg, W, pk, acc_w=acc_w)
+    pair.workspace(max_tokens=batch.n_tokens, max_chunks=3, max_decode=2, max_ctx=1400)
+    pair.step(batch)
+    print(pair.report, flush=True)
+
+
+def test_bf16_batch_over_1280_rows_flags_a_bad_page():
+    """The same batch with one block-table entry past the pool: the rotation/append kernel of
+    more than 256 rows flags the page error and skips that page; the step completes."""
+    from paper_2609_25405_amd import runtime as R
+    cfg, W, pk, batch, acc_w = _over_1280_rows()
+    dm = R.DeviceModel(cfg, W)
+    kv = R.DeviceKV.from_paged(pk)
+    bt = pk.block_table.copy()
+    bt[2, 1] = pk.n_pages                 # chunk 2's rows 16..31 point past the pool
+    kv.set_block_table(bt)
+    ws = R.Workspace(dm, dm, batch.n_tokens, 3, 2, 1400)
+    S = torch.zeros((pk.n_seq, cfg.d_model), device="cuda")
+    Wc = torch.tensor(acc_w, dtype=torch.float32, device="cuda")
+    out = torch.zeros((3, cfg.d_model), device="cuda")
+    lg = torch.zeros((2, cfg.vocab), device="cuda")
+    R.step(dm, dm, batch, kv, kv, S, Wc, lg, out, ws)
+    torch.cuda.synchronize()
+    assert ws.device_error() == 1
+    # the requests whose pages are all valid still get finite results
+    assert torch.isfinite(lg).all()
+    assert torch.isfinite(out[0]).all() and abs(out[0].norm().item() - 1.0) < 1e-3
