@@ -96,7 +96,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
         } else {
             load_row_pend<RV>(xv, xrow, a.pend + (size_t)r * a.d, a.pend_stride, a.npend, nv);
         }
-        if (GATHER && a.cs && threadIdx.x < a.hd / 2) {
+        if (GATHER && a.cs && (int)threadIdx.x < a.hd / 2) {
             // rotation table of this token for the QKV epilogue (angle evaluated in double)
             const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
             double sv, cv;
@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(NormArgs a) {
         }
         return;
     }
-    if (GATHER && a.cs && threadIdx.x < a.hd / 2) {
+    if (GATHER && a.cs && (int)threadIdx.x < a.hd / 2) {
         // rotation table of this token for the QKV epilogue (angle evaluated in double)
         const double inv_freq = pow((double)a.rope_base, -2.0 * (double)threadIdx.x / (double)a.hd);
         double sv, cv;
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
     const int t = blockIdx.x;
     const int half = a.hd / 2;
     const int pos = a.pos[t];
-    if (threadIdx.x < half) {
+    if ((int)threadIdx.x < half) {
         if (a.cs) {
             const float2 v = a.cs[(size_t)t * half + threadIdx.x];
             cs[threadIdx.x] = v.x;

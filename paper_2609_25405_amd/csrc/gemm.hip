@@ -19,10 +19,6 @@ namespace {
 
 constexpr int BK = 64;
 
-__device__ __forceinline__ int swz(int row, int chunk) {
-    return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
-}
-
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
 
 // 16-byte global -> LDS copy: lane i of the wave writes lds + 16 * i (lds is wave-uniform).
