@@ -90,13 +90,29 @@ typedef struct orthrus_layer_weights {
 
 /* Model weights.  tok_emb [vocab][d] and lm_head [vocab][d] (may be NULL for an embedding-only
  * model) are device memory of the model dtype; final_norm is fp32 [d] device memory.  `layers`
- * is a HOST array of n_layers entries, copied by orthrus_model_create(). */
+ * is a HOST array of n_layers entries, copied by orthrus_model_create().  lm_head_blocked
+ * (optional, bf16 models only, else NULL): the same LM head in the 64 x 64 blocked layout
+ * orthrus_block_weights() writes; when set, the LM head GEMM reads it instead of lm_head, which
+ * must still be given (it marks the model as having an LM head). */
 typedef struct orthrus_weights {
     const void *tok_emb;
     const float *final_norm;
     const void *lm_head;
     const orthrus_layer_weights *layers;
+    const void *lm_head_blocked;
 } orthrus_weights;
+
+/* Bytes of the blocked copy of a bf16 [rows][cols] weight matrix: ceil(rows / 64) * 64 * cols * 2
+ * (0 unless rows > 0 and cols is a positive multiple of 64). */
+size_t orthrus_blocked_bytes(int32_t rows, int32_t cols);
+
+/* Write the blocked copy of the bf16 row-major matrix src [rows][cols] (device) into dst (device,
+ * orthrus_blocked_bytes() bytes, caller-owned): blocks of 64 rows x 64 columns, row blocks
+ * outermost, each block's 64 rows of 64 values contiguous (8 KB), so the copy of one 64-deep
+ * stage of a weight-streaming GEMM tile reads whole 8 KB runs; rows past `rows` in the last
+ * block are zero.  Enqueued on `stream`.  EINVAL for null pointers or sizes orthrus_blocked_bytes
+ * rejects. */
+int orthrus_block_weights(const void *src, void *dst, int32_t rows, int32_t cols, void *stream);
 
 typedef struct orthrus_model orthrus_model; /* opaque host-side handle */
 

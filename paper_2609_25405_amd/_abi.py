@@ -52,7 +52,7 @@ class orthrus_layer_weights(Structure):
 
 class orthrus_weights(Structure):
     _fields_ = [("tok_emb", c_void_p), ("final_norm", c_void_p), ("lm_head", c_void_p),
-                ("layers", POINTER(orthrus_layer_weights))]
+                ("layers", POINTER(orthrus_layer_weights)), ("lm_head_blocked", c_void_p)]
 
 
 class orthrus_lora_layer(Structure):
@@ -133,6 +133,8 @@ SIGNATURES = {
     "orthrus_model_set_adapters": (c_int, [c_void_p, POINTER(orthrus_lora), c_int32]),
     "orthrus_workspace_bytes": (c_size_t, [c_void_p, c_void_p, c_int32, c_int32, c_int32,
                                            c_int32]),
+    "orthrus_blocked_bytes": (c_size_t, [c_int32, c_int32]),
+    "orthrus_block_weights": (c_int, [c_void_p, c_void_p, c_int32, c_int32, c_void_p]),
     "orthrus_step": (c_int, [c_void_p, c_void_p, POINTER(orthrus_batch), POINTER(orthrus_kv),
                              POINTER(orthrus_kv), c_void_p, c_void_p, c_void_p, c_void_p,
                              c_void_p, c_size_t, c_void_p]),
@@ -201,6 +203,14 @@ def orthrus_model_set_adapters(model, adapters, n):
 
 def orthrus_workspace_bytes(emb, gen, max_tokens, max_chunks, max_decode, max_ctx):
     return load().orthrus_workspace_bytes(emb, gen, max_tokens, max_chunks, max_decode, max_ctx)
+
+
+def orthrus_blocked_bytes(rows, cols):
+    return load().orthrus_blocked_bytes(rows, cols)
+
+
+def orthrus_block_weights(src, dst, rows, cols, stream):
+    return load().orthrus_block_weights(src, dst, rows, cols, stream)
 
 
 def orthrus_step(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits, out_emb, workspace,

@@ -97,8 +97,13 @@ struct GemmArgs {
     size_t split_stride;
     QkvRope rope;    // EPI_QKV_ROPE only
     LoraGemm lora;   // adds the low-rank update before the epilogue (split 0 of a split-K launch)
+    // B0 in the 64 x 64 blocked layout ([ceil(N/64)][K/64][64][64]; bf16 path, not SwiGLU):
+    // one tile stage reads whole 8 KB runs instead of 128-byte pieces of 64 rows
+    int b_blocked;
 };
 hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
+// bf16 [rows][cols] -> the 64 x 64 blocked layout GemmArgs::b_blocked reads (cols % 64 == 0)
+hipError_t launch_block_weights(const void *src, void *dst, int rows, int cols, hipStream_t s);
 // split-K factor (<= max_splits; each split a run of whole 64-deep stages, the stages dealt as
 // evenly as the count allows) for a bf16 residual-add projection of this shape; launch_gemm
 // ignores a requested split count larger than K's number of stages

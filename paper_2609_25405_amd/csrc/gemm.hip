@@ -10,6 +10,8 @@
 // the same XCD (blocks are dealt round-robin to the 8 XCDs), which keeps re-reads of a
 // weight tile inside one L2.
 // fp32 path: plain LDS-tiled FMA kernel (64x64 tile, 4x4 per thread) for exact checks.
+#include <algorithm>
+
 #include "common.hpp"
 #include "orthrus.h"
 
@@ -119,8 +121,11 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
         } else {
             grow = n0 + r;
         }
-        b_src[i] = src + (size_t)min(grow, a.N - 1) * ldb_b + chunk * 16;
+        const int gn = min(grow, a.N - 1);
+        b_src[i] = a.b_blocked ? src + ((size_t)(gn / 64) * (a.K / 64) * 64 + gn % 64) * ROWB + chunk * 16
+                               : src + (size_t)gn * ldb_b + chunk * 16;
     }
+    const size_t b_stage = a.b_blocked ? 64 * ROWB : ROWB;   // bytes between k-stages of a B row
     // this wave's copies of K stage kt of A (into A buffer buf) and of B (into B buffer buf)
     auto copy_a = [&](int kt, int buf) {
         const size_t kb = (size_t)kt * ROWB;
@@ -129,7 +134,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_kernel(GemmArgs a) 
             copy16_to_lds(a_src[j] + kb, smem + buf * BM * ROWB + (NW * j + wave) * 1024);
     };
     auto copy_b = [&](int kt, int buf) {
-        const size_t kb = (size_t)kt * ROWB;
+        const size_t kb = (size_t)kt * b_stage;
 #pragma unroll
         for (int j = 0; j < B_INST; ++j)
             copy16_to_lds<STREAM_B ? kNonTemporal : 0>(b_src[j] + kb, smem_b + buf * BN * ROWB + (NW * j + wave) * 1024);
@@ -511,6 +516,7 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
     const int splits =
         (EPI == EPI_ADD_F32 && a.partial && a.splits > 1 && a.K % BKS == 0 && a.K / BKS >= a.splits) ? a.splits : 1;
     if (STREAM_B && mt != 1) return hipErrorInvalidValue;
+    if (a.b_blocked && (BKS != 64 || EPI == EPI_SWIGLU || a.K % 64)) return hipErrorInvalidValue;
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, BKS, STAGES, BSTAGES, STREAM_B>), dim3(mt * nt * splits),
                        dim3(64 * WM * WN), 0, s, a);
     return hipGetLastError();
@@ -617,8 +623,33 @@ int gemm_add_splits(int M, int N, int K, int max_splits) {
     return best;
 }
 
+// dst [ceil(rows/64)][cols/64][64][64] <- src [rows][cols] (bf16), one 16-byte piece per thread
+// step; rows past `rows` in the last row block are zero
+__global__ __launch_bounds__(256) void block_weights_kernel(const uint4 *src, uint4 *dst, int rows, int cols) {
+    const int cpr = cols / 8;                              // 16-byte pieces per source row
+    const size_t total = (size_t)((rows + 63) / 64) * 64 * cpr;
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (size_t)gridDim.x * 256) {
+        const int c = (int)(i % 8);                        // piece within the block row
+        const size_t q = i / 8;
+        const int r = (int)(q % 64);                       // row within the block
+        const size_t bq = q / 64;                          // block index: rb * (cols / 64) + cb
+        const int cb = (int)(bq % (cols / 64));
+        const int row = (int)(bq / (cols / 64)) * 64 + r;
+        dst[i] = row < rows ? src[(size_t)row * cpr + cb * 8 + c] : uint4{0, 0, 0, 0};
+    }
+}
+
+hipError_t launch_block_weights(const void *src, void *dst, int rows, int cols, hipStream_t s) {
+    const size_t total = (size_t)((rows + 63) / 64) * 64 * (cols / 8);
+    const int blocks = (int)std::min<size_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(block_weights_kernel, dim3(blocks), dim3(256), 0, s, (const uint4 *)src, (uint4 *)dst,
+                       rows, cols);
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, hipStream_t s) {
     if (a.M <= 0) return hipSuccess;
+    if (a.b_blocked && dtype != 1) return hipErrorInvalidValue;
     if (dtype == 1) {
         switch (epi) {
             case EPI_STORE_F32: return dispatch_bf16<EPI_STORE_F32>(a, s);

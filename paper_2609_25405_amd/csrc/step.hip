@@ -188,6 +188,8 @@ int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, or
     const int rc = validate_config(*cfg);
     if (rc) return rc;
     if (!w->tok_emb || !w->final_norm || (cfg->n_layers > 0 && !w->layers)) return ORTHRUS_EINVAL;
+    if (w->lm_head_blocked && !w->lm_head) return ORTHRUS_EINVAL;
+    if (w->lm_head_blocked && cfg->dtype != ORTHRUS_BF16) return ORTHRUS_EUNSUPPORTED;
     for (int l = 0; l < cfg->n_layers; ++l) {
         const orthrus_layer_weights &lw = w->layers[l];
         if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.mlp_norm || !lw.w_gate || !lw.w_up || !lw.w_down)
@@ -201,6 +203,17 @@ int orthrus_model_create(const orthrus_config *cfg, const orthrus_weights *w, or
     m->w.layers = m->layers.data();
     *out = m;
     return ORTHRUS_OK;
+}
+
+size_t orthrus_blocked_bytes(int32_t rows, int32_t cols) {
+    if (rows <= 0 || cols <= 0 || cols % 64) return 0;
+    return (size_t)((rows + 63) / 64) * 64 * (size_t)cols * 2;
+}
+
+int orthrus_block_weights(const void *src, void *dst, int32_t rows, int32_t cols, void *stream) {
+    if (!src || !dst || orthrus_blocked_bytes(rows, cols) == 0) return ORTHRUS_EINVAL;
+    return launch_block_weights(src, dst, rows, cols, (hipStream_t)stream) == hipSuccess ? ORTHRUS_OK
+                                                                                          : ORTHRUS_EHIP;
 }
 
 int orthrus_model_set_adapters(orthrus_model *m, const orthrus_lora *adapters, int32_t n) {
@@ -714,7 +727,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     if (p.n_lm > 0) {
         GemmArgs ga{};
         ga.A = act;
-        ga.B0 = gen->w.lm_head;
+        ga.B0 = gen->w.lm_head_blocked ? gen->w.lm_head_blocked : gen->w.lm_head;
+        ga.b_blocked = gen->w.lm_head_blocked != nullptr;
         ga.out = out_logits;
         ga.M = p.n_lm;
         ga.N = gen->cfg.vocab;

@@ -39,9 +39,12 @@ def abi_config(cfg) -> A.orthrus_config:
 
 
 class DeviceModel:
-    """Weights uploaded to the GPU in the model dtype (norm gains fp32) plus the library handle."""
+    """Weights uploaded to the GPU in the model dtype (norm gains fp32) plus the library handle.
 
-    def __init__(self, cfg, weights, device="cuda"):
+    bf16 models with an LM head also get its 64 x 64 blocked copy (orthrus_block_weights), which
+    the step's LM head GEMM then reads; ``block_lm_head=False`` keeps the row-major one only."""
+
+    def __init__(self, cfg, weights, device="cuda", block_lm_head: bool = True):
         self.cfg = cfg
         dt = torch_dtype(cfg)
 
@@ -62,8 +65,20 @@ class DeviceModel:
         for i, lw in enumerate(self.layers):
             self._lw[i] = A.orthrus_layer_weights(*[_vp(lw[k]) for k in (
                 "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate", "w_up", "w_down")])
+        self.lm_head_blocked = None
+        if (block_lm_head and self.lm_head is not None and cfg.dtype == "bf16"
+                and torch.device(device).type == "cuda"):
+            V, d = self.lm_head.shape
+            nb = A.orthrus_blocked_bytes(V, d)
+            if nb == 0:
+                raise A.OrthrusError(A.ORTHRUS_EINVAL, "orthrus_blocked_bytes")
+            self.lm_head_blocked = torch.empty(nb // 2, dtype=torch.bfloat16, device=device)
+            _check(A.orthrus_block_weights(_vp(self.lm_head), _vp(self.lm_head_blocked), V, d,
+                                           c_void_p(current_stream())), "orthrus_block_weights")
+            torch.cuda.current_stream().synchronize()   # steps may run on another stream
         self._w = A.orthrus_weights(_vp(self.tok_emb), _vp(self.final_norm), _vp(self.lm_head),
-                                    ctypes.cast(self._lw, POINTER(A.orthrus_layer_weights)))
+                                    ctypes.cast(self._lw, POINTER(A.orthrus_layer_weights)),
+                                    _vp(self.lm_head_blocked))
         self._cfg = abi_config(cfg)
         h = c_void_p()
         _check(A.orthrus_model_create(byref(self._cfg), byref(self._w), byref(h)),

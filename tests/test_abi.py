@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = P.load()
     names = header_functions()
     assert [os.path.basename(h) for h in HEADERS] == ["orthrus.h", "orthrus_sched.h"]
-    assert len(names) == 12 + 12
+    assert len(names) == 14 + 12
     for n in names:
         assert hasattr(lib, n), n
         assert n in A.SIGNATURES, n
@@ -517,3 +517,15 @@ def test_adapter_registration_and_host_validation():
     # four distinct adapters (one of them twice) plan fine
     ok = Batch([EmbChunk(s, 0, 2, True) for s in range(5)], [], ids[:10], chunk_adapter=[3, 1, 3, 0, 5])
     R.plan(m, m, ok, kv, kv)
+
+
+def test_blocked_weight_sizes():
+    """The blocked copy of a [rows][cols] bf16 matrix rounds rows up to whole 64-row blocks and
+    needs cols to be a multiple of 64."""
+    from paper_2609_25405_amd import _abi as A
+    assert A.orthrus_blocked_bytes(32000, 4096) == 32000 * 4096 * 2
+    assert A.orthrus_blocked_bytes(100, 64) == 128 * 64 * 2
+    assert A.orthrus_blocked_bytes(1, 128) == 64 * 128 * 2
+    for rows, cols in ((0, 64), (-1, 64), (64, 0), (64, 96), (64, -64)):
+        assert A.orthrus_blocked_bytes(rows, cols) == 0
+    assert A.orthrus_block_weights(None, None, 64, 64, None) == A.ORTHRUS_EINVAL

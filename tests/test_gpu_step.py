@@ -211,6 +211,38 @@ def test_layer7b_decode_batches_up_to_192_rows(n_dec):
     print(pair.report, flush=True)
 
 
+@pytest.mark.parametrize("n_dec", [64, 128])
+def test_blocked_lm_head_gives_the_same_logits(n_dec):
+    """The LM head read from its 64 x 64 blocked copy (the default for bf16 models) and from the
+    row-major weights give bit-identical logits (same tiles, same arithmetic); a vocabulary that
+    is not a multiple of 64 exercises the zero-padded last row block."""
+    cfg = ModelConfig(n_layers=1, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128, d_ff=1024,
+                      vocab=4000 + 37, dtype="bf16")
+    W = make_weights(cfg, 71)
+    P = cfg.page_size
+    pk = PagedKV(cfg, n_dec * 4 + 3, n_dec, 4, 71)
+    rows = [DecodeRow(i, 17 + i % 40) for i in range(n_dec)]
+    for r in rows:
+        pk.fill_random(r.seq, r.ctx_len, 71)
+        pk.reserve(r.seq, r.ctx_len + 1)
+    batch = Batch([], rows, draw_tokens(71, 1, n_dec, cfg.vocab))
+    out = {}
+    for blocked in (True, False):
+        dm = R.DeviceModel(cfg, W, block_lm_head=blocked)
+        assert (dm.lm_head_blocked is not None) == blocked
+        kv = R.DeviceKV.from_paged(pk)
+        ws = R.Workspace(dm, dm, n_dec, 1, n_dec, 4 * P)
+        lg = torch.zeros((n_dec, cfg.vocab), device="cuda")
+        S = torch.zeros((n_dec, cfg.d_model), device="cuda")
+        Wc = torch.zeros(n_dec, device="cuda")
+        R.step(dm, dm, batch, kv, kv, S, Wc, lg, None, ws)
+        torch.cuda.synchronize()
+        assert ws.device_error() == 0
+        out[blocked] = lg.cpu()
+    assert torch.isfinite(out[True]).all()
+    assert torch.equal(out[True], out[False])
+
+
 def test_device_errors_are_flagged_not_faulted():
     """A chunk whose pooling state does not match its offset, and a block-table entry past the
     pool, raise device error bits; the step still completes and nothing outside is written."""
