@@ -102,7 +102,9 @@ typedef struct orthrus_weights {
     const void *lm_head_blocked;
 } orthrus_weights;
 
-/* Bytes of the blocked copy of a bf16 [rows][cols] weight matrix: ceil(rows / 64) * 64 * cols * 2
+/* Weight layout helpers for the LM head that turns the decode rows' hidden states into logits
+ * (the generation side of Algorithm 1's forward pass); a memory layout only, no arithmetic.
+ * Bytes of the blocked copy of a bf16 [rows][cols] weight matrix: ceil(rows / 64) * 64 * cols * 2
  * (0 unless rows > 0 and cols is a positive multiple of 64). */
 size_t orthrus_blocked_bytes(int32_t rows, int32_t cols);
 
