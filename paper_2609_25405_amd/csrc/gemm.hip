@@ -565,6 +565,9 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
         if (a.M > 896 || (w128 > 512 && w192 <= 256) || pad192 <= pad128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else {
+        // the blocked LM head of 33..64 rows: 64x128 tiles (16 KB runs per stage) 49.5 -> 46.9 us
+        if (EPI == EPI_STORE_F32 && a.b_blocked && a.M > 32 && a.M <= 64)
+            return run_bf16<64, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
         if (a.M <= 64) return run_bf16<64, 64, 2, 2, EPI, 64, 4, 4, true>(a, s);
         const bool split = EPI == EPI_ADD_F32 && a.partial && a.splits > 1;
         if (split && a.M <= 128) return run_bf16<128, 64, 2, 2, EPI, 64, 4, 4, true>(a, s);
