@@ -1,20 +1,25 @@
 #!/usr/bin/env python3
 """Throughput of the mixed embedding-chunk + decode step on one MI355X.
 
-Workload: one 7B-shape decoder layer in bf16 (hidden 4096, 32 query heads sharing 8 KV heads
-of 128, SwiGLU 14336, vocab-32000 LM head) over a 2048-token-budget mixed batch: 1024
-embedding-chunk tokens from two requests (chunk 512, last-token pooling; one request resumes
-after 1536 cached tokens) plus 64 decode rows with contexts uniform in [1024, 4096] on 16-token
-pages.  Weights N(0, 0.02), caches N(0, 1), token ids uniform: all seeded and synthetic.
+Default workload (the largest configuration that fits one GPU): two resident 32-layer 7B-shape
+models in bf16 (hidden 4096, 32 query heads sharing 8 KV heads of 128, SwiGLU 14336): an
+embedding model (mean pooling, L2-normalised output, no LM head) and a generator (vocab 32000).
+One step holds half of a 2048-token budget in embedding-query chunks (lengths lognormal with
+mean 64, single final chunks) and 256 decode rows of generation requests (contexts lognormal
+with mean 512, 16-token pages).  Weights N(0, 0.02) and caches N(0, 1) are drawn on the device
+from seeds, token ids uniform: all synthetic.
 
-A step is one orthrus_step call over that batch (every kernel of the path).  The same step is
-repeated: the decode rows rewrite their own slot and the resuming request's token count is
-restored before each step (a one-element device fill), so every repetition is a valid step.
+A step is one orthrus_step call over that batch (every kernel of the path, both models).  The
+same step is repeated: the queries restart at offset 0 and the decode rows rewrite their own
+slot, so every repetition is a valid step.
 
 Prints one JSON line.  `value` = (embedding tokens + decode tokens) per second of step time,
-inputs resident in HBM.  `roofline` describes the kernel with the largest share of the step,
-from HIP events around each launch on the step's stream.  `cpu_baseline` times the float64
-CPU oracle on the same step.
+inputs resident in HBM.  `kernels` gives every launch class's average time (HIP events around
+each launch on the stream it runs on) against its own roofline: algorithmic flops against bf16
+MFMA peak or algorithmic bytes against HBM peak, whichever bounds it.  `roofline` describes the
+kernel with the largest share of the step.  `cpu_baseline` times the float64 CPU oracle on a
+sample of the same step (see cpu_baseline_two_models).  Extra keys: the same two models over an
+embedding-fraction sweep (`sweep`), and the one-7B-layer mixed step (`layer7b`).
 """
 from __future__ import annotations
 
@@ -30,13 +35,15 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 METRIC = "mixed-step throughput: embed tokens/s + decode tokens/s; %MFMA and %HBM peak"
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_gate_up_7b_layer_mixed_traffic.md")
+PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_25405_amd", "csrc", f) for f in ("gemm.hip", "common.hpp")]
+DATA = "synthetic (seeded N(0,0.02) weights and N(0,1) bf16 caches drawn on the device, uniform token ids)"
+GEMMS = ("gemm_qkv", "gemm_qkv_rope", "gemm_o", "gemm_gate_up", "gemm_down", "lm_head")
 
 
 def kernel_source_hash() -> str:
-    """SHA-256 of the dominant kernel's sources with comments and whitespace removed: a change of
-    code invalidates the committed counter summary, a change of comments does not."""
+    """SHA-256 of the GEMM kernel's sources with comments and whitespace removed: a change of
+    code invalidates a committed counter summary, a change of comments does not."""
     import hashlib
     import re
     h = hashlib.sha256()
@@ -49,94 +56,470 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary,
-    or None when the summary is missing, covers another kernel, or the source changed since."""
-    try:
-        kv = {}
-        with open(TRAFFIC_SUMMARY) as f:
-            for line in f:
-                if ":" in line and not line.startswith("#"):
-                    k, v = line.split(":", 1)
-                    kv[k.strip().lstrip("- ").strip()] = v.strip()
-        if kv.get("step_kernel") != kernel or kv.get("source_sha256") != kernel_source_hash():
-            return None
-        return float(kv["traffic_bytes_per_launch"])
-    except (OSError, KeyError, ValueError):
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` in `workload` from a committed rocprofv3 counter summary
+    (profiles/*_traffic.md), or None when there is none for that pair or the GEMM sources changed
+    since it was taken."""
+    if not os.path.isdir(PROFILES):
         return None
+    for fn in sorted(os.listdir(PROFILES)):
+        if not fn.endswith("_traffic.md"):
+            continue
+        kv = {}
+        try:
+            with open(os.path.join(PROFILES, fn)) as f:
+                for line in f:
+                    if ":" in line and line.startswith("- "):
+                        k, v = line[2:].split(":", 1)
+                        kv[k.strip()] = v.strip()
+        except OSError:
+            continue
+        if kv.get("step_kernel") == kernel and kv.get("workload") == workload:
+            if kv.get("source_sha256") != kernel_source_hash():
+                return None
+            try:
+                return float(kv["traffic_bytes_per_launch"])
+            except (KeyError, ValueError):
+                return None
+    return None
 
 
-def algorithmic_work(cfg, batch):
-    """Flops (GEMMs, attention) and bytes (decode KV reads) the step must do, per launch class."""
-    T, Te, D = batch.n_tokens, batch.n_emb_tokens, len(batch.rows)
-    d, F, V = cfg.d_model, cfg.d_ff, cfg.vocab
-    qd, qkv = cfg.q_dim, cfg.qkv_dim
-    L = cfg.n_layers
+# ------------------------------------------------------------------------------ work per launch
+def group_rows(batch, two_models: bool):
+    """Rows of each profile tag: '' (the embedding model's rows, or all rows with one model) and
+    '@gen' (the generator's rows of a two-model step)."""
+    T, Te = batch.n_tokens, batch.n_emb_tokens
+    return {"": Te, "@gen": T - Te} if two_models else {"": T}
+
+
+def launch_work(cfg, batch, two_models: bool):
+    """Algorithmic work of every profiled launch name: {name: (flops, bytes)} per launch.
+
+    What the method must compute or move, not what the kernels execute: GEMMs 2 M K N flops over
+    their weights, input rows and output rows (residual-add projections read and write the fp32
+    residual rows once); attention 4 hd nq flops per (query, visible key) pair of chunk rows and
+    decode rows, over every visible key's K and V once per KV head plus q and o; norms and the
+    final norm / pooler over their rows.  Split-K slabs, attention partials and the fp32 rows of
+    the unfused rotation path are implementation traffic: rope_append and attn_combine carry no
+    algorithmic work (their work is counted in gemm_qkv and attention)."""
+    d, F, V, L = cfg.d_model, cfg.d_ff, cfg.vocab, cfg.n_layers
+    qd, kvd, qkv = cfg.q_dim, cfg.kv_dim, cfg.qkv_dim
     es = 2 if cfg.dtype == "bf16" else 4
-    work = {
-        "gemm_qkv": ("flop", 2.0 * T * d * qkv, L),
-        "gemm_qkv_rope": ("flop", 2.0 * T * d * qkv, L),   # bf16: rotation and cache append fused
-        "gemm_o": ("flop", 2.0 * T * qd * d, L),
-        "gemm_gate_up": ("flop", 2.0 * T * d * 2 * F, L),
-        "gemm_down": ("flop", 2.0 * T * F * d, L),
-        "lm_head": ("flop", 2.0 * D * d * V, 1),
-    }
-    # attention: chunk rows (query, visible key) pairs on MFMA; decode rows read K and V of every
-    # visible key once per KV head
+    T = batch.n_tokens
+    work = {}
+    for tag, M in group_rows(batch, two_models).items():
+        if M == 0:
+            continue
+        work["gather_norm" + tag] = (0.0, M * d * (es + 4 + es))
+        work["rmsnorm" + tag] = (0.0, M * d * (4 + es))
+        qkv_w = (2.0 * M * d * qkv, d * qkv * es + M * d * es + M * qd * es + M * 2 * kvd * es)
+        work["gemm_qkv_rope" + tag] = qkv_w
+        work["gemm_qkv" + tag] = qkv_w
+        work["gemm_o" + tag] = (2.0 * M * qd * d, qd * d * es + M * qd * es + 2 * M * d * 4)
+        work["gemm_gate_up" + tag] = (2.0 * M * d * 2 * F, 2 * F * d * es + M * d * es + M * F * es)
+        work["gemm_down" + tag] = (2.0 * M * F * d, F * d * es + M * F * es + 2 * M * d * 4)
     pairs = sum(sum(c.offset + i + 1 for i in range(c.len)) for c in batch.chunks)
+    pairs += sum(sum(c.offset + i + 1 for i in range(c.len)) for c in (getattr(batch, "gen_chunks", None) or []))
     dec_keys = sum(r.ctx_len + 1 for r in batch.rows)
-    work["attention"] = ("byte", 2.0 * dec_keys * cfg.n_kv_heads * cfg.head_dim * es, L)
-    work["_attention_flop"] = ("flop", 4.0 * pairs * cfg.head_dim * cfg.n_q_heads, L)
+    chunk_keys = sum(c.offset + c.len for c in batch.chunks)
+    chunk_keys += sum(c.offset + c.len for c in (getattr(batch, "gen_chunks", None) or []))
+    kv_per_key = 2 * kvd * es
+    work["attention"] = (4.0 * (pairs + dec_keys) * cfg.head_dim * cfg.n_q_heads,
+                         (dec_keys + chunk_keys) * kv_per_key + 2 * T * qd * es)
+    work["rope_append"] = (0.0, 0.0)
+    work["attn_combine"] = (0.0, 0.0)
+    n_lm = batch.n_logit_rows
+    final = batch.n_emb_tokens * d * 4 + n_lm * d * (4 + es) + len(batch.chunks) * d * 4 * 3
+    work["final_norm_pool"] = (0.0, final)
+    work["final_norm"] = (0.0, final)
+    work["pool"] = (0.0, 0.0)
+    if n_lm:
+        work["lm_head"] = (2.0 * n_lm * d * V, d * V * es + n_lm * d * es + n_lm * V * 4)
     return work
 
 
-def step_roofline(cfg, batch, t_step_ms):
-    """Ideal step time if every kernel class ran at its own roofline, one after another:
-    sum over classes of max(F / bf16 MFMA peak, B / HBM peak), with F the algorithmic flops and
-    B the least HBM bytes the class must move (weights, activations in and out, the KV it reads
-    and writes, the residual stream read and written once; split-K slabs, partials and
-    metadata are implementation traffic and not counted).  Returns (ideal_ms, ideal / measured)."""
-    T, Te, D = batch.n_tokens, batch.n_emb_tokens, len(batch.rows)
-    d, F, V = cfg.d_model, cfg.d_ff, cfg.vocab
-    qd, kvd, qkv = cfg.q_dim, cfg.kv_dim, cfg.qkv_dim
+def decode_kv_bytes(cfg, batch) -> float:
+    """Keys and values the decode rows must read per layer (every visible key once per KV head)."""
     es = 2 if cfg.dtype == "bf16" else 4
-    L = cfg.n_layers
-    pairs = sum(sum(c.offset + i + 1 for i in range(c.len)) for c in batch.chunks)
-    dec_keys = sum(r.ctx_len + 1 for r in batch.rows)
-    chunk_keys = sum(c.offset + c.len for c in batch.chunks)       # each chunk reads its keys once
-    kv_per_key = 2 * kvd * es
-    n_lm = D + sum(1 for c in getattr(batch, "gen_chunks", None) or [] if c.last)
-    classes = {
-        "gather_norm": (0.0, T * d * (es + 4 + es)),
-        "gemm_qkv_rope": (2.0 * T * d * qkv * L, (d * qkv * es + T * d * es + T * qd * es + T * kv_per_key) * L),
-        "attention": (4.0 * pairs * cfg.head_dim * cfg.n_q_heads * L,
-                      ((dec_keys + chunk_keys) * kv_per_key + 2 * T * qd * es) * L),
-        "gemm_o": (2.0 * T * qd * d * L, (qd * d * es + T * qd * es + 2 * T * d * 4) * L),
-        "rmsnorm": (0.0, T * d * (4 + es) * (2 * L - 1)),
-        "gemm_gate_up": (2.0 * T * d * 2 * F * L, (2 * F * d * es + T * d * es + T * F * es) * L),
-        "gemm_down": (2.0 * T * F * d * L, (F * d * es + T * F * es + 2 * T * d * 4) * L),
-        "final_norm_pool": (0.0, (n_lm + len(batch.chunks)) * d * (4 + es)),
-        "lm_head": (2.0 * n_lm * d * V, d * V * es + n_lm * d * es + n_lm * V * 4),
+    return 2.0 * sum(r.ctx_len + 1 for r in batch.rows) * cfg.kv_dim * es
+
+
+def kernel_table(cfg, batch, two_models: bool, prof: dict, steps: int):
+    """Per launch name: launches per step, average ms, and the launch against its roofline."""
+    work = launch_work(cfg, batch, two_models)
+    out = {}
+    for name, (n, tot) in prof.items():
+        avg = tot / max(n, 1)
+        ent = {"launches_per_step": n / steps, "avg_ms": avg}
+        if name in work and any(work[name]):
+            f, b = work[name]
+            t_f, t_b = f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)
+            ent["bound"] = "mfma" if t_f >= t_b else "hbm"
+            if ent["bound"] == "mfma":
+                ent["tflops"] = f / (avg * 1e-3) / 1e12
+            else:
+                ent["gbs"] = b / (avg * 1e-3) / 1e9
+            ent["frac"] = max(t_f, t_b) / (avg * 1e-3)
+            ent["algorithmic_flop"], ent["algorithmic_bytes"] = f, b
+        out[name] = ent
+    return out
+
+
+def summarize(cfg, batch, two_models: bool, ms: float, prof: dict, steps: int, workload: str) -> dict:
+    """tokens/s, the kernel table, the MFMA fraction of the MFMA-bound GEMMs, the HBM fraction
+    of the decode attention, the dominant kernel's roofline and the step roofline."""
+    kernels = kernel_table(cfg, batch, two_models, prof, steps)
+    Te, T, D = batch.n_emb_tokens, batch.n_tokens, len(batch.rows)
+    work = launch_work(cfg, batch, two_models)
+    f_m = t_m = b_h = t_h = 0.0
+    for name, e in kernels.items():
+        if name.split("@")[0] in GEMMS and "bound" in e:
+            t = e["avg_ms"] * e["launches_per_step"]
+            if e["bound"] == "mfma":
+                f_m += e["algorithmic_flop"] * e["launches_per_step"]
+                t_m += t
+            else:
+                b_h += e["algorithmic_bytes"] * e["launches_per_step"]
+                t_h += t
+    attn = kernels.get("attention")
+    res = {
+        "ms_per_step": ms,
+        "value": T / (ms * 1e-3),
+        "embed_tokens_per_s": Te / (ms * 1e-3),
+        "decode_tokens_per_s": D / (ms * 1e-3),
+        "gemm_frac_mfma": f_m / (t_m * 1e-3) / 1e12 / PEAK_BF16_TFLOPS if t_m else None,
+        "gemm_hbm_bound_frac_hbm": b_h / (t_h * 1e-3) / 1e9 / PEAK_HBM_GBS if t_h else None,
+        "attention_frac_hbm": (decode_kv_bytes(cfg, batch) / (attn["avg_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS
+                               if attn and batch.rows else None),
+        "attention_roofline_frac": attn.get("frac") if attn else None,
     }
-    ideal_s = sum(max(f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)) for f, b in classes.values())
-    return ideal_s * 1e3, ideal_s * 1e3 / t_step_ms
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches_per_step"])
+    dk = kernels[dom]
+    f, b = work.get(dom, (0.0, 0.0))
+    if dk.get("bound") == "mfma":
+        roof = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"], "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": dk["frac"], "traffic": measured_traffic(dom, workload),
+                "algorithmic_per_launch": f, "algorithmic_bytes_per_launch": b, "avg_launch_ms": dk["avg_ms"]}
+    else:
+        roof = {"kernel": dom, "bound": "hbm", "achieved": dk.get("gbs"), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": dk.get("frac"), "traffic": measured_traffic(dom, workload),
+                "algorithmic_per_launch": b, "avg_launch_ms": dk["avg_ms"]}
+    res["roofline"] = roof
+    res["kernels"] = kernels
+    ideal = sum(max(w[0] / (PEAK_BF16_TFLOPS * 1e12), w[1] / (PEAK_HBM_GBS * 1e9)) * kernels[k]["launches_per_step"]
+                for k, w in work.items() if k in kernels)
+    res["step_roofline"] = {"ideal_ms": ideal * 1e3, "frac": ideal * 1e3 / ms,
+                            "definition": "sum over the step's launches of max(algorithmic flops / 2.5 PFLOP/s, "
+                                          "algorithmic bytes / 8 TB/s), divided by the measured step time"}
+    return res
+
+
+# ------------------------------------------------------------------------------ device set-up
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def device_model(cfg, seed, tag):
+    import torch
+    from paper_2609_25405_amd import runtime as R
+    from workload import device_weights
+    W = device_weights(cfg, seed, tag)
+    torch.cuda.synchronize()
+    dm = R.DeviceModel(cfg, W)
+    log(f"model (tag {tag}) drawn: {cfg.n_layers} layers")
+    return dm, W
+
+
+def device_kv(cfg, n_pages, n_seq, max_blocks, block_table, seed):
+    import torch
+    from paper_2609_25405_amd import runtime as R
+    from workload import fill_device_pools
+    need = 2 * cfg.n_layers * n_pages * cfg.n_kv_heads * cfg.page_size * cfg.head_dim * 2
+    free = torch.cuda.mem_get_info()[0]
+    if need > 0.9 * free:
+        raise SystemExit(f"cache of {need / 2**30:.1f} GiB does not fit ({free / 2**30:.1f} GiB free)")
+    kv = R.DeviceKV(cfg, n_pages, n_seq, max_blocks, fill=0.0)
+    kv.set_block_table(block_table)
+    fill_device_pools(kv.k, kv.v, seed)
+    torch.cuda.synchronize()
+    log(f"cache {need / 2**30:.1f} GiB drawn")
+    return kv
+
+
+class Stepper:
+    """Repeats one batch through orthrus_step with fixed output buffers; `reset` restores what a
+    repetition must find (e.g. a resuming request's token count) before each step."""
+
+    def __init__(self, dm_e, dm_g, kv_e, kv_g, batch, ws, n_seq_e, acc_w0=None):
+        import torch
+        from paper_2609_25405_amd import runtime as R
+        self.R = R
+        self.args = (dm_e, dm_g, kv_e, kv_g)
+        self.batch, self.ws = batch, ws
+        d = dm_e.cfg.d_model
+        self.acc_sum = torch.zeros((n_seq_e, d), device="cuda")
+        self.acc_w0 = (torch.zeros(n_seq_e, device="cuda") if acc_w0 is None
+                       else torch.as_tensor(acc_w0, dtype=torch.float32, device="cuda"))
+        self.acc_w = self.acc_w0.clone()
+        self.logits = torch.empty((max(1, batch.n_logit_rows), dm_g.cfg.vocab), device="cuda")
+        self.out_emb = torch.empty((max(1, len(batch.chunks)), d), device="cuda")
+        self.packed = R.PackedBatch(batch)
+
+    def __call__(self):
+        dm_e, dm_g, kv_e, kv_g = self.args
+        self.acc_w.copy_(self.acc_w0)
+        self.R.step(dm_e, dm_g, self.batch, kv_e, kv_g, self.acc_sum, self.acc_w, self.logits, self.out_emb,
+                    self.ws, packed=self.packed)
+
+    def time(self, steps: int, warmup: int) -> float:
+        """Average ms per step over `steps` steps after `warmup` untimed ones."""
+        import torch
+        for _ in range(warmup):
+            self()
+        torch.cuda.synchronize()
+        assert self.ws.device_error() == 0, "device error during warmup"
+        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        st.record()
+        for _ in range(steps):
+            self()
+        en.record()
+        torch.cuda.synchronize()
+        assert self.ws.device_error() == 0, "device error during timed steps"
+        return st.elapsed_time(en) / steps
+
+    def profile(self, steps: int) -> dict:
+        """Per launch name (launches, total ms) from HIP events around each launch."""
+        import torch
+        dm_e = self.args[0]
+        self.R.profile_begin(dm_e)
+        for _ in range(steps):
+            self()
+        prof = self.R.profile_end(dm_e)
+        torch.cuda.synchronize()
+        assert self.ws.device_error() == 0, "device error during the profiled steps"
+        return prof
+
+
+# ------------------------------------------------------------------------------ CPU baseline
+def host_info() -> dict:
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+
+
+def blas_threads(n: int):
+    """Limit BLAS threads to n; returns (limiter or None, threads in use)."""
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        lim = threadpool_limits(limits=n)
+        used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return lim, used
+    except Exception:
+        return None, n
+
+
+def host_layers(W, n_layers: int):
+    """float64 host copies of the global tensors and the first n_layers layers of device weights."""
+    import numpy as np
+    f = lambda t: None if t is None else t.float().cpu().numpy().astype(np.float64)
+    return {"tok_emb": f(W["tok_emb"]), "final_norm": f(W["final_norm"]), "lm_head": f(W.get("lm_head")),
+            "layers": [{k: f(v) for k, v in W["layers"][l].items()} for l in range(n_layers)]}
+
+
+def cpu_baseline_two_models(W_e, W_g, kv_g, batch, rec_g, threads: int, n_rows: int = 32) -> dict:
+    """The float64 oracle on a sample of the two-model step, extrapolated to the whole step.
+
+    Sample: every query (through the embedding model) and the first `n_rows` decode rows (through
+    the generator, keys and values copied from the device cache), each at 1 and at 2 layers of
+    the same device-drawn weights (copied to the host).  Per-layer time = t(2) - t(1); the 32-layer
+    time of each part is t(1) + 31 (t(2) - t(1)) (the LM head and the final norm counted once),
+    and the decode part is scaled by D / n_rows (the oracle runs each request alone).  An
+    extrapolation, stated as one in the result."""
+    import numpy as np
+    import torch
+    from oracle import OracleKV, step_oracle
+    from workload import Batch, DecodeRow, EmbChunk, llm7b_config
+    n = threads or len(os.sched_getaffinity(0))
+    lim, used = blas_threads(n)
+    P = 16
+    Te, D = batch.n_emb_tokens, len(batch.rows)
+    rows = batch.rows[:n_rows]
+    q = Batch([EmbChunk(i, 0, c.len, True, c.pool) for i, c in enumerate(batch.chunks)], [],
+              batch.token_ids[:Te])
+    r = Batch([], [DecodeRow(i, x.ctx_len) for i, x in enumerate(rows)], batch.token_ids[Te:Te + len(rows)])
+    pages = [rec_g.block_table[x.seq][rec_g.block_table[x.seq] >= 0] for x in rows]
+    flat = torch.from_numpy(np.concatenate(pages).astype(np.int64)).to(kv_g.k.device)
+    bt = np.full((len(rows), rec_g.max_blocks), -1, np.int64)
+    o = 0
+    for i, p in enumerate(pages):
+        bt[i, :len(p)] = np.arange(o, o + len(p))
+        o += len(p)
+    q_pages = sum(-(-c.len // P) for c in batch.chunks)
+    q_bt = np.full((len(batch.chunks), 2048 // P + 1), -1, np.int64)
+    o = 0
+    for i, c in enumerate(batch.chunks):
+        k = -(-c.len // P)
+        q_bt[i, :k] = np.arange(o, o + k)
+        o += k
+    times = {}
+    for L in (1, 2):
+        cfg_e = llm7b_config(n_layers=L, has_lm_head=False)
+        cfg_g = llm7b_config(n_layers=L)
+        We, Wg = host_layers(W_e, L), host_layers(W_g, L)
+        k64 = kv_g.k[:L, flat].float().cpu().numpy().astype(np.float64)
+        v64 = kv_g.v_by_position[:L, flat].float().cpu().numpy().astype(np.float64)
+        okv_g = OracleKV(k64, v64, bt, P)
+        shape = (L, q_pages, cfg_e.n_kv_heads, P, cfg_e.head_dim)
+        okv_e = OracleKV(np.zeros(shape), np.zeros(shape), q_bt, P)
+        t0 = time.perf_counter()
+        step_oracle((cfg_e, We), (cfg_g, Wg), q, okv_e, okv_g, np.zeros((len(batch.chunks), cfg_e.d_model)),
+                    np.zeros(len(batch.chunks)))
+        t1 = time.perf_counter()
+        step_oracle((cfg_e, We), (cfg_g, Wg), r, okv_e, okv_g, np.zeros((len(batch.chunks), cfg_e.d_model)),
+                    np.zeros(len(batch.chunks)))
+        t2 = time.perf_counter()
+        times[L] = (t1 - t0, t2 - t1)
+        del We, Wg, okv_g, okv_e, k64, v64
+    (q1, r1), (q2, r2) = times[1], times[2]
+    t_q = q1 + 31 * (q2 - q1)
+    t_r = (r1 + 31 * (r2 - r1)) * D / len(rows)
+    if lim is not None:
+        lim.restore_original_limits()
+    return {"value": (Te + D) / (t_q + t_r), "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "sample": f"float64 oracle on the same step's {len(batch.chunks)} queries ({Te} tokens) and "
+                      f"{len(rows)} of its {D} decode rows, each at 1 and 2 layers of the same weights "
+                      f"(queries {q1:.2f} / {q2:.2f} s, rows {r1:.2f} / {r2:.2f} s); extrapolated to 32 "
+                      f"layers as t1 + 31 (t2 - t1) and to all {D} rows: {t_q + t_r:.1f} s per step",
+            "extrapolated": True, **host_info()}
+
+
+def cpu_baseline_step(wl, threads: int, min_seconds: float = 10.0) -> dict:
+    """The float64 oracle on a whole one-layer step, repeated to about `min_seconds`."""
+    from oracle import OracleKV, step_oracle
+    from workload import as_float64
+    n = threads or len(os.sched_getaffinity(0))
+    lim, used = blas_threads(n)
+    okv = OracleKV.from_paged(wl.kv)
+    W64 = as_float64(wl.weights)
+    reps, t0 = 0, time.time()
+    while reps == 0 or time.time() - t0 < min_seconds:
+        step_oracle((wl.cfg, W64), (wl.cfg, W64), wl.batch, okv, okv, wl.acc_sum, wl.acc_w)
+        reps += 1
+    dt = (time.time() - t0) / reps
+    if lim is not None:
+        lim.restore_original_limits()
+    T = wl.batch.n_tokens
+    return {"value": T / dt, "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "sample": f"{reps} full steps of the same workload ({T} tokens each), float64 NumPy, {dt:.2f} s per step",
+            **host_info()}
+
+
+# ------------------------------------------------------------------------------ workloads
+TWO_MODELS = ("two-models-32l: two resident 32-layer 7B-shape bf16 models (embedding: mean pooling, no LM "
+              "head; generator: vocab 32000), 2048-token budget at embedding fraction 0.5: {nq} query "
+              "chunks (lognormal mean 64, {te} tokens) + {d} decode rows (contexts lognormal mean 512), page 16")
+LAYER7B = ("7b-layer-mixed-2048: 1 layer d4096 32q/8kv x128 ffn14336 vocab32000 bf16; 2 chunks x512 (offsets 0 "
+           "and 1536, last-token pooling) + 64 decode rows ctx U[1024,4096], page 16")
+
+
+def two_models_bench(args, layers: int = 32) -> dict:
+    """The headline: both models at embedding fraction 0.5, with the fraction sweep as extras."""
+    import torch
+    from paper_2609_25405_amd import runtime as R
+    from workload import llm7b_config, retrieval_mix_scenario
+    _, _, _, _, paged_e, paged_g, steps = retrieval_mix_scenario(n_layers=1)
+    cfg_e, cfg_g = llm7b_config(n_layers=layers, has_lm_head=False), llm7b_config(n_layers=layers)
+    dm_e, W_e = device_model(cfg_e, 1003, 1)
+    dm_g, W_g = device_model(cfg_g, 1003, 2)
+    kv_e = device_kv(cfg_e, paged_e.n_pages, paged_e.n_seq, paged_e.max_blocks, paged_e.block_table, 1)
+    kv_g = device_kv(cfg_g, paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
+    ws = R.Workspace(dm_e, dm_g, max(b.n_tokens for b in steps), max(1, max(len(b.chunks) for b in steps)),
+                     max(len(b.rows) for b in steps), 4096)
+    batch = steps[2]
+    st = Stepper(dm_e, dm_g, kv_e, kv_g, batch, ws, paged_e.n_seq)
+    ms = st.time(args.steps, args.warmup)
+    log(f"{args.steps} steps, {ms:.3f} ms/step")
+    prof = st.profile(args.steps)
+    res = summarize(cfg_g, batch, True, ms, prof, args.steps, "two-models-32l")
+    config = {"workload": TWO_MODELS.format(nq=len(batch.chunks), te=batch.n_emb_tokens, d=len(batch.rows)),
+              "embed_tokens": batch.n_emb_tokens, "decode_tokens": len(batch.rows), "layers": layers,
+              "models": 2}
+    sweep = []
+    for f, b in zip((0.0, 0.25, 0.5, 0.75, 1.0), steps):
+        t = Stepper(dm_e, dm_g, kv_e, kv_g, b, ws, paged_e.n_seq).time(max(3, args.steps // 4), 2)
+        sweep.append({"embedding_fraction": f, "embed_tokens": b.n_emb_tokens, "decode_rows": len(b.rows),
+                      "ms_per_step": t, "tokens_per_s": b.n_tokens / (t * 1e-3)})
+    res["sweep"] = sweep
+    res["sweep_tokens_per_s"] = sum(b.n_tokens for b in steps) / (sum(s["ms_per_step"] for s in sweep) * 1e-3)
+    if not args.no_cpu_baseline:
+        from workload import DeviceKVRecipe
+        rec_g = DeviceKVRecipe(paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
+        res["cpu_baseline"] = cpu_baseline_two_models(W_e, W_g, kv_g, batch, rec_g, args.cpu_threads)
+    del st, ws, kv_e, kv_g, dm_e, dm_g, W_e, W_g
+    torch.cuda.empty_cache()
+    return config, res
+
+
+def layer7b_bench(args, with_cpu: bool) -> dict:
+    """The one-7B-layer mixed step (device-drawn weights and caches) with a decode-only pass."""
+    import torch
+    from paper_2609_25405_amd import runtime as R
+    from workload import Batch, layer7b_mixed_workload
+    wl = layer7b_mixed_workload(with_pools=False, weights={})
+    cfg, batch = wl.cfg, wl.batch
+    dm, W = device_model(cfg, 1002, 0)
+    kv = device_kv(cfg, wl.kv.n_pages, wl.kv.n_seq, wl.kv.max_blocks, wl.kv.block_table, 1002)
+    ws = R.Workspace(dm, dm, batch.n_tokens, len(batch.chunks), len(batch.rows), 4096)
+    st = Stepper(dm, dm, kv, kv, batch, ws, wl.kv.n_seq, acc_w0=wl.acc_w)
+    ms = st.time(args.steps, args.warmup)
+    res = summarize(cfg, batch, False, ms, st.profile(args.steps), args.steps, "7b-layer-mixed")
+    # the decode rows alone: HBM figure of the decode attention without the chunk tiles
+    dec = Batch([], batch.rows, batch.token_ids[batch.n_emb_tokens:])
+    sd = Stepper(dm, dm, kv, kv, dec, ws, wl.kv.n_seq)
+    sd.time(3, 3)
+    n_a, tot_a = sd.profile(20)["attention"]
+    gbs = decode_kv_bytes(cfg, dec) / (tot_a / n_a * 1e-3) / 1e9
+    res["attention_decode_only"] = {"avg_ms": tot_a / n_a, "gbs": gbs, "frac_hbm": gbs / PEAK_HBM_GBS}
+    config = {"workload": LAYER7B, "embed_tokens": batch.n_emb_tokens, "decode_tokens": len(batch.rows), "layers": 1}
+    if with_cpu and not args.no_cpu_baseline:
+        from workload import make_weights
+        wl_host = layer7b_mixed_workload()
+        res["cpu_baseline"] = cpu_baseline_step(wl_host, args.cpu_threads)
+    del st, sd, ws, kv, dm, W
+    torch.cuda.empty_cache()
+    return config, res
+
+
+def line(args, config: dict, res: dict, steps: int, warmup: int) -> dict:
+    out = {"metric": METRIC, "value": res.pop("value"), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": res.pop("ms_per_step"), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": DATA, "config": config}
+    out.update(res)
+    return out
 
 
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="headline only (no one-layer figures)")
     ap.add_argument("--cpu-threads", type=int, default=0, help="BLAS threads for the oracle (0 = all)")
-    ap.add_argument("--workload", default="7b-layer-mixed",
-                    choices=["7b-layer-mixed", "retrieval-sweep-32l", "long-docs-32l", "decode-heavy-32l",
-                             "serving-32l"],
-                    help="7b-layer-mixed (default): the headline one-layer step with roofline and CPU "
-                         "baseline.  The others run the full 32-layer configurations on device-drawn "
-                         "weights and caches: two models over an embedding-fraction sweep, 16 documents "
-                         "of 8192 tokens chunked by 512 next to 32 decode rows, and 256 decode rows at "
-                         "contexts 4096-8192 next to 8 short queries")
+    ap.add_argument("--workload", default="two-models-32l",
+                    choices=["two-models-32l", "7b-layer-mixed", "long-docs-32l", "decode-heavy-32l", "serving-32l"],
+                    help="two-models-32l (default): both 32-layer models at embedding fraction 0.5, with the "
+                         "fraction sweep and the one-layer step as extra keys.  7b-layer-mixed: one 7B layer, "
+                         "1024 chunk tokens + 64 decode rows.  long-docs-32l: 16 documents of 8192 tokens "
+                         "chunked by 512 next to 32 decode rows.  decode-heavy-32l: 256 decode rows at contexts "
+                         "4096-8192 next to 8 short queries.  serving-32l: the scheduler and runner")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three plain 1 GiB device copies (the reference kernel for scaling "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -155,271 +538,71 @@ def main() -> int:
               "(independent replicas per GPU; no collective in the method). Use --gpus 1.",
               file=sys.stderr)
         return 2
-    if args.workload != "7b-layer-mixed":
-        print(json.dumps(full_model_bench(args)), flush=True)
-        return 0
-
-    import numpy as np
-    import torch
-
-    from paper_2609_25405_amd import runtime as R
-    from workload import layer7b_mixed_workload
-
-    t0 = time.time()
-    wl = layer7b_mixed_workload()
-    cfg, batch = wl.cfg, wl.batch
-    print(f"[bench] workload built in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
-    dm = R.DeviceModel(cfg, wl.weights)
-    kv = R.DeviceKV.from_paged(wl.kv)
-    acc_sum = torch.tensor(wl.acc_sum, device="cuda")
-    acc_w0 = torch.tensor(wl.acc_w, device="cuda")
-    acc_w = acc_w0.clone()
-    D, nc = len(batch.rows), len(batch.chunks)
-    logits = torch.empty((D, cfg.vocab), device="cuda")
-    out_emb = torch.empty((nc, cfg.d_model), device="cuda")
-    ws = R.Workspace(dm, dm, batch.n_tokens, nc, D, 4096)
-    packed = R.PackedBatch(batch)
-
-    def one_step():
-        acc_w.copy_(acc_w0)
-        R.step(dm, dm, batch, kv, kv, acc_sum, acc_w, logits, out_emb, ws, packed=packed)
-
-    for _ in range(args.warmup):
-        one_step()
-    torch.cuda.synchronize()
-    assert ws.device_error() == 0, "device error during warmup"
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        one_step()
-    end.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
-    assert ws.device_error() == 0, "device error during timed steps"
-    print(f"[bench] {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
-
-    # per-kernel times: HIP events around each launch, on the step's stream
-    R.profile_begin(dm)
-    for _ in range(args.steps):
-        one_step()
-    prof = R.profile_end(dm)
-    torch.cuda.synchronize()
-    work = algorithmic_work(cfg, batch)
-    kernels = {}
-    for name, (n, tot) in prof.items():
-        avg = tot / max(n, 1)
-        ent = {"launches_per_step": n / args.steps, "avg_ms": avg}
-        if name in work:
-            kind, amount, per_step = work[name]
-            per_launch = amount * per_step / (n / args.steps)
-            if kind == "flop":
-                ent["tflops"] = per_launch / (avg * 1e-3) / 1e12
-                ent["frac_mfma"] = ent["tflops"] / PEAK_BF16_TFLOPS
-            else:
-                ent["gbs"] = per_launch / (avg * 1e-3) / 1e9
-                ent["frac_hbm"] = ent["gbs"] / PEAK_HBM_GBS
-        kernels[name] = ent
-    dom = max(prof, key=lambda k: prof[k][1])
-    dk = kernels[dom]
-    kind, amount, per_step = work.get(dom, ("flop", 0.0, 1))
-    per_launch = amount * per_step / max(dk["launches_per_step"], 1e-9)
-    if kind == "flop":
-        roof = {"kernel": dom, "bound": "mfma", "achieved": dk.get("tflops"), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": dk.get("frac_mfma"), "traffic": measured_traffic(dom),
-                "algorithmic_per_launch": per_launch, "avg_launch_ms": dk["avg_ms"]}
+    if args.workload == "two-models-32l":
+        config, res = two_models_bench(args)
+        out = line(args, config, res, args.steps, args.warmup)
+        if not args.no_extras:
+            c7, r7 = layer7b_bench(args, with_cpu=False)
+            out["layer7b"] = dict(config=c7, **r7)
+    elif args.workload == "7b-layer-mixed":
+        config, res = layer7b_bench(args, with_cpu=True)
+        out = line(args, config, res, args.steps, args.warmup)
     else:
-        roof = {"kernel": dom, "bound": "hbm", "achieved": dk.get("gbs"), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": dk.get("frac_hbm"), "traffic": None,
-                "algorithmic_per_launch": per_launch, "avg_launch_ms": dk["avg_ms"]}
-    gemm_names = ["gemm_qkv", "gemm_qkv_rope", "gemm_o", "gemm_gate_up", "gemm_down", "lm_head"]
-    gemm_flop = sum(work[k][1] * work[k][2] for k in gemm_names if k in prof)
-    gemm_ms = sum(prof[k][1] for k in gemm_names if k in prof) / args.steps
-    attn_ms = prof.get("attention", (0, 0.0))[1] / args.steps
-    Te, T = batch.n_emb_tokens, batch.n_tokens
-    result = {
-        "metric": METRIC,
-        "value": T / (ms * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) bf16 KV, uniform token ids)",
-        "config": {"workload": "7b-layer-mixed-2048: 1 layer d4096 32q/8kv x128 ffn14336 vocab32000 bf16; "
-                               "2 chunks x512 (offsets 0 and 1536, last-token pooling) + 64 decode rows "
-                               "ctx U[1024,4096], page 16",
-                   "embed_tokens": Te, "decode_tokens": D, "layers": cfg.n_layers},
-        "embed_tokens_per_s": Te / (ms * 1e-3),
-        "decode_tokens_per_s": D / (ms * 1e-3),
-        "gemm_frac_mfma": gemm_flop / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS if gemm_ms else None,
-        "attention_frac_hbm": kernels.get("attention", {}).get("frac_hbm"),
-        "roofline": roof,
-        "kernels": kernels,
-    }
-    ideal_ms, frac = step_roofline(cfg, batch, ms)
-    result["step_roofline"] = {"ideal_ms": ideal_ms, "frac": frac,
-                               "definition": "sum over kernel classes of max(algorithmic flops / 2.5 PFLOP/s, "
-                                             "least HBM bytes / 8 TB/s), divided by the measured step time"}
-    # the decode rows alone (no chunk tiles in the attention launch): HBM figure of the decode
-    # attention without the chunk tiles that share its CUs in the mixed step
-    from workload import Batch
-    dec_batch = Batch([], batch.rows, batch.token_ids[Te:])
-    dec_packed = R.PackedBatch(dec_batch)
-    for _ in range(3):
-        R.step(dm, dm, dec_batch, kv, kv, acc_sum, acc_w, logits, out_emb, ws, packed=dec_packed)
-    R.profile_begin(dm)
-    for _ in range(20):
-        R.step(dm, dm, dec_batch, kv, kv, acc_sum, acc_w, logits, out_emb, ws, packed=dec_packed)
-    prof_dec = R.profile_end(dm)
-    torch.cuda.synchronize()
-    assert ws.device_error() == 0, "device error during the decode-only pass"
-    n_a, tot_a = prof_dec["attention"]
-    dec_bytes = algorithmic_work(cfg, dec_batch)["attention"][1]
-    result["attention_decode_only"] = {"avg_ms": tot_a / n_a, "gbs": dec_bytes / (tot_a / n_a * 1e-3) / 1e9,
-                                       "frac_hbm": dec_bytes / (tot_a / n_a * 1e-3) / 1e9 / PEAK_HBM_GBS}
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
-    print(json.dumps(result), flush=True)
+        out = full_model_bench(args)
+    print(json.dumps(out), flush=True)
     return 0
 
 
 def full_model_bench(args) -> dict:
-    """The 32-layer configurations: seeded weights and caches drawn on the device (their host
-    images would not fit), batches from the workload module's scenario generators.  Parity at
-    these sizes is covered by the one-layer tests of the same kernels; no CPU baseline here (the
-    float64 oracle would take hours per step)."""
-    import numpy as np
+    """The other 32-layer configurations, on weights and caches drawn on the device."""
     import torch
-
     from paper_2609_25405_amd import runtime as R
-    from workload import (decode_heavy_scenario, device_weights, fill_device_pools, llm7b_config,
-                          long_document_scenario, retrieval_mix_scenario)
+    from workload import decode_heavy_scenario, llm7b_config, long_document_scenario
 
     L = 32
-
-    def log(msg):
-        print(f"[bench] {msg}", file=sys.stderr, flush=True)
-
-    def device_kv(cfg, n_pages, n_seq, max_blocks, block_table, seed):
-        need = 2 * cfg.n_layers * n_pages * cfg.n_kv_heads * cfg.page_size * cfg.head_dim * 2
-        free = torch.cuda.mem_get_info()[0]
-        if need > 0.9 * free:
-            raise SystemExit(f"cache of {need / 2**30:.1f} GiB does not fit ({free / 2**30:.1f} GiB free)")
-        kv = R.DeviceKV(cfg, n_pages, n_seq, max_blocks, fill=0.0)
-        kv.set_block_table(block_table)
-        fill_device_pools(kv.k, kv.v, seed)
-        torch.cuda.synchronize()
-        log(f"cache {need / 2**30:.1f} GiB drawn")
-        return kv
-
-    def model(cfg, seed, tag):
-        W = device_weights(cfg, seed, tag)
-        torch.cuda.synchronize()
-        dm = R.DeviceModel(cfg, W)
-        del W
-        log(f"model (tag {tag}) drawn: {cfg.n_layers} layers")
-        return dm
-
-    def time_steps(dm_e, dm_g, kv_e, kv_g, batches, ws, n_seq_e, repeat):
-        """Each batch run `repeat` times back to back (a repeated step rewrites the same cache
-        slots and restarts its offset-0 chunks, so every repetition is a valid step)."""
-        acc_sum = torch.zeros((n_seq_e, dm_e.cfg.d_model), device="cuda")
-        acc_w = torch.zeros(n_seq_e, device="cuda")
-        D_max = max(b.n_logit_rows for b in batches)
-        logits = torch.empty((max(1, D_max), dm_g.cfg.vocab), device="cuda")
-        out_emb = torch.empty((max(1, max(len(b.chunks) for b in batches)), dm_e.cfg.d_model), device="cuda")
-        packed = [R.PackedBatch(b) for b in batches]
-        times = []
-        for b, pb in zip(batches, packed):
-            st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            st.record()
-            for _ in range(repeat):
-                R.step(dm_e, dm_g, b, kv_e, kv_g, acc_sum, acc_w, logits, out_emb, ws, packed=pb)
-            en.record()
-            torch.cuda.synchronize()
-            times.append(st.elapsed_time(en) / repeat)
-        assert ws.device_error() == 0, "device error"
-        return times
-
-    def attention_gbs(dm, kv_e, kv_g, batch, ws, n_seq_e):
-        acc_sum = torch.zeros((n_seq_e, dm.cfg.d_model), device="cuda")
-        acc_w = torch.zeros(n_seq_e, device="cuda")
-        logits = torch.empty((max(1, batch.n_logit_rows), dm.cfg.vocab), device="cuda")
-        out_emb = torch.empty((max(1, len(batch.chunks)), dm.cfg.d_model), device="cuda")
-        R.profile_begin(dm)
-        R.step(dm, dm, batch, kv_e, kv_g, acc_sum, acc_w, logits, out_emb, ws)
-        prof = R.profile_end(dm)
-        n, tot = prof["attention"]
-        per_launch = algorithmic_work(dm.cfg, batch)["attention"][1]
-        return per_launch / (tot / n * 1e-3) / 1e9, {k: round(v[1] / v[0] * 1e3, 1) for k, v in prof.items()}
-
-    rep = max(1, args.steps // 4)
     base = {"metric": METRIC, "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True,
-            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-            "data": "synthetic (seeded N(0,0.02) weights and N(0,1) bf16 caches drawn on the device, "
-                    "uniform token ids)"}
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": DATA}
     if args.workload == "decode-heavy-32l":
         _, _, batch, rec = decode_heavy_scenario(n_layers=1)
         cfg = llm7b_config(n_layers=L)
-        dm = model(cfg, rec.seed, 0)
+        dm, _ = device_model(cfg, rec.seed, 0)
         kv = device_kv(cfg, rec.n_pages, rec.n_seq, rec.max_blocks, rec.block_table, rec.seed)
         ws = R.Workspace(dm, dm, batch.n_tokens, len(batch.chunks), len(batch.rows), 8192)
-        time_steps(dm, dm, kv, kv, [batch], ws, rec.n_seq, 2)
-        (ms,) = time_steps(dm, dm, kv, kv, [batch], ws, rec.n_seq, rep)
-        gbs, kern = attention_gbs(dm, kv, kv, batch, ws, rec.n_seq)
-        Te, D = batch.n_emb_tokens, len(batch.rows)
-        return dict(base, value=(Te + D) / (ms * 1e-3), steps=rep, warmup=2, ms_per_step=ms,
-                    config={"workload": "decode-heavy-32l: 32 layers 7B shape bf16 vocab 32000; 256 decode "
-                                        "rows ctx U[4096,8192] + 8 queries x16 tokens (mean pooling), page 16",
-                            "embed_tokens": Te, "decode_tokens": D, "layers": L},
-                    embed_tokens_per_s=Te / (ms * 1e-3), decode_tokens_per_s=D / (ms * 1e-3),
-                    attention_gbs=gbs, attention_frac_hbm=gbs / PEAK_HBM_GBS, kernel_avg_us=kern)
-    if args.workload == "retrieval-sweep-32l":
-        cfg_e1, _, cfg_g1, _, paged_e, paged_g, steps = retrieval_mix_scenario(n_layers=1)
-        cfg_e, cfg_g = llm7b_config(n_layers=L, has_lm_head=False), llm7b_config(n_layers=L)
-        dm_e, dm_g = model(cfg_e, 1003, 1), model(cfg_g, 1003, 2)
-        kv_e = device_kv(cfg_e, paged_e.n_pages, paged_e.n_seq, paged_e.max_blocks, paged_e.block_table, 1)
-        kv_g = device_kv(cfg_g, paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
-        ws = R.Workspace(dm_e, dm_g, max(b.n_tokens for b in steps), max(1, max(len(b.chunks) for b in steps)),
-                         max(len(b.rows) for b in steps), 4096)
-        time_steps(dm_e, dm_g, kv_e, kv_g, steps, ws, paged_e.n_seq, 1)
-        times = time_steps(dm_e, dm_g, kv_e, kv_g, steps, ws, paged_e.n_seq, rep)
-        sweep = []
-        for f, b, t in zip((0.0, 0.25, 0.5, 0.75, 1.0), steps, times):
-            sweep.append({"embedding_fraction": f, "embed_tokens": b.n_emb_tokens, "decode_rows": len(b.rows),
-                          "ms_per_step": t, "tokens_per_s": (b.n_emb_tokens + len(b.rows)) / (t * 1e-3)})
-        tok = sum(b.n_emb_tokens + len(b.rows) for b in steps)
-        ms = sum(times) / len(times)
-        return dict(base, value=tok / (sum(times) * 1e-3), steps=rep * len(steps), warmup=len(steps),
-                    ms_per_step=ms,
-                    config={"workload": "retrieval-sweep-32l: two 32-layer 7B-shape models (embedding: mean "
-                                        "pooling, no LM head; generator: vocab 32000), 2048-token budget, "
-                                        "embedding fraction 0/.25/.5/.75/1, queries lognormal mean 64, up to "
-                                        "256 decode rows with contexts lognormal mean 512",
-                            "layers": L},
-                    embed_tokens_per_s=sum(b.n_emb_tokens for b in steps) / (sum(times) * 1e-3),
-                    decode_tokens_per_s=sum(len(b.rows) for b in steps) / (sum(times) * 1e-3),
-                    sweep=sweep)
+        st = Stepper(dm, dm, kv, kv, batch, ws, rec.n_seq)
+        steps = max(1, args.steps // 4)
+        ms = st.time(steps, 2)
+        res = summarize(cfg, batch, False, ms, st.profile(steps), steps, "decode-heavy-32l")
+        config = {"workload": "decode-heavy-32l: 32 layers 7B shape bf16 vocab 32000; 256 decode rows ctx "
+                              "U[4096,8192] + 8 queries x16 tokens (mean pooling), page 16",
+                  "embed_tokens": batch.n_emb_tokens, "decode_tokens": len(batch.rows), "layers": L}
+        return dict(base, steps=steps, warmup=2, config=config, **res)
     if args.workload == "serving-32l":
-        return serving_bench(args, model, log, L)
-    # long documents
+        return serving_bench(args, L)
+    # long documents: every step once, in order (each chunk's keys are written by earlier steps)
     _, _, paged, steps = long_document_scenario(n_layers=1, n_docs=16, doc_len=8192, chunk=512, per_step=3,
                                                 n_dec=32, ctx0=2048)
     cfg = llm7b_config(n_layers=L)
-    dm = model(cfg, 1004, 0)
+    dm, _ = device_model(cfg, 1004, 0)
     kv = device_kv(cfg, paged.n_pages, paged.n_seq, paged.max_blocks, paged.block_table, 4)
     ws = R.Workspace(dm, dm, max(b.n_tokens for b in steps), 3, 32, paged.max_blocks * 16)
-    time_steps(dm, dm, kv, kv, steps[:1], ws, paged.n_seq, 2)
-    times = time_steps(dm, dm, kv, kv, steps, ws, paged.n_seq, 1)
+    acc_sum = torch.zeros((paged.n_seq, cfg.d_model), device="cuda")
+    acc_w = torch.zeros(paged.n_seq, device="cuda")
+    logits = torch.empty((32, cfg.vocab), device="cuda")
+    out_emb = torch.empty((3, cfg.d_model), device="cuda")
+    packed = [R.PackedBatch(b) for b in steps]
+    times = []
+    for b, pb in zip(steps, packed):
+        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        st.record()
+        R.step(dm, dm, b, kv, kv, acc_sum, acc_w, logits, out_emb, ws, packed=pb)
+        en.record()
+        torch.cuda.synchronize()
+        times.append(st.elapsed_time(en))
+    assert ws.device_error() == 0, "device error"
     Te = sum(b.n_emb_tokens for b in steps)
     D = sum(len(b.rows) for b in steps)
     tsum = sum(times) * 1e-3
-    return dict(base, value=(Te + D) / tsum, steps=len(steps), warmup=2, ms_per_step=sum(times) / len(times),
+    return dict(base, value=(Te + D) / tsum, steps=len(steps), warmup=0, ms_per_step=sum(times) / len(times),
                 config={"workload": "long-docs-32l: 32 layers 7B shape bf16 vocab 32000; 16 documents x8192 "
                                     "tokens chunked by 512 (mean pooling), 3 chunks per step, + 32 decode rows "
                                     "from context 2048", "layers": L, "steps": len(steps)},
@@ -427,7 +610,7 @@ def full_model_bench(args) -> dict:
                 ms_per_step_first_last=[times[0], times[-1]])
 
 
-def serving_bench(args, model, log, L: int) -> dict:
+def serving_bench(args, L: int) -> dict:
     """The serving loop on the GPU: the native intra-batch scheduler and the runner (schedule,
     step, sample, commit; one host synchronisation per iteration) serve a closed set of
     requests to completion on a 32-layer 7B-shape model.  Value: every token the model processed
@@ -441,7 +624,7 @@ def serving_bench(args, model, log, L: int) -> dict:
     from workload import llm7b_config
 
     cfg = llm7b_config(n_layers=L)
-    dm = model(cfg, 1005, 0)
+    dm, _ = device_model(cfg, 1005, 0)
     rng = np.random.default_rng(1005)
     n_emb, n_gen, prompt, new = 384, 96, 512, 128
     sigma = 0.6
@@ -515,32 +698,6 @@ def serving_bench(args, model, log, L: int) -> dict:
             "decode_only_iterations": int(sum(f * budget <= n_gen for f in fills)),
             "decode_only_ms_mean": float(np.mean([t for t, f in zip(iter_s, fills) if f * budget <= n_gen]
                                                  or [0])) * 1e3}
-
-
-def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):
-    """The float64 oracle on the same step (decode rows and both chunks), host cores, repeated
-    until about `min_seconds` of CPU work (a bounded sample: whole steps of the same batch)."""
-    import numpy as np
-    from oracle import OracleKV, step_oracle
-    from workload import as_float64
-    n = threads or len(os.sched_getaffinity(0))
-    try:
-        from threadpoolctl import threadpool_limits
-        lim = threadpool_limits(limits=n)
-    except Exception:
-        lim = None
-    okv = OracleKV.from_paged(wl.kv)
-    W64 = as_float64(wl.weights)   # one-time upcast, like loading, outside the timed calls
-    reps, t0 = 0, time.time()
-    while reps == 0 or time.time() - t0 < min_seconds:
-        # the decode rows rewrite their own slots, so repeating the step is a valid step
-        step_oracle((wl.cfg, W64), (wl.cfg, W64), wl.batch, okv, okv, wl.acc_sum, wl.acc_w)
-        reps += 1
-    dt = (time.time() - t0) / reps
-    T = wl.batch.n_tokens
-    return {"value": T / dt, "unit": "tokens/s", "cores": n, "kind": "oracle",
-            "sample": f"{reps} full steps of the same workload ({T} tokens each), float64 NumPy, "
-                      f"{dt:.2f} s per step"}
 
 
 if __name__ == "__main__":

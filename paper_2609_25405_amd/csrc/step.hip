@@ -131,7 +131,7 @@ struct Prof {
     hipEvent_t a = nullptr;
     int id = -1;
     bool on() const { return m && m->profiling; }
-    int begin(const char *name) {
+    int begin(const std::string &name) {
         if (!on()) return ORTHRUS_OK;
         std::lock_guard<std::mutex> lk(m->mu);
         id = -1;
@@ -322,7 +322,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 
     hipStream_t s = (hipStream_t)stream;
     Prof prof{const_cast<orthrus_model *>(emb), s};
-    auto timed = [&](hipStream_t st, const char *name, auto &&launch) -> int {
+    auto timed = [&](hipStream_t st, const std::string &name, auto &&launch) -> int {
         prof.s = st;
         int r = prof.begin(name);
         if (r) return r;
@@ -335,10 +335,11 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
         const int r_ = timed(s, name, [&]() { return (expr); });    \
         if (r_) return r_;                                          \
     } while (0)
-#define RUNG(g, name, expr)                                         \
-    do {                                                            \
-        const int r_ = timed((g).st, name, [&]() { return (expr); }); \
-        if (r_) return r_;                                          \
+#define RUNG(g, name, expr)                                                                   \
+    do {                                                                                      \
+        const int r_ = timed((g).st, prof.on() ? std::string(name) + (g).tag : std::string(), \
+                             [&]() { return (expr); });                                       \
+        if (r_) return r_;                                                                    \
     } while (0)
     char *ws = (char *)workspace;
     int *err = (int *)(ws + L.err);
@@ -360,13 +361,14 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 
     // row groups: [0, Te) through the embedding model, [Te, T) (prompt chunks, then decode rows)
     // through the generator
-    struct Group { const orthrus_model *m; int r0, r1; hipStream_t st; };
+    // (profiled launches of the generator's group carry the tag "@gen" in their names)
+    struct Group { const orthrus_model *m; int r0, r1; hipStream_t st; const char *tag; };
     Group groups[2];
     int n_groups = 0;
-    if (one_model) groups[n_groups++] = {emb, 0, T, s};
+    if (one_model) groups[n_groups++] = {emb, 0, T, s, ""};
     else {
-        if (Te > 0) groups[n_groups++] = {emb, 0, Te, s};
-        if (T > Te) groups[n_groups++] = {gen, Te, T, s};
+        if (Te > 0) groups[n_groups++] = {emb, 0, Te, s, ""};
+        if (T > Te) groups[n_groups++] = {gen, Te, T, s, "@gen"};
     }
     // Two row groups touch disjoint rows, weights and cache slots between one attention launch
     // and the next, so the second group's launches run on the handle's auxiliary stream,

@@ -211,11 +211,12 @@ def test_layer7b_decode_batches_up_to_192_rows(n_dec):
     print(pair.report, flush=True)
 
 
-@pytest.mark.parametrize("n_dec", [64, 128])
+@pytest.mark.parametrize("n_dec", [33, 47, 64, 128])
 def test_blocked_lm_head_gives_the_same_logits(n_dec):
     """The LM head read from its 64 x 64 blocked copy (the default for bf16 models) and from the
     row-major weights give bit-identical logits (same tiles, same arithmetic); a vocabulary that
-    is not a multiple of 64 exercises the zero-padded last row block."""
+    is not a multiple of 64 exercises the zero-padded last row block, and 33 or 47 rows a partly
+    filled row tile of the 64 x 128 tiles that serve 33..64 rows."""
     cfg = ModelConfig(n_layers=1, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128, d_ff=1024,
                       vocab=4000 + 37, dtype="bf16")
     W = make_weights(cfg, 71)

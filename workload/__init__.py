@@ -368,16 +368,16 @@ class StepWorkload:
 
 
 def layer7b_mixed_workload(seed: int = 1002, with_pools: bool = True,
-                           weights: Optional[Dict] = None) -> StepWorkload:
-    """One 7B-shape layer (bf16, vocab 32000 LM head), 2048-token budget mixed step.
+                           weights: Optional[Dict] = None, n_layers: int = 1) -> StepWorkload:
+    """7B-shape layers (one by default; bf16, vocab 32000 LM head), 2048-token budget mixed step.
 
     Two embedding requests contribute 1024 chunk tokens (chunk 512, last-token
     pooling): request 0 is at offset 0 (first chunk, not last), request 1 at
     offset 1536 (its final chunk, after 1536 tokens already cached).  64 decode
     rows have contexts drawn uniformly from [1024, 4096].  Cached keys/values
-    are N(0, 1) in bf16.
+    are N(0, 1) in bf16 in every layer.
     """
-    cfg = llm7b_config(n_layers=1)
+    cfg = llm7b_config(n_layers=n_layers)
     if weights is None:
         weights = make_weights(cfg, seed)
     rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(91,)))
