@@ -248,6 +248,26 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
                  float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the same step as orthrus_step() with the workspace
+ * replaced by library-owned scratch, a static device array of ORTHRUS_SCRATCH_BYTES that every
+ * GPU the library runs on holds until the process ends.  It calls no hipMalloc, hipFree,
+ * hipHostMalloc or other allocating routine and creates no stream or event: the step's metadata
+ * is copied from host memory with hipMemcpyAsync on `stream`, the two row groups of a two-model
+ * step run one after the other on `stream`, and kernel timing (orthrus_profile_begin) does not
+ * apply.  Results are identical to orthrus_step()'s.
+ *   device_error: device int32 or NULL; once the stream has synchronised it holds this step's
+ *     device error bits (ORTHRUS_DEVERR_*, 0 = none).  Every call starts with no bits set.
+ * ECAPACITY when the batch needs more workspace than ORTHRUS_SCRATCH_BYTES (orthrus_workspace_bytes
+ * with this batch's sizes tells in advance; nothing is enqueued then); otherwise the return codes
+ * of orthrus_step().  All calls on one GPU share its scratch, which keeps the last call's
+ * contents: calls that overlap on one GPU (several streams or host threads) race and corrupt each
+ * other's results, so serialise them. */
+#define ORTHRUS_SCRATCH_BYTES (64u << 20)
+int orthrus_step_noalloc(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                         const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
+                         float *out_logits, float *out_emb, int32_t *device_error, void *stream);
+
 /* Greedy sampling (the sampler of Algorithm 1): out_tokens[r] = argmax over v of
  * logits[r * vocab + v] for r < rows, enqueued on `stream`.  Ties go to the lowest index; a NaN
  * counts as larger than every number (the first NaN wins), so the result equals a first-maximum

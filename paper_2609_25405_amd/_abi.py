@@ -21,6 +21,7 @@ ORTHRUS_ECAPACITY = -4
 ORTHRUS_EUNSUPPORTED = -5
 ORTHRUS_EHIP = -6
 ORTHRUS_EDEVICE = -7
+ORTHRUS_SCRATCH_BYTES = 64 << 20
 ORTHRUS_F32 = 0
 ORTHRUS_BF16 = 1
 ORTHRUS_CHUNK_LAST = 1
@@ -140,6 +141,9 @@ SIGNATURES = {
                              c_void_p, c_size_t, c_void_p]),
     "orthrus_sample_greedy": (c_int, [c_void_p, c_int32, c_int32, c_void_p, c_void_p]),
     "orthrus_workspace_init": (c_int, [c_void_p, c_void_p]),
+    "orthrus_step_noalloc": (c_int, [c_void_p, c_void_p, POINTER(orthrus_batch), POINTER(orthrus_kv),
+                                     POINTER(orthrus_kv), c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_void_p]),
     "orthrus_device_error": (c_int, [c_void_p, c_void_p, POINTER(c_int32)]),
     "orthrus_plan": (c_int, [c_void_p, c_void_p, POINTER(orthrus_batch), POINTER(orthrus_kv),
                              POINTER(orthrus_kv), POINTER(c_int32), POINTER(c_int32),
@@ -225,6 +229,12 @@ def orthrus_sample_greedy(logits, rows, vocab, out_tokens, stream):
 
 def orthrus_workspace_init(workspace, stream):
     return load().orthrus_workspace_init(workspace, stream)
+
+
+def orthrus_step_noalloc(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits, out_emb,
+                         device_error, stream):
+    return load().orthrus_step_noalloc(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits,
+                                       out_emb, device_error, stream)
 
 
 def orthrus_device_error(workspace, stream, bits):

@@ -303,9 +303,18 @@ int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthr
     return ORTHRUS_OK;
 }
 
-int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
-                 const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
-                 float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace orthrus {
+namespace {
+
+// One step (the body of orthrus_step).  no_alloc (orthrus_step_noalloc): the metadata is copied
+// with hipMemcpyAsync from host memory together with a zero error word, both row groups run on
+// `stream` (no auxiliary stream, no events) and kernel timing is off, so nothing is allocated
+// or created.
+int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+              const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
+              float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream, bool no_alloc) {
     if (!emb || !gen || !batch || !workspace || !kv_ok(emb_kv, emb) || !kv_ok(gen_kv, gen)) return ORTHRUS_EINVAL;
     if (gen != emb && !same_shape(emb->cfg, gen->cfg)) return ORTHRUS_EUNSUPPORTED;
     if (batch->n_chunks > 0 && (!acc_sum || !acc_w || !out_emb)) return ORTHRUS_EINVAL;
@@ -321,7 +330,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     if (ws_bytes < L.total) return ORTHRUS_ECAPACITY;
 
     hipStream_t s = (hipStream_t)stream;
-    Prof prof{const_cast<orthrus_model *>(emb), s};
+    Prof prof{no_alloc ? nullptr : const_cast<orthrus_model *>(emb), s};
     auto timed = [&](hipStream_t st, const std::string &name, auto &&launch) -> int {
         prof.s = st;
         int r = prof.begin(name);
@@ -344,8 +353,17 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     char *ws = (char *)workspace;
     int *err = (int *)(ws + L.err);
     const int32_t *meta = (const int32_t *)(ws + L.meta);
-    rc = upload_meta(const_cast<orthrus_model *>(emb), p, ws + L.meta, s);
-    if (rc) return rc;
+    if (no_alloc) {
+        // [error word region (zeros) | metadata] in one copy: every call starts with no error bits
+        static_assert(sizeof(int32_t) == 4, "int32 metadata");
+        std::vector<int32_t> head(kAlign / 4 + p.meta.size(), 0);
+        std::memcpy(head.data() + kAlign / 4, p.meta.data(), p.meta.size() * 4);
+        if (L.meta != L.err + kAlign) return ORTHRUS_EHIP;
+        HIP_TRY(hipMemcpyAsync(ws + L.err, head.data(), head.size() * 4, hipMemcpyHostToDevice, s));
+    } else {
+        rc = upload_meta(const_cast<orthrus_model *>(emb), p, ws + L.meta, s);
+        if (rc) return rc;
+    }
 
     const int dt = c.dtype;
     const size_t es = dt == ORTHRUS_BF16 ? 2 : 4;
@@ -375,7 +393,7 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
     // concurrently with the first's: forked after the plan upload and after each attention
     // launch, joined before each launch over all rows (measured on the two-model retrieval steps)
     orthrus_model *mh = const_cast<orthrus_model *>(emb);
-    const bool concurrent = n_groups == 2;
+    const bool concurrent = n_groups == 2 && !no_alloc;
     std::unique_lock<std::mutex> step_lock(mh->step_mu, std::defer_lock);
     if (concurrent) {
         step_lock.lock();
@@ -744,6 +762,61 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
 #undef RUN
 #undef RUNG
 #undef SYNC_GROUPS
+}
+
+// Scratch of orthrus_step_noalloc: a file-scope device array, one per device (zero at load).  In
+// host code `scratch` names a host-side stand-in; its device address comes from
+// hipGetSymbolAddress, taken once per device with that device current and kept in scratch_dev.
+constexpr size_t kScratchBytes = ORTHRUS_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_dev[kMaxDevices] = {};
+
+// the current device's scratch address, or nullptr on a HIP failure
+void *scratch_address() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(scratch_mu);
+    if (!scratch_dev[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+        scratch_dev[dev] = ptr;
+    }
+    return scratch_dev[dev];
+}
+
+// hands the step's error bits to the caller's word and clears the scratch copy
+__global__ void error_out_kernel(int *err, int *out) {
+    if (threadIdx.x == 0) {
+        if (out) out[0] = err[0];
+        err[0] = 0;
+    }
+}
+
+}  // namespace
+}  // namespace orthrus
+
+extern "C" {
+
+int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                 const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
+                 float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream) {
+    return step_impl(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits, out_emb, workspace, ws_bytes,
+                     stream, false);
+}
+
+int orthrus_step_noalloc(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
+                         const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
+                         float *out_logits, float *out_emb, int32_t *device_error, void *stream) {
+    if (!emb || !gen || !batch) return ORTHRUS_EINVAL;
+    void *ws = scratch_address();
+    if (!ws) return ORTHRUS_EHIP;
+    const int rc = step_impl(emb, gen, batch, emb_kv, gen_kv, acc_sum, acc_w, out_logits, out_emb, ws,
+                             kScratchBytes, stream, true);
+    if (rc) return rc;
+    hipLaunchKernelGGL(error_out_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, (int *)ws, (int *)device_error);
+    return hipGetLastError() == hipSuccess ? ORTHRUS_OK : ORTHRUS_EHIP;
 }
 
 int orthrus_profile_begin(orthrus_model *m) {

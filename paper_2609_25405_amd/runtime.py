@@ -280,6 +280,20 @@ def step(emb: DeviceModel, gen: DeviceModel, batch, emb_kv: DeviceKV, gen_kv: De
     _check(rc, "orthrus_step")
 
 
+def step_noalloc(emb: DeviceModel, gen: DeviceModel, batch, emb_kv: DeviceKV, gen_kv: DeviceKV,
+                 acc_sum: torch.Tensor, acc_w: torch.Tensor, out_logits: Optional[torch.Tensor],
+                 out_emb: Optional[torch.Tensor], device_error: Optional[torch.Tensor] = None,
+                 stream: Optional[int] = None) -> int:
+    """Enqueue one orthrus_step_noalloc (library-owned scratch instead of a workspace); returns
+    the status code (0 or a negative ORTHRUS_E* value) without raising.  ``device_error``: int32
+    [1] device tensor that receives the step's device error bits."""
+    pb = PackedBatch(batch)
+    ekv, gkv = emb_kv.struct(), (emb_kv.struct() if gen_kv is emb_kv else gen_kv.struct())
+    s = current_stream() if stream is None else stream
+    return A.orthrus_step_noalloc(emb.handle, gen.handle, byref(pb.c), byref(ekv), byref(gkv), _vp(acc_sum),
+                                  _vp(acc_w), _vp(out_logits), _vp(out_emb), _vp(device_error), c_void_p(s))
+
+
 def sample_greedy(logits: torch.Tensor, out_tokens: torch.Tensor,
                   stream: Optional[int] = None) -> None:
     """Enqueue orthrus_sample_greedy on fp32 logits [rows][vocab] into int32 out_tokens [rows]."""
