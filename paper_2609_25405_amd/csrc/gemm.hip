@@ -529,7 +529,10 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //    workgroups) with a 4-deep copy ring keep enough bytes in flight per CU (LM head
 //    64 x 32000 x 4096: 70 -> 43 us with warm caches; decode-batch QKV 35 -> 25 us); gate/up
 //    on 64x128 tiles (224 workgroups instead of 112: 58.6 -> 43.9 us with cold weights);
-//  - gate/up: 192x256 tiles over 8 waves;
+//  - gate/up above 896 rows: 192x256 or 256x256 tiles over 8 waves, whichever needs fewer
+//    rounds of workgroups times tile rows;
+//  - gate/up of 129..256 rows: one 256x128 row tile, the weights streamed once (non-temporal)
+//    through 3-deep rings (M = 256 with cold weights: 110 -> 71 us against 128x128 tiles);
 //  - residual-add projections of M > 896 rows: 256x256 tiles over 8 waves with the split-K
 //    count gemm_add_splits picks (o 58 -> 46 us, down 177 -> 135 us against 128x128 tiles at
 //    M = 1088; down at M = 1568 264 -> 195 us, at M = 2048 275 -> 211 us against 192x256
@@ -545,11 +548,10 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //  - split-K residual-add projections of 128 < M <= 256: 128x128 tiles with 4-deep rings (one
 //    workgroup per CU; down at M = 192 57.1 -> 45.7 us, o at M = 256 27.1 -> 21.8 us); above 256
 //    rows two 64 KiB workgroups per CU win again (down at M = 384: 71 against 86 us);
-//  - gate/up of 128 < M <= 896, measured on the 7B shape with cold weights: 128x128 up to
-//    M = 256 (192x256 tiles would leave most CUs idle: M = 192 75 against 97 us); above, 192x256
-//    when 128x128 tiles need more than the 512 slots of one round and 192x256 tiles fit in
-//    one (M = 640: 172 against 195 us), else the tile that pads M least (M = 384 98 against
-//    130 us, M = 512 147 against 174 us, M = 896 240 against 256 us).
+//  - gate/up of 256 < M <= 896, measured on the 7B shape with cold weights: 192x256 when
+//    128x128 tiles need more than the 512 slots of one round and 192x256 tiles fit in one
+//    (M = 640: 172 against 195 us), else the tile that pads M least (M = 384 98 against 130 us,
+//    M = 512 147 against 174 us, M = 896 240 against 256 us).
 template <int EPI>
 hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
     if constexpr (EPI == EPI_QKV_ROPE) {
@@ -559,10 +561,18 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
     } else if constexpr (EPI == EPI_SWIGLU) {
         if (a.M <= 64) return run_bf16<64, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
         if (a.M <= 128) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
-        if (a.M <= 256) return run_bf16<128, 128, 2, 2, EPI>(a, s);
+        if (a.M <= 256) return run_bf16<256, 128, 4, 2, EPI, 64, 3, 3, true>(a, s);
+        if (a.M > 896) {
+            // the row tile whose rounds of workgroups over 256 CUs cost least, a round costing
+            // its tile's rows (M = 1024: 256x256 tiles, two rounds, 211 against 242 us)
+            const long t192 = (long)((a.M + 191) / 192) * ((a.N + 127) / 128);
+            const long t256 = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
+            if ((t256 + 255) / 256 * 256 < (t192 + 255) / 256 * 192) return run_bf16<256, 256, 2, 4, EPI>(a, s);
+            return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        }
         const int pad128 = (a.M + 127) / 128 * 128 - a.M, pad192 = (a.M + 191) / 192 * 192 - a.M;
         const int w128 = (a.M + 127) / 128 * ((a.N + 127) / 128), w192 = (a.M + 191) / 192 * ((a.N + 255) / 256);
-        if (a.M > 896 || (w128 > 512 && w192 <= 256) || pad192 <= pad128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
+        if ((w128 > 512 && w192 <= 256) || pad192 <= pad128) return run_bf16<192, 256, 2, 4, EPI>(a, s);
         return run_bf16<128, 128, 2, 2, EPI>(a, s);
     } else {
         // the blocked LM head of 33..64 rows: 64x128 tiles (16 KB runs per stage) 49.5 -> 46.9 us

@@ -29,20 +29,25 @@ struct Layout {
 };
 // split-K slabs of one residual-add projection: at most kMaxSplits fp32 [T][d] slabs
 constexpr int kMaxSplits = 4;
-// QKV projections of at most kQkvSplitRows rows per model split K in two (bf16 path): their fp32
-// partial sums [2][T][qkv_dim] get a region of qkv_slab_rows(T) rows (two such groups).
+// QKV projections of at most kQkvSplitRows rows per model, or of more than kQkvSplitMinRows and
+// at most kQkvFusedMaxRows, split K in two (bf16 path): their fp32 partial sums [2][T][qkv_dim]
+// get a region of qkv_slab_rows(T) rows, which the rotation/append kernel sums in split order.
 // Measured on the 7B shape at 64 rows: the split projection and the rotation kernel take
 // 18.6 + 6.9 us against 42.6 us fused (48 whole-head tiles); 8 splits 22.1 + 10.3 us; at 96
 // rows 23.9 + 8.2 us against 44.0 us, at 128 rows 25.8 + 8.4 against 45.1 us; at 384 rows the
-// fused projection is faster (54.5 us against 46.2 + 15.4 us with 4 splits)
+// fused projection is faster (54.5 us against 46.2 + 15.4 us with 4 splits).  At 1024 rows the
+// split projection on 256x256 tiles (192 workgroups) takes 58 us against 79 us for the 128x128
+// whole-head tiles before their fused epilogue (90 us with it in the two-model step)
 constexpr int kQkvSplitRows = 128;
+constexpr int kQkvSplitMinRows = 896;
 constexpr int kQkvSplits = 2;
 // QKV projections of more than kQkvFusedMaxRows rows per model (bf16 path) store fp32 rows
 // from one round of 192x256 or 256x256 tiles and rotate them in the row kernel: whole-head
 // 128x128 tiles with the fused epilogue need more than one round there (7B shape: 1568 rows
 // 138 us fused against 86 + ~12 us; 2048 rows 173 us against 104 + ~15 us)
 constexpr int kQkvFusedMaxRows = 1280;
-size_t qkv_slab_rows(size_t T) { return (size_t)kQkvSplits * std::min<size_t>(T, 2 * kQkvSplitRows); }
+size_t qkv_slab_rows(size_t T) { return (size_t)kQkvSplits * std::min<size_t>(T, 2 * kQkvFusedMaxRows); }
+bool qkv_split_rows(int rows) { return rows <= kQkvSplitRows || (rows > kQkvSplitMinRows && rows <= kQkvFusedMaxRows); }
 
 Layout make_layout(const Model &m, size_t T, size_t meta_ints, size_t n_partials) {
     const size_t es = m.cfg.dtype == ORTHRUS_BF16 ? 2 : 4;
@@ -598,7 +603,7 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
         // small bf16 projections (decode-only batches) stream their weights, and whole-head tiles
         // for the fused rotation leave too few workgroups (48 at 64 rows): they split K into fp32
         // partials, which the rotation/append row kernel sums in split order
-        const int qkv_splits = dt == ORTHRUS_BF16 && max_rows <= kQkvSplitRows && d % (kQkvSplits * 64) == 0 &&
+        const int qkv_splits = dt == ORTHRUS_BF16 && qkv_split_rows(max_rows) && d % (kQkvSplits * 64) == 0 &&
                                        d / kQkvSplits >= 512 && (size_t)kQkvSplits * T <= qkv_slab_rows(T)
                                    ? kQkvSplits
                                    : 1;
