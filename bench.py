@@ -118,14 +118,25 @@ def launch_work(cfg, batch, two_models: bool):
         work["gemm_o" + tag] = (2.0 * M * qd * d, qd * d * es + M * qd * es + 2 * M * d * 4)
         work["gemm_gate_up" + tag] = (2.0 * M * d * 2 * F, 2 * F * d * es + M * d * es + M * F * es)
         work["gemm_down" + tag] = (2.0 * M * F * d, F * d * es + M * F * es + 2 * M * d * 4)
-    pairs = sum(sum(c.offset + i + 1 for i in range(c.len)) for c in batch.chunks)
-    pairs += sum(sum(c.offset + i + 1 for i in range(c.len)) for c in (getattr(batch, "gen_chunks", None) or []))
-    dec_keys = sum(r.ctx_len + 1 for r in batch.rows)
-    chunk_keys = sum(c.offset + c.len for c in batch.chunks)
-    chunk_keys += sum(c.offset + c.len for c in (getattr(batch, "gen_chunks", None) or []))
     kv_per_key = 2 * kvd * es
-    work["attention"] = (4.0 * (pairs + dec_keys) * cfg.head_dim * cfg.n_q_heads,
-                         (dec_keys + chunk_keys) * kv_per_key + 2 * T * qd * es)
+
+    def attention(chunks, rows, n_tok):
+        pairs = sum(sum(c.offset + i + 1 for i in range(c.len)) for c in chunks)
+        dec_keys = sum(r.ctx_len + 1 for r in rows)
+        chunk_keys = sum(c.offset + c.len for c in chunks)
+        return (4.0 * (pairs + dec_keys) * cfg.head_dim * cfg.n_q_heads,
+                (dec_keys + chunk_keys) * kv_per_key + 2 * n_tok * qd * es)
+
+    gen_chunks = list(getattr(batch, "gen_chunks", None) or [])
+    if two_models:
+        # one attention launch per model: the embedding chunks; the prompt chunks and decode rows
+        Te = batch.n_emb_tokens
+        work["attention"] = attention(batch.chunks, [], Te)
+        work["attention@gen"] = attention(gen_chunks, batch.rows, T - Te)
+        work["rope_append@gen"] = (0.0, 0.0)
+        work["attn_combine@gen"] = (0.0, 0.0)
+    else:
+        work["attention"] = attention(list(batch.chunks) + gen_chunks, batch.rows, T)
     work["rope_append"] = (0.0, 0.0)
     work["attn_combine"] = (0.0, 0.0)
     n_lm = batch.n_logit_rows
@@ -181,7 +192,7 @@ def summarize(cfg, batch, two_models: bool, ms: float, prof: dict, steps: int, w
             else:
                 b_h += e["algorithmic_bytes"] * e["launches_per_step"]
                 t_h += t
-    attn = kernels.get("attention")
+    attn = kernels.get("attention@gen" if two_models else "attention")
     res = {
         "ms_per_step": ms,
         "value": T / (ms * 1e-3),
@@ -191,7 +202,7 @@ def summarize(cfg, batch, two_models: bool, ms: float, prof: dict, steps: int, w
         "gemm_hbm_bound_frac_hbm": b_h / (t_h * 1e-3) / 1e9 / PEAK_HBM_GBS if t_h else None,
         "attention_frac_hbm": (decode_kv_bytes(cfg, batch) / (attn["avg_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS
                                if attn and batch.rows else None),
-        "attention_roofline_frac": attn.get("frac") if attn else None,
+        "attention_roofline_frac": attn.get("frac") if attn else None,   # the decode rows' launch
     }
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches_per_step"])
     dk = kernels[dom]

@@ -304,8 +304,8 @@ int orthrus_plan(const orthrus_model *emb, const orthrus_model *gen, const orthr
  * stream around each kernel launch.  orthrus_profile_end() synchronises those events and writes
  * up to `cap` entries (one per kernel name, in first-launch order) with the launch count and the
  * summed event time; *n_out receives the number of names.  In a step of two distinct models the
- * launches over the generator's rows are named with the suffix "@gen" (e.g. "gemm_o@gen"), those
- * over the embedding model's rows and those over all rows (attention) without it.  Returns EHIP on a runtime failure. */
+ * launches over the generator's rows (prompt chunks and decode rows, attention included) are named
+ * with the suffix "@gen" (e.g. "attention@gen"), those over the embedding model's rows without it.  Returns EHIP on a runtime failure. */
 typedef struct orthrus_kernel_time {
     char name[32];
     int32_t launches;

@@ -204,6 +204,20 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
         }
         std::stable_sort(pre.begin(), pre.end(), [](const Pre &a, const Pre &b2) { return a.work > b2.work; });
     }
+    // two distinct models: the embedding chunks' items and merge entries first (heaviest first
+    // within each model), so each model's rows can be served by a launch of their own
+    if (&emb != &gen) {
+        const int n_emb_chunks = b.n_chunks;
+        const auto emb_item = [n_emb_chunks](const Pre &t) { return t.chunk < n_emb_chunks; };
+        p.n_pre_emb = (int)(std::stable_partition(pre.begin(), pre.end(), emb_item) - pre.begin());
+        const int te = p.Te;
+        p.n_merge_emb = (int)(std::stable_partition(merges.begin(), merges.end(),
+                                                    [te](const Merge &m) { return m.tok < te; }) -
+                              merges.begin());
+    } else {
+        p.n_pre_emb = (int)pre.size();
+        p.n_merge_emb = (int)merges.size();
+    }
     p.n_prefill = (int)pre.size();
     p.n_split_prefill = (int)merges.size();
 

@@ -64,6 +64,10 @@ struct StepPlan {
     bool shared_kv = true;
     int n_prefill = 0, n_decode_items = 0, n_partials = 0, n_split_rows = 0;
     int n_split_prefill = 0;  // prefill items cut along keys (merge entries at off_combine)
+    // two distinct models: the first n_pre_emb prefill items and the first n_merge_emb merge
+    // entries belong to embedding chunks (the embedding model's rows), the rest to generation
+    // prefill chunks; each model's rows then get attention launches of their own
+    int n_pre_emb = 0, n_merge_emb = 0;
     int n_lm = 0;  // rows that get logits: last rows of final prompt chunks, then decode rows
     // heads in the batch that need every embedding row's final norm (mean, weighted mean,
     // buffered), and the optional per-token arrays they read

@@ -393,10 +393,10 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
         if (Te > 0) groups[n_groups++] = {emb, 0, Te, s, ""};
         if (T > Te) groups[n_groups++] = {gen, Te, T, s, "@gen"};
     }
-    // Two row groups touch disjoint rows, weights and cache slots between one attention launch
-    // and the next, so the second group's launches run on the handle's auxiliary stream,
-    // concurrently with the first's: forked after the plan upload and after each attention
-    // launch, joined before each launch over all rows (measured on the two-model retrieval steps)
+    // Two row groups touch disjoint rows, weights and cache slots through every layer, so the
+    // second group's launches run on the handle's auxiliary stream, concurrently with the
+    // first's: forked after the plan upload, joined before the final norm (measured on the
+    // two-model retrieval steps)
     orthrus_model *mh = const_cast<orthrus_model *>(emb);
     const bool concurrent = n_groups == 2 && !no_alloc;
     std::unique_lock<std::mutex> step_lock(mh->step_mu, std::defer_lock);
@@ -589,6 +589,37 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
     }
     const size_t e_stride = layer_stride(M, *emb_kv), g_stride = layer_stride(M, *gen_kv);
     const int qd = M.q_dim(), qkvd = M.qkv_dim(), F = c.d_ff;
+    // Two row groups (two models) never share a row, a work item or a cache slot: each group's
+    // rotation/append, attention and merge run on the group's stream over its own rows, the
+    // planner's items of its chunks (and, for the generator, the decode rows) and its merge
+    // entries, so the groups' layer chains proceed independently
+    auto rope_group = [&](const Group &g) -> hipError_t {
+        RopeArgs r = ra;
+        r.qkv = ra.qkv + (size_t)g.r0 * qkvd;
+        r.cs = ra.cs ? ra.cs + (size_t)g.r0 * (c.head_dim / 2) : nullptr;
+        r.q_out = qb + (size_t)g.r0 * qd * es;
+        r.pos = ra.pos + g.r0;
+        r.seq = ra.seq + g.r0;
+        r.T = g.r1 - g.r0;
+        r.Te = std::max(0, std::min(Te - g.r0, r.T));
+        return launch_rope_append(dt, r, g.st);
+    };
+    const int merges_gen = p.n_split_prefill - p.n_merge_emb;
+    auto attn_group = [&](int gi, bool combine) -> hipError_t {
+        AttnArgs ag = aa;
+        int n_dec = 0;
+        if (gi == 0) {
+            ag.n_items = p.n_pre_emb;
+            ag.n_combine = p.n_merge_emb;
+        } else {
+            ag.items = aa.items + kItemInts * p.n_pre_emb;
+            ag.n_items = aa.n_items - p.n_pre_emb;
+            ag.combine = aa.combine + kCombineInts * p.n_merge_emb;
+            ag.n_combine = merges_gen;
+            n_dec = p.n_split_rows > 0 ? p.D : 0;
+        }
+        return combine ? launch_attn_combine(dt, ag, n_dec, groups[gi].st) : launch_attention(dt, ag, groups[gi].st);
+    };
 
     for (int l = 0; l < c.n_layers; ++l) {
         if (l > 0) {
@@ -627,8 +658,11 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
             }
             ra.nslab = qkv_splits;
             ra.slab_stride = (size_t)T * qkvd;
-            SYNC_GROUPS(join());
-            RUN("rope_append", launch_rope_append(dt, ra, s));
+            if (n_groups == 2) {
+                for (int gi = 0; gi < n_groups; ++gi) RUNG(groups[gi], "rope_append", rope_group(groups[gi]));
+            } else {
+                RUN("rope_append", launch_rope_append(dt, ra, s));
+            }
         } else if (dt == ORTHRUS_BF16 && max_rows <= kQkvFusedMaxRows) {
             // QKV projection with rotation and cache append in its epilogue
             for (int gi = 0; gi < n_groups; ++gi) {
@@ -671,18 +705,26 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
                 RUNG(groups[gi], "gemm_qkv", gemm(EPI_STORE_F32, groups[gi], act, d, lw.w_qkv, nullptr, qkv, qkvd, 4, qkvd, d, lg));
             }
             ra.nslab = 1;
-            SYNC_GROUPS(join());
-            RUN("rope_append", launch_rope_append(dt, ra, s));
+            if (n_groups == 2) {
+                for (int gi = 0; gi < n_groups; ++gi) RUNG(groups[gi], "rope_append", rope_group(groups[gi]));
+            } else {
+                RUN("rope_append", launch_rope_append(dt, ra, s));
+            }
         }
         for (int i = 0; i < 2; ++i) {
             aa.k_cache[i] = ra.k_cache[i];
             aa.v_cache[i] = ra.v_cache[i];
         }
-        SYNC_GROUPS(join());
-        RUN("attention", launch_attention(dt, aa, s));
-        if (p.n_split_rows > 0 || p.n_split_prefill > 0)
-            RUN("attn_combine", launch_attn_combine(dt, aa, p.n_split_rows > 0 ? p.D : 0, s));
-        SYNC_GROUPS(fork());
+        if (n_groups == 2) {
+            RUNG(groups[0], "attention", attn_group(0, false));
+            if (p.n_merge_emb > 0) RUNG(groups[0], "attn_combine", attn_group(0, true));
+            RUNG(groups[1], "attention", attn_group(1, false));
+            if (p.n_split_rows > 0 || merges_gen > 0) RUNG(groups[1], "attn_combine", attn_group(1, true));
+        } else {
+            RUN("attention", launch_attention(dt, aa, s));
+            if (p.n_split_rows > 0 || p.n_split_prefill > 0)
+                RUN("attn_combine", launch_attn_combine(dt, aa, p.n_split_rows > 0 ? p.D : 0, s));
+        }
         int splits = add_splits(qd);
         for (int gi = 0; gi < n_groups; ++gi) {
             const orthrus_layer_weights &lw = groups[gi].m->layers[l];
