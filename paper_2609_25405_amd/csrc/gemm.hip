@@ -582,6 +582,9 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
         const bool split = EPI == EPI_ADD_F32 && a.partial && a.splits > 1;
         if (split && a.M <= 128) return run_bf16<128, 64, 2, 2, EPI, 64, 4, 4, true>(a, s);
         if (EPI != EPI_ADD_F32 && a.M <= 128) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, true>(a, s);
+        // stored rows of 129..256 (the LM head of up to 256 decode rows): one 256-row tile, the
+        // weights streamed once
+        if (EPI == EPI_STORE_F32 && a.M <= 256) return run_bf16<256, 128, 4, 2, EPI, 64, 3, 3, true>(a, s);
         if (split && a.M <= 256) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, false>(a, s);
         if (split && a.M <= 896) return run_bf16<128, 128, 2, 2, EPI>(a, s);
         if (EPI == EPI_ADD_F32 && a.partial && a.M > 896) return run_bf16<256, 256, 2, 4, EPI>(a, s);

@@ -211,7 +211,7 @@ def test_layer7b_decode_batches_up_to_192_rows(n_dec):
     print(pair.report, flush=True)
 
 
-@pytest.mark.parametrize("n_dec", [33, 47, 64, 128])
+@pytest.mark.parametrize("n_dec", [33, 47, 64, 128, 200])
 def test_blocked_lm_head_gives_the_same_logits(n_dec):
     """The LM head read from its 64 x 64 blocked copy (the default for bf16 models) and from the
     row-major weights give bit-identical logits (same tiles, same arithmetic); a vocabulary that
