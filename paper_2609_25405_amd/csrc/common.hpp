@@ -100,6 +100,10 @@ struct GemmArgs {
     // B0 in the 64 x 64 blocked layout ([ceil(N/64)][K/64][64][64]; bf16 path, not SwiGLU):
     // one tile stage reads whole 8 KB runs instead of 128-byte pieces of 64 rows
     int b_blocked;
+    // 1: the launch runs concurrently with another stream's launches, so the workgroup time it
+    // takes from the shared CUs, not its own length, is what it costs; the bf16 dispatch then
+    // gives split-K projections of 129..256 rows the largest tiles
+    int wide;
 };
 hipError_t launch_gemm(int dtype, int epilogue, const GemmArgs &a, hipStream_t s);
 // bf16 [rows][cols] -> the 64 x 64 blocked layout GemmArgs::b_blocked reads (cols % 64 == 0)

@@ -547,7 +547,12 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //    down split 4 ways on 128x64 tiles 38.8 -> 32.7 us (M = 96, cold weights);
 //  - split-K residual-add projections of 128 < M <= 256: 128x128 tiles with 4-deep rings (one
 //    workgroup per CU; down at M = 192 57.1 -> 45.7 us, o at M = 256 27.1 -> 21.8 us); above 256
-//    rows two 64 KiB workgroups per CU win again (down at M = 384: 71 against 86 us);
+//    rows two 64 KiB workgroups per CU win again (down at M = 384: 71 against 86 us).  Run
+//    concurrently with another stream (GemmArgs::wide), the same projections take 256x256
+//    tiles: 4x fewer workgroup-microseconds per flop at a longer launch, which the other
+//    stream's launches fill (the two-model 32-layer step, QKV, o and down of the generator's
+//    256 decode rows so tiled: 23.4 -> 22.5 ms and 23.9 -> 23.2 ms on two GPUs; gate/up so
+//    tiled as well measured slower than neither);
 //  - gate/up of 256 < M <= 896, measured on the 7B shape with cold weights: 192x256 when
 //    128x128 tiles need more than the 512 slots of one round and 192x256 tiles fit in one
 //    (M = 640: 172 against 195 us), else the tile that pads M least (M = 384 98 against 130 us,
@@ -585,6 +590,7 @@ hipError_t dispatch_bf16(const GemmArgs &a, hipStream_t s) {
         // stored rows of 129..256 (the LM head of up to 256 decode rows): one 256-row tile, the
         // weights streamed once
         if (EPI == EPI_STORE_F32 && a.M <= 256) return run_bf16<256, 128, 4, 2, EPI, 64, 3, 3, true>(a, s);
+        if (split && a.wide && a.M > 128 && a.M <= 256) return run_bf16<256, 256, 2, 4, EPI>(a, s);
         if (split && a.M <= 256) return run_bf16<128, 128, 2, 2, EPI, 64, 4, 4, false>(a, s);
         if (split && a.M <= 896) return run_bf16<128, 128, 2, 2, EPI>(a, s);
         if (EPI == EPI_ADD_F32 && a.partial && a.M > 896) return run_bf16<256, 256, 2, 4, EPI>(a, s);

@@ -532,6 +532,7 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
         ga.partial = slabs ? slabs + (size_t)g.r0 * d : nullptr;  // the group's rows of each slab
         ga.split_stride = slab_stride;
         ga.lora = lg;
+        ga.wide = concurrent;
         return launch_gemm(dt, EPI_ADD_F32, ga, g.st);
     };
 
@@ -653,6 +654,7 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
                 ga.splits = qkv_splits;
                 ga.partial = qkv + (size_t)g.r0 * qkvd;
                 ga.split_stride = (size_t)T * qkvd;
+                ga.wide = concurrent;
                 if (lora_on(0, g)) RUNG(g, "lora_shrink", lora(0, l, g, act, d, d, ga.lora));
                 RUNG(g, "gemm_qkv", launch_gemm(dt, EPI_ADD_F32, ga, g.st));
             }
