@@ -313,6 +313,11 @@ typedef struct orthrus_kernel_time {
 } orthrus_kernel_time;
 int orthrus_profile_begin(orthrus_model *m);
 int orthrus_profile_end(orthrus_model *m, orthrus_kernel_time *out, int32_t cap, int32_t *n_out);
+/* Limits the launches that profiling windows of `m` time to those named `name` (the names
+ * orthrus_profile_end reports; NULL or "" = every launch, the initial state), so that a window can
+ * time one kernel inside steps otherwise run as usual: two events per named launch instead of two
+ * per launch.  Stays in effect until changed; EINVAL for a null model. */
+int orthrus_profile_only(orthrus_model *m, const char *name);
 
 const char *orthrus_strerror(int code);
 

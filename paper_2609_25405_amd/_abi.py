@@ -149,6 +149,7 @@ SIGNATURES = {
                              POINTER(orthrus_kv), POINTER(c_int32), POINTER(c_int32),
                              POINTER(c_int32), c_int32]),
     "orthrus_profile_begin": (c_int, [c_void_p]),
+    "orthrus_profile_only": (c_int, [c_void_p, c_char_p]),
     "orthrus_profile_end": (c_int, [c_void_p, POINTER(orthrus_kernel_time), c_int32,
                                     POINTER(c_int32)]),
     "orthrus_strerror": (c_char_p, [c_int]),
@@ -247,6 +248,10 @@ def orthrus_plan(emb, gen, batch, emb_kv, gen_kv, n_prefill, n_decode, items, ca
 
 def orthrus_profile_begin(model):
     return load().orthrus_profile_begin(model)
+
+
+def orthrus_profile_only(model, name):
+    return load().orthrus_profile_only(model, name)
 
 
 def orthrus_profile_end(model, out, cap, n_out):

@@ -23,13 +23,15 @@ struct orthrus_model : public orthrus::Model {
     hipEvent_t ev[2] = {nullptr, nullptr};
     int next = 0;
     // steps with two row groups (two models) run the generator group's launches on `aux`
-    // (default priority), forked from and joined to the step's stream around each attention
-    // launch; step_mu serialises the host side of such steps on this handle
+    // (default priority), forked from the step's stream after the plan upload and joined to it
+    // before the final norm; step_mu serialises the host side of such steps on this handle
     hipStream_t aux = nullptr;
     hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     std::mutex step_mu;
-    // kernel timing (orthrus_profile_begin / _end)
+    // kernel timing (orthrus_profile_begin / _end); prof_only (orthrus_profile_only) limits the
+    // timed launches to one name, empty = all
     bool profiling = false;
+    std::string prof_only;
     struct Mark { int name; hipEvent_t a, b; };
     std::vector<std::string> prof_names;
     std::vector<Mark> marks;

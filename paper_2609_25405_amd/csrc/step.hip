@@ -139,6 +139,10 @@ struct Prof {
     int begin(const std::string &name) {
         if (!on()) return ORTHRUS_OK;
         std::lock_guard<std::mutex> lk(m->mu);
+        if (!m->prof_only.empty() && name != m->prof_only) {
+            id = -2;   // not timed in this window
+            return ORTHRUS_OK;
+        }
         id = -1;
         for (size_t i = 0; i < m->prof_names.size(); ++i)
             if (m->prof_names[i] == name) id = (int)i;
@@ -151,7 +155,7 @@ struct Prof {
         return ORTHRUS_OK;
     }
     int end() {
-        if (!on()) return ORTHRUS_OK;
+        if (!on() || id == -2) return ORTHRUS_OK;
         hipEvent_t b = nullptr;
         HIP_TRY(hipEventCreate(&b));
         HIP_TRY(hipEventRecord(b, s));
@@ -872,6 +876,13 @@ int orthrus_profile_begin(orthrus_model *m) {
     if (!m) return ORTHRUS_EINVAL;
     std::lock_guard<std::mutex> lk(m->mu);
     m->profiling = true;
+    return ORTHRUS_OK;
+}
+
+int orthrus_profile_only(orthrus_model *m, const char *name) {
+    if (!m) return ORTHRUS_EINVAL;
+    std::lock_guard<std::mutex> lk(m->mu);
+    m->prof_only = name ? name : "";
     return ORTHRUS_OK;
 }
 

@@ -324,6 +324,11 @@ def profile_begin(model: DeviceModel) -> None:
     _check(A.orthrus_profile_begin(model.handle), "orthrus_profile_begin")
 
 
+def profile_only(model: DeviceModel, name: str | None) -> None:
+    """Time only the launches named `name` in later profiling windows (None: every launch)."""
+    _check(A.orthrus_profile_only(model.handle, (name or "").encode()), "orthrus_profile_only")
+
+
 def profile_end(model: DeviceModel):
     """{kernel name: (launches, total ms)} since profile_begin (synchronises the events)."""
     cap = 64

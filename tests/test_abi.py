@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = P.load()
     names = header_functions()
     assert [os.path.basename(h) for h in HEADERS] == ["orthrus.h", "orthrus_sched.h"]
-    assert len(names) == 15 + 12
+    assert len(names) == 16 + 12
     for n in names:
         assert hasattr(lib, n), n
         assert n in A.SIGNATURES, n
