@@ -20,7 +20,7 @@ shift how the two models' streams overlap) against its own roofline: algorithmic
 bf16 MFMA peak or algorithmic bytes against HBM peak, whichever bounds it.  `roofline` describes
 the kernel with the largest share of the step, timed by event pairs around its launches inside
 the timed steps (no events on any other launch there).  `cpu_baseline` times the float64 CPU oracle on a
-sample of the same step (see cpu_baseline_two_models).  Extra keys: the same two models over an
+sample of the same step (see cpu_baseline_sample).  Extra keys: the same two models over an
 embedding-fraction sweep (`sweep`), and the one-7B-layer mixed step (`layer7b`).
 """
 from __future__ import annotations
@@ -375,15 +375,18 @@ def host_layers(W, n_layers: int):
             "layers": [{k: f(v) for k, v in W["layers"][l].items()} for l in range(n_layers)]}
 
 
-def cpu_baseline_two_models(W_e, W_g, kv_g, batch, rec_g, threads: int, n_rows: int = 32) -> dict:
-    """The float64 oracle on a sample of the two-model step, extrapolated to the whole step.
+def cpu_baseline_sample(W_e, W_g, kv_g, batch, block_table, max_blocks: int, threads: int, n_rows: int = 32,
+                        layers: int = 32, emb_lm_head: bool = False) -> dict:
+    """The float64 oracle on a sample of a 32-layer step, extrapolated to the whole step.
 
-    Sample: every query (through the embedding model) and the first `n_rows` decode rows (through
-    the generator, keys and values copied from the device cache), each at 1 and at 2 layers of
-    the same device-drawn weights (copied to the host).  Per-layer time = t(2) - t(1); the 32-layer
-    time of each part is t(1) + 31 (t(2) - t(1)) (the LM head and the final norm counted once),
-    and the decode part is scaled by D / n_rows (the oracle runs each request alone).  An
-    extrapolation, stated as one in the result."""
+    Sample: every embedding chunk of the step (through the embedding model W_e, each run as one
+    final chunk at offset 0 over its own tokens) and the first `n_rows` decode rows (through the
+    generator W_g, keys and values copied from the device cache `kv_g` by `block_table`), each at
+    1 and at 2 layers of the same device-drawn weights (copied to the host).  Per-layer time =
+    t(2) - t(1); the whole-depth time of each part is t(1) + (layers - 1) (t(2) - t(1)) (the LM
+    head and the final norm counted once), and the decode part is scaled by D / n_rows (the
+    oracle runs each request alone).  With one model, W_e is W_g.  An extrapolation, stated as
+    one in the result."""
     import numpy as np
     import torch
     from oracle import OracleKV, step_oracle
@@ -396,15 +399,16 @@ def cpu_baseline_two_models(W_e, W_g, kv_g, batch, rec_g, threads: int, n_rows: 
     q = Batch([EmbChunk(i, 0, c.len, True, c.pool) for i, c in enumerate(batch.chunks)], [],
               batch.token_ids[:Te])
     r = Batch([], [DecodeRow(i, x.ctx_len) for i, x in enumerate(rows)], batch.token_ids[Te:Te + len(rows)])
-    pages = [rec_g.block_table[x.seq][rec_g.block_table[x.seq] >= 0] for x in rows]
+    pages = [block_table[x.seq][:-(-(x.ctx_len + 1) // P)] for x in rows]
     flat = torch.from_numpy(np.concatenate(pages).astype(np.int64)).to(kv_g.k.device)
-    bt = np.full((len(rows), rec_g.max_blocks), -1, np.int64)
+    bt = np.full((len(rows), max_blocks), -1, np.int64)
     o = 0
     for i, p in enumerate(pages):
         bt[i, :len(p)] = np.arange(o, o + len(p))
         o += len(p)
     q_pages = sum(-(-c.len // P) for c in batch.chunks)
-    q_bt = np.full((len(batch.chunks), 2048 // P + 1), -1, np.int64)
+    q_bt = np.full((len(batch.chunks), max(-(-c.len // P) for c in batch.chunks) if batch.chunks else 1), -1,
+                   np.int64)
     o = 0
     for i, c in enumerate(batch.chunks):
         k = -(-c.len // P)
@@ -412,33 +416,34 @@ def cpu_baseline_two_models(W_e, W_g, kv_g, batch, rec_g, threads: int, n_rows: 
         o += k
     times = {}
     for L in (1, 2):
-        cfg_e = llm7b_config(n_layers=L, has_lm_head=False)
+        cfg_e = llm7b_config(n_layers=L, has_lm_head=emb_lm_head)
         cfg_g = llm7b_config(n_layers=L)
-        We, Wg = host_layers(W_e, L), host_layers(W_g, L)
+        We = host_layers(W_e, L)
+        Wg = We if W_g is W_e else host_layers(W_g, L)
         k64 = kv_g.k[:L, flat].float().cpu().numpy().astype(np.float64)
         v64 = kv_g.v_by_position[:L, flat].float().cpu().numpy().astype(np.float64)
         okv_g = OracleKV(k64, v64, bt, P)
-        shape = (L, q_pages, cfg_e.n_kv_heads, P, cfg_e.head_dim)
+        shape = (L, max(q_pages, 1), cfg_e.n_kv_heads, P, cfg_e.head_dim)
         okv_e = OracleKV(np.zeros(shape), np.zeros(shape), q_bt, P)
+        n_q = max(1, len(batch.chunks))
         t0 = time.perf_counter()
-        step_oracle((cfg_e, We), (cfg_g, Wg), q, okv_e, okv_g, np.zeros((len(batch.chunks), cfg_e.d_model)),
-                    np.zeros(len(batch.chunks)))
+        if batch.chunks:
+            step_oracle((cfg_e, We), (cfg_g, Wg), q, okv_e, okv_g, np.zeros((n_q, cfg_e.d_model)), np.zeros(n_q))
         t1 = time.perf_counter()
-        step_oracle((cfg_e, We), (cfg_g, Wg), r, okv_e, okv_g, np.zeros((len(batch.chunks), cfg_e.d_model)),
-                    np.zeros(len(batch.chunks)))
+        step_oracle((cfg_e, We), (cfg_g, Wg), r, okv_e, okv_g, np.zeros((n_q, cfg_e.d_model)), np.zeros(n_q))
         t2 = time.perf_counter()
         times[L] = (t1 - t0, t2 - t1)
         del We, Wg, okv_g, okv_e, k64, v64
     (q1, r1), (q2, r2) = times[1], times[2]
-    t_q = q1 + 31 * (q2 - q1)
-    t_r = (r1 + 31 * (r2 - r1)) * D / len(rows)
+    t_q = q1 + (layers - 1) * (q2 - q1)
+    t_r = (r1 + (layers - 1) * (r2 - r1)) * D / len(rows)
     if lim is not None:
         lim.restore_original_limits()
     return {"value": (Te + D) / (t_q + t_r), "unit": "tokens/s", "cores": used, "kind": "oracle",
-            "sample": f"float64 oracle on the same step's {len(batch.chunks)} queries ({Te} tokens) and "
+            "sample": f"float64 oracle on the same step's {len(batch.chunks)} embedding chunks ({Te} tokens) and "
                       f"{len(rows)} of its {D} decode rows, each at 1 and 2 layers of the same weights "
-                      f"(queries {q1:.2f} / {q2:.2f} s, rows {r1:.2f} / {r2:.2f} s); extrapolated to 32 "
-                      f"layers as t1 + 31 (t2 - t1) and to all {D} rows: {t_q + t_r:.1f} s per step",
+                      f"(chunks {q1:.2f} / {q2:.2f} s, rows {r1:.2f} / {r2:.2f} s); extrapolated to {layers} "
+                      f"layers as t1 + {layers - 1} (t2 - t1) and to all {D} rows: {t_q + t_r:.1f} s per step",
             "extrapolated": True, **host_info()}
 
 
@@ -507,7 +512,8 @@ def two_models_bench(args, layers: int = 32) -> dict:
     if not args.no_cpu_baseline:
         from workload import DeviceKVRecipe
         rec_g = DeviceKVRecipe(paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
-        res["cpu_baseline"] = cpu_baseline_two_models(W_e, W_g, kv_g, batch, rec_g, args.cpu_threads)
+        res["cpu_baseline"] = cpu_baseline_sample(W_e, W_g, kv_g, batch, rec_g.block_table, rec_g.max_blocks,
+                                                  args.cpu_threads)
     del st, ws, kv_e, kv_g, dm_e, dm_g, W_e, W_g
     torch.cuda.empty_cache()
     return config, res
@@ -613,13 +619,17 @@ def full_model_bench(args) -> dict:
     if args.workload == "decode-heavy-32l":
         _, _, batch, rec = decode_heavy_scenario(n_layers=1)
         cfg = llm7b_config(n_layers=L)
-        dm, _ = device_model(cfg, rec.seed, 0)
+        dm, W = device_model(cfg, rec.seed, 0)
         kv = device_kv(cfg, rec.n_pages, rec.n_seq, rec.max_blocks, rec.block_table, rec.seed)
         ws = R.Workspace(dm, dm, batch.n_tokens, len(batch.chunks), len(batch.rows), 8192)
         st = Stepper(dm, dm, kv, kv, batch, ws, rec.n_seq)
         steps = max(1, args.steps // 4)
-        ms = st.time(steps, 2)
-        res = summarize(cfg, batch, False, ms, st.profile(steps), steps, "decode-heavy-32l")
+        dom = dominant_kernel(cfg, batch, False, st.profile(2), 2)
+        ms, (n_dom, t_dom) = st.time(steps, 0, only=dom)
+        res = summarize(cfg, batch, False, ms, st.profile(steps), steps, "decode-heavy-32l", (dom, n_dom, t_dom))
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = cpu_baseline_sample(W, W, kv, batch, rec.block_table, rec.max_blocks,
+                                                      args.cpu_threads, n_rows=16, emb_lm_head=True)
         config = {"workload": "decode-heavy-32l: 32 layers 7B shape bf16 vocab 32000; 256 decode rows ctx "
                               "U[4096,8192] + 8 queries x16 tokens (mean pooling), page 16",
                   "embed_tokens": batch.n_emb_tokens, "decode_tokens": len(batch.rows), "layers": L}
@@ -630,7 +640,7 @@ def full_model_bench(args) -> dict:
     _, _, paged, steps = long_document_scenario(n_layers=1, n_docs=16, doc_len=8192, chunk=512, per_step=3,
                                                 n_dec=32, ctx0=2048)
     cfg = llm7b_config(n_layers=L)
-    dm, _ = device_model(cfg, 1004, 0)
+    dm, W = device_model(cfg, 1004, 0)
     kv = device_kv(cfg, paged.n_pages, paged.n_seq, paged.max_blocks, paged.block_table, 4)
     ws = R.Workspace(dm, dm, max(b.n_tokens for b in steps), 3, 32, paged.max_blocks * 16)
     acc_sum = torch.zeros((paged.n_seq, cfg.d_model), device="cuda")
@@ -650,12 +660,18 @@ def full_model_bench(args) -> dict:
     Te = sum(b.n_emb_tokens for b in steps)
     D = sum(len(b.rows) for b in steps)
     tsum = sum(times) * 1e-3
-    return dict(base, value=(Te + D) / tsum, steps=len(steps), warmup=0, ms_per_step=sum(times) / len(times),
-                config={"workload": "long-docs-32l: 32 layers 7B shape bf16 vocab 32000; 16 documents x8192 "
-                                    "tokens chunked by 512 (mean pooling), 3 chunks per step, + 32 decode rows "
-                                    "from context 2048", "layers": L, "steps": len(steps)},
-                embed_tokens_per_s=Te / tsum, decode_tokens_per_s=D / tsum,
-                ms_per_step_first_last=[times[0], times[-1]])
+    out = dict(base, value=(Te + D) / tsum, steps=len(steps), warmup=0, ms_per_step=sum(times) / len(times),
+               config={"workload": "long-docs-32l: 32 layers 7B shape bf16 vocab 32000; 16 documents x8192 "
+                                   "tokens chunked by 512 (mean pooling), 3 chunks per step, + 32 decode rows "
+                                   "from context 2048", "layers": L, "steps": len(steps)},
+               embed_tokens_per_s=Te / tsum, decode_tokens_per_s=D / tsum,
+               ms_per_step_first_last=[times[0], times[-1]])
+    if not args.no_cpu_baseline:
+        # the first step: three 512-token chunks at offset 0 and the 32 decode rows (their keys and
+        # values from the cache as it was drawn; the decode rows' own slots rewritten since)
+        out["cpu_baseline"] = cpu_baseline_sample(W, W, kv, steps[0], paged.block_table, paged.max_blocks,
+                                                  args.cpu_threads, n_rows=8, emb_lm_head=True)
+    return out
 
 
 def serving_bench(args, L: int) -> dict:
