@@ -108,6 +108,29 @@ def test_noalloc_step_equals_workspace_step_two_models():
     run_both(dm_e, dm_g, pe, pg, [big, small], 4)
 
 
+def test_noalloc_two_models_wide_generator_group():
+    """A generator group of 129..256 decode rows beside the embedding rows: the two-stream step gives
+    that group's split-K projections 256x256 tiles, the allocation-free one-stream step 128x128;
+    each output element sums the same K stages in the same order either way, so bitwise equal."""
+    cfg = _cfg()
+    dm_e = R.DeviceModel(cfg, make_weights(cfg, 2305, model_tag=1, qk_std=0.06))
+    dm_g = R.DeviceModel(cfg, make_weights(cfg, 2305, model_tag=2, qk_std=0.06))
+    n_g = 200
+    pe = PagedKV(cfg, 64, 4, 16, 1)
+    pg = PagedKV(cfg, n_g * 8, n_g, 8, 2)
+    for s in range(4):
+        pe.reserve(s, 200)
+    ctx = [20 + (37 * s) % 90 for s in range(n_g)]
+    for s, c in enumerate(ctx):
+        pg.fill_random(s, c, 5)
+        pg.reserve(s, c + 2)
+    big = Batch([EmbChunk(0, 0, 180, True, "mean"), EmbChunk(1, 0, 120, False, "cls")],
+                [DecodeRow(s, ctx[s]) for s in range(n_g)], draw_tokens(2305, 3, 180 + 120 + n_g, 512))
+    small = Batch([EmbChunk(1, 120, 30, True, "cls")], [DecodeRow(s, ctx[s] + 1) for s in range(150)],
+                  draw_tokens(2305, 4, 30 + 150, 512))
+    run_both(dm_e, dm_g, pe, pg, [big, small], 4)
+
+
 def test_noalloc_error_bits_and_capacity():
     cfg = _cfg()
     dm = R.DeviceModel(cfg, make_weights(cfg, 2303))
