@@ -20,8 +20,10 @@ shift how the two models' streams overlap) against its own roofline: algorithmic
 bf16 MFMA peak or algorithmic bytes against HBM peak, whichever bounds it.  `roofline` describes
 the kernel with the largest share of the step, timed by event pairs around its launches inside
 the timed steps (no events on any other launch there).  `cpu_baseline` times the float64 CPU oracle on a
-sample of the same step (see cpu_baseline_sample).  Extra keys: the same two models over an
-embedding-fraction sweep (`sweep`), and the one-7B-layer mixed step (`layer7b`).
+sample of the same step (see cpu_baseline_sample), with its embedding and decode tokens/s and the
+GPU/CPU ratio.  Extra keys: the same two models over an embedding-fraction sweep (`sweep`), the
+one-7B-layer mixed step (`layer7b`), and a plain 1 GiB device copy's rate (`copy_ceiling`, a
+practical HBM ceiling, not a target).
 """
 from __future__ import annotations
 
@@ -440,6 +442,8 @@ def cpu_baseline_sample(W_e, W_g, kv_g, batch, block_table, max_blocks: int, thr
     if lim is not None:
         lim.restore_original_limits()
     return {"value": (Te + D) / (t_q + t_r), "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "embed_tokens_per_s": Te / (t_q + t_r), "decode_tokens_per_s": D / (t_q + t_r),
+            "seconds_per_step": t_q + t_r,
             "sample": f"float64 oracle on the same step's {len(batch.chunks)} embedding chunks ({Te} tokens) and "
                       f"{len(rows)} of its {D} decode rows, each at 1 and 2 layers of the same weights "
                       f"(chunks {q1:.2f} / {q2:.2f} s, rows {r1:.2f} / {r2:.2f} s); extrapolated to {layers} "
@@ -551,11 +555,34 @@ def layer7b_bench(args, with_cpu: bool) -> dict:
     return config, res
 
 
+def copy_ceiling() -> dict:
+    """A plain 1 GiB device-to-device copy (torch): read + written bytes per second, a practical
+    HBM ceiling reported beside the rooflines (not a target)."""
+    import torch
+    x = torch.ones(256 * 1024 * 1024, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    st.record()
+    for _ in range(10):
+        y.copy_(x)
+    en.record()
+    torch.cuda.synchronize()
+    ms = st.elapsed_time(en) / 10
+    del x, y
+    torch.cuda.empty_cache()
+    return {"gbs": 2 * (1 << 30) / (ms * 1e-3) / 1e9, "ms": ms, "what": "torch copy of 1 GiB: bytes read + written / time"}
+
+
 def line(args, config: dict, res: dict, steps: int, warmup: int) -> dict:
     out = {"metric": METRIC, "value": res.pop("value"), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
            "warmup": warmup, "ms_per_step": res.pop("ms_per_step"), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": DATA, "config": config}
     out.update(res)
+    cb = out.get("cpu_baseline")
+    if cb and cb.get("value"):
+        cb["gpu_over_cpu"] = out["value"] / cb["value"]
     return out
 
 
@@ -598,6 +625,7 @@ def main() -> int:
         if not args.no_extras:
             c7, r7 = layer7b_bench(args, with_cpu=False)
             out["layer7b"] = dict(config=c7, **r7)
+            out["copy_ceiling"] = copy_ceiling()
     elif args.workload == "7b-layer-mixed":
         config, res = layer7b_bench(args, with_cpu=True)
         out = line(args, config, res, args.steps, args.warmup)
@@ -630,6 +658,7 @@ def full_model_bench(args) -> dict:
         if not args.no_cpu_baseline:
             res["cpu_baseline"] = cpu_baseline_sample(W, W, kv, batch, rec.block_table, rec.max_blocks,
                                                       args.cpu_threads, n_rows=16, emb_lm_head=True)
+            res["cpu_baseline"]["gpu_over_cpu"] = res["value"] / res["cpu_baseline"]["value"]
         config = {"workload": "decode-heavy-32l: 32 layers 7B shape bf16 vocab 32000; 256 decode rows ctx "
                               "U[4096,8192] + 8 queries x16 tokens (mean pooling), page 16",
                   "embed_tokens": batch.n_emb_tokens, "decode_tokens": len(batch.rows), "layers": L}
@@ -671,6 +700,7 @@ def full_model_bench(args) -> dict:
         # values from the cache as it was drawn; the decode rows' own slots rewritten since)
         out["cpu_baseline"] = cpu_baseline_sample(W, W, kv, steps[0], paged.block_table, paged.max_blocks,
                                                   args.cpu_threads, n_rows=8, emb_lm_head=True)
+        out["cpu_baseline"]["gpu_over_cpu"] = out["value"] / out["cpu_baseline"]["value"]
     return out
 
 
