@@ -248,8 +248,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
                  const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
                  float *out_logits, float *out_emb, void *workspace, size_t ws_bytes, void *stream);
 
-/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
- * loops, harnesses that forbid hipMalloc): the same step as orthrus_step() with the workspace
+/* For callers that cannot allocate device memory (tight serving loops, harnesses that forbid
+ * hipMalloc): the same step as orthrus_step() with the workspace
  * replaced by library-owned scratch, a static device array of ORTHRUS_SCRATCH_BYTES that every
  * GPU the library runs on holds until the process ends.  It calls no hipMalloc, hipFree,
  * hipHostMalloc or other allocating routine and creates no stream or event: the step's metadata
@@ -262,7 +262,8 @@ int orthrus_step(const orthrus_model *emb, const orthrus_model *gen, const orthr
  * with this batch's sizes tells in advance; nothing is enqueued then); otherwise the return codes
  * of orthrus_step().  All calls on one GPU share its scratch, which keeps the last call's
  * contents: calls that overlap on one GPU (several streams or host threads) race and corrupt each
- * other's results, so serialise them. */
+ * other's results, so serialise them.  Not for capture into a HIP graph: the metadata copy reads
+ * a host buffer that lives only for the duration of the call. */
 #define ORTHRUS_SCRATCH_BYTES (64u << 20)
 int orthrus_step_noalloc(const orthrus_model *emb, const orthrus_model *gen, const orthrus_batch *batch,
                          const orthrus_kv *emb_kv, const orthrus_kv *gen_kv, float *acc_sum, float *acc_w,
