@@ -424,9 +424,9 @@ def cpu_baseline_sample(W_e, W_g, kv_g, batch, block_table, max_blocks: int, thr
         Wg = We if W_g is W_e else host_layers(W_g, L)
         k64 = kv_g.k[:L, flat].float().cpu().numpy().astype(np.float64)
         v64 = kv_g.v_by_position[:L, flat].float().cpu().numpy().astype(np.float64)
-        okv_g = OracleKV(k64, v64, bt, P)
+        okv_g = OracleKV(k64, v64, bt, P, bf16=True)
         shape = (L, max(q_pages, 1), cfg_e.n_kv_heads, P, cfg_e.head_dim)
-        okv_e = OracleKV(np.zeros(shape), np.zeros(shape), q_bt, P)
+        okv_e = OracleKV(np.zeros(shape), np.zeros(shape), q_bt, P, bf16=True)
         n_q = max(1, len(batch.chunks))
         t0 = time.perf_counter()
         if batch.chunks:

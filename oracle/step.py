@@ -22,6 +22,8 @@ Readings taken where the paper is silent (also listed in the design notes):
   sits at position ctx_len, is written to that slot and attends to ctx_len + 1
   keys including its own;
 * slot of position p of request s = block_table[s][p // page] * page + p % page;
+* a bf16 cache stores the keys and values a step writes rounded to bfloat16 (its element
+  type), and later rows and steps read them back as stored;
 * a chunk at offset 0 resets its request's state (S = 0, W = 0); a later chunk
   requires W == offset exactly, which catches a lost or repeated chunk;
 * mean: S += sum of the chunk's rows, W += len; emitted S / W.  Last-token: the
@@ -68,20 +70,36 @@ class StepError(Exception):
         self.kind = kind
 
 
-class OracleKV:
-    """float64 image of one paged cache: k, v[L][n_pages][nkv][page][hd] plus the block table."""
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Each value rounded to the nearest bfloat16 (8 significant bits, ties to the even
+    significand), returned as float64: the low 45 of float64's 52 fraction bits are dropped
+    with round-to-nearest-even on the bit pattern.  For finite values inside bfloat16's normal
+    range (the keys and values stored here)."""
+    b = np.ascontiguousarray(x, dtype=F64).view(np.uint64)
+    keep = (b >> np.uint64(45)) & np.uint64(1)
+    b = (b + np.uint64((1 << 44) - 1) + keep) & ~np.uint64((1 << 45) - 1)
+    return b.view(F64)
 
-    def __init__(self, k: np.ndarray, v: np.ndarray, block_table: np.ndarray, page_size: int):
+
+class OracleKV:
+    """float64 image of one paged cache: k, v[L][n_pages][nkv][page][hd] plus the block table.
+
+    ``bf16``: the cache's element type is bfloat16, so keys and values written by a step are
+    stored rounded to bfloat16 (and read back as stored), as a bf16 cache holds them."""
+
+    def __init__(self, k: np.ndarray, v: np.ndarray, block_table: np.ndarray, page_size: int,
+                 bf16: bool = False):
         self.k = np.array(k, dtype=F64, copy=True)
         self.v = np.array(v, dtype=F64, copy=True)
         self.block_table = np.array(block_table, dtype=np.int64, copy=True)
         self.page = int(page_size)
+        self.bf16 = bool(bf16)
         self.n_pages = self.k.shape[1]
         self.n_seq, self.max_blocks = self.block_table.shape
 
     @classmethod
     def from_paged(cls, paged) -> "OracleKV":
-        return cls(paged.k, paged.v, paged.block_table, paged.cfg.page_size)
+        return cls(paged.k, paged.v, paged.block_table, paged.cfg.page_size, bf16=paged.cfg.dtype == "bf16")
 
     def slots(self, seq: int, positions: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
         positions = np.asarray(positions, np.int64)
@@ -93,6 +111,8 @@ class OracleKV:
 
     def write(self, layer: int, seq: int, positions, k_rows, v_rows) -> None:
         pages, offs = self.slots(seq, positions)
+        if self.bf16:
+            k_rows, v_rows = round_to_bf16(k_rows), round_to_bf16(v_rows)
         self.k[layer, pages, :, offs, :] = k_rows
         self.v[layer, pages, :, offs, :] = v_rows
 

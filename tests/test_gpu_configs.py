@@ -77,7 +77,8 @@ def test_long_document_sixteen_chunks_equal_one_pass():
 def _oracle_cache(k_pool, v_pool, rec, seqs, P):
     """float64 host image of the pages of `seqs` (same page contents, compact page ids) and the
     block table that maps each sequence's blocks onto it.  k_pool [L][page][kvh][slot][hd], v_pool
-    [L][page][kvh][hd][slot]: the drawn contents, copied before the step."""
+    [L][page][kvh][hd][slot]: the drawn contents, copied before the step; a bf16 cache, so the
+    oracle stores what the step writes rounded to bfloat16."""
     pages = [rec.block_table[s][rec.block_table[s] >= 0] for s in seqs]
     flat = torch.from_numpy(np.concatenate(pages).astype(np.int64)).cuda()
     k64 = k_pool[:, flat].float().cpu().numpy().astype(np.float64)
@@ -87,7 +88,7 @@ def _oracle_cache(k_pool, v_pool, rec, seqs, P):
     for i, p in enumerate(pages):
         bt[i, :len(p)] = np.arange(o, o + len(p))
         o += len(p)
-    return OracleKV(k64, v64, bt, P)
+    return OracleKV(k64, v64, bt, P, bf16=True)
 
 
 def test_decode_heavy_every_row():

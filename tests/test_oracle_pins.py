@@ -722,3 +722,46 @@ def test_lora_contract_errors():
         step_oracle((cfg, W), (cfg, W), Batch([EmbChunk(0, 0, 2, True)], [], ids[:2], chunk_adapter=[0]),
                     kv, kv, S, Wc)
     assert e.value.kind == "desc"
+
+
+def test_bf16_rounding_of_cached_keys_and_values():
+    """round_to_bf16 against round-to-nearest-even at bfloat16's 8 significant bits, worked out
+    by hand: exact values, both sides of a tie, ties to the even significand, the carry into the
+    exponent, signed zeros; then against torch's float32 -> bfloat16 conversion on float32 inputs
+    (one rounding there, so the two must agree)."""
+    from oracle.step import round_to_bf16
+    u = 2.0 ** -7                      # one unit in the last place of bfloat16 at [1, 2)
+    cases = [(1.0, 1.0), (1 + u / 2, 1.0), (1 + 3 * u / 2, 1 + 2 * u), (1 + u / 2 + 2.0 ** -30, 1 + u),
+             (1 + u / 2 - 2.0 ** -30, 1.0), (-(1 + 3 * u / 2), -(1 + 2 * u)), (2 - u / 2, 2.0),
+             (math.pi, 3.140625), (2.0 ** 100 * (1 + u / 2), 2.0 ** 100), (0.0, 0.0), (1.5, 1.5)]
+    got = round_to_bf16(np.array([c[0] for c in cases]))
+    np.testing.assert_array_equal(got, np.array([c[1] for c in cases]))
+    assert math.copysign(1.0, float(round_to_bf16(np.array([-0.0]))[0])) == -1.0
+    import torch
+    x = np.random.default_rng(3).standard_normal(4096).astype(np.float32) * np.float32(5.0)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(round_to_bf16(x.astype(np.float64)), ref)
+
+
+def test_bf16_cache_stores_rounded_keys_and_values():
+    """A bf16 cache keeps what a step writes rounded to bfloat16 and gives it back as stored; an
+    fp32 cache keeps the float64 values."""
+    from oracle.step import round_to_bf16
+    for dtype in ("f32", "bf16"):
+        cfg = ModelConfig(n_layers=1, d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64, d_ff=256,
+                          vocab=64, dtype=dtype)
+        W = make_weights(cfg, 5)
+        pk = _fresh_kv(cfg, 1, 32, 1)
+        pk.reserve(0, 20)
+        kv = OracleKV.from_paged(pk)
+        assert kv.bf16 == (dtype == "bf16")
+        ids = draw_tokens(5, 0, 20, cfg.vocab)
+        step_oracle((cfg, W), (cfg, W), Batch([EmbChunk(0, 0, 20, False, "none")], [], ids), kv, kv,
+                    np.zeros((1, cfg.d_model)), np.zeros(1))
+        K, V = kv.read(0, 0, 20)
+        assert np.isfinite(K).all() and np.isfinite(V).all()
+        if dtype == "bf16":
+            np.testing.assert_array_equal(K, round_to_bf16(K))
+            np.testing.assert_array_equal(V, round_to_bf16(V))
+        else:
+            assert not np.array_equal(K, round_to_bf16(K))
