@@ -331,6 +331,16 @@ class Stepper:
         self.R.profile_only(dm_e, None)
         return ms, prof.get(only, (0, 0.0))
 
+    def warm_dominant(self, cfg, two_models: bool, warmup: int) -> str:
+        """`warmup` untimed steps (at least two): the first plain (it pays the first launches'
+        one-time costs), the rest with events around every launch; returns the launch name
+        with the largest share of those."""
+        import torch
+        self()
+        torch.cuda.synchronize()
+        n = max(1, warmup - 1)
+        return dominant_kernel(cfg, self.batch, two_models, self.profile(n), n)
+
     def profile(self, steps: int) -> dict:
         """Per launch name (launches, total ms) from HIP events around each launch."""
         import torch
@@ -495,10 +505,11 @@ def two_models_bench(args, layers: int = 32) -> dict:
                      max(len(b.rows) for b in steps), 4096)
     batch = steps[2]
     st = Stepper(dm_e, dm_g, kv_e, kv_g, batch, ws, paged_e.n_seq)
-    # the warm-up steps time every launch (naming the dominant kernel), the timed steps carry
-    # events on the dominant kernel's launches only, and steps of their own time every launch for
-    # the per-launch table (events around every launch shift the two streams' overlap)
-    dom = dominant_kernel(cfg_g, batch, True, st.profile(max(1, args.warmup)), max(1, args.warmup))
+    # the warm-up steps (after a plain first one) time every launch, naming the dominant kernel;
+    # the timed steps carry events on the dominant kernel's launches only, and steps of their own
+    # time every launch for the per-launch table (events around every launch shift the two
+    # streams' overlap)
+    dom = st.warm_dominant(cfg_g, True, args.warmup)
     ms, (n_dom, t_dom) = st.time(args.steps, 0, only=dom)
     log(f"{args.steps} steps, {ms:.3f} ms/step")
     prof = st.profile(args.steps)
@@ -534,7 +545,7 @@ def layer7b_bench(args, with_cpu: bool) -> dict:
     kv = device_kv(cfg, wl.kv.n_pages, wl.kv.n_seq, wl.kv.max_blocks, wl.kv.block_table, 1002)
     ws = R.Workspace(dm, dm, batch.n_tokens, len(batch.chunks), len(batch.rows), 4096)
     st = Stepper(dm, dm, kv, kv, batch, ws, wl.kv.n_seq, acc_w0=wl.acc_w)
-    dom = dominant_kernel(cfg, batch, False, st.profile(max(1, args.warmup)), max(1, args.warmup))
+    dom = st.warm_dominant(cfg, False, args.warmup)
     ms, (n_dom, t_dom) = st.time(args.steps, 0, only=dom)
     prof = st.profile(args.steps)
     res = summarize(cfg, batch, False, ms, prof, args.steps, "7b-layer-mixed", (dom, n_dom, t_dom))
@@ -652,7 +663,7 @@ def full_model_bench(args) -> dict:
         ws = R.Workspace(dm, dm, batch.n_tokens, len(batch.chunks), len(batch.rows), 8192)
         st = Stepper(dm, dm, kv, kv, batch, ws, rec.n_seq)
         steps = max(1, args.steps // 4)
-        dom = dominant_kernel(cfg, batch, False, st.profile(2), 2)
+        dom = st.warm_dominant(cfg, False, 2)
         ms, (n_dom, t_dom) = st.time(steps, 0, only=dom)
         res = summarize(cfg, batch, False, ms, st.profile(steps), steps, "decode-heavy-32l", (dom, n_dom, t_dom))
         if not args.no_cpu_baseline:
