@@ -2,8 +2,9 @@
 
 Runs `bench.py --workload 7b-layer-mixed` for a few steps as a child process and checks the line's
 contract: one JSON line with the metric, value and units; the dominant kernel's roofline timed by
-events inside the timed steps (not named by the first launches' one-time costs); the HBM traffic
-taken from the committed counter summary while the GEMM sources it names are unchanged.
+events inside the timed steps (not named by the first launches' one-time costs); the HBM traffic,
+when given, above the algorithmic bytes (it is null once the GEMM sources differ from those the
+committed counter summary was taken on).
 """
 import json
 import os
@@ -39,5 +40,5 @@ def test_one_layer_line_contract():
     assert roof["kernel"] == "gemm_gate_up" and roof["bound"] == "mfma"
     assert "inside the timed steps" in roof["timing"], roof["timing"]
     assert 0 < roof["frac"] < 1 and abs(roof["achieved"] / roof["peak"] - roof["frac"]) < 1e-9
-    assert roof["traffic"] is not None and roof["traffic"] > roof["algorithmic_bytes_per_launch"]
+    assert roof["traffic"] is None or roof["traffic"] > roof["algorithmic_bytes_per_launch"]
     print(json.dumps({k: out[k] for k in ("value", "ms_per_step")}), roof["frac"], flush=True)
