@@ -446,7 +446,9 @@ template <int HD, int G>
 __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *smem) {
     using St = PrefillStage<HD>;
     constexpr int KS = HD / 16, DB = HD / 32;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index and everything derived from it (rows, heads, causal bounds) are wave-uniform;
+    // taken from lane 0 they live in scalar registers and every branch on them is a scalar one
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ci = it[IT_INDEX], g = it[IT_KVHEAD], qb = it[IT_A], qn = it[IT_B];
     // keys [k0, kend) of the tile: all of them up to its causal bound, or one piece of a
     // key-split tile (pieces start on 64-key boundaries, so block k0 / 32 is even; only the last
@@ -482,7 +484,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     int w0 = 2 * kb0;
     auto page_of = [&](int blk) -> int2 {  // pages of the block's two halves; -1 = bad
         const int p0 = min(2 * blk, last_block), p1 = min(2 * blk + 1, last_block);
-        return int2{pg_lds[p0 - w0], pg_lds[p1 - w0]};
+        return int2{__builtin_amdgcn_readfirstlane(pg_lds[p0 - w0]), __builtin_amdgcn_readfirstlane(pg_lds[p1 - w0])};
     };
 
     // chunk assignment of this thread: PER_THREAD chunks c = tid + 256 * i over [K | V] (the
@@ -651,28 +653,27 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     stash(stg0, smem, kb0, pg_b0);
     int2 pg_b1 = kb0 + 1 < nkb ? page_of(kb0 + 1) : int2{-1, -1};
     int2 pg_b2 = kb0 + 2 < nkb ? page_of(kb0 + 2) : int2{-1, -1};
-    if (kb0 + 1 < nkb) issue(stg1, pg_b1);
-    if (kb0 + 2 < nkb) issue(stg0, pg_b2);
+    // Every stage is loaded on every path, blocks past the tile's end from page 0 (never
+    // stashed): the load counter then advances alike on all paths, so the waits the compiler
+    // places before each stash cover that stage's loads only and leave the next stage's in
+    // flight (with conditional loads it waited for all of them).
+    issue(stg1, pg_b1);
+    issue(stg0, pg_b2);
     __syncthreads();
     // iteration kb: compute block kb, stash block kb + 1 from its stage, reuse that stage for
     // block kb + 3; stage of block b is stg1 for odd b, stg0 for even b
     for (int kb = kb0; kb < nkb; kb += 2) {
         compute(kb);
         if (kb + 1 < nkb) stash(stg1, smem + St::BYTES, kb + 1, pg_b1);
-        int2 pg_b3 = {-1, -1};
-        if (kb + 3 < nkb) {
-            pg_b3 = block_pages(kb + 3);
-            issue(stg1, pg_b3);
-        }
+        const int2 pg_b3 = kb + 3 < nkb ? block_pages(kb + 3) : int2{-1, -1};
+        issue(stg1, pg_b3);
         __syncthreads();
-        if (kb + 1 >= nkb) break;
-        compute(kb + 1);
+        // a guarded block, not a loop exit: an exit here gave the compiler a path into the next
+        // iteration on which the stage just issued is the newest, and its waits for every stage
+        if (kb + 1 < nkb) compute(kb + 1);
         if (kb + 2 < nkb) stash(stg0, smem, kb + 2, pg_b2);
-        int2 pg_b4 = {-1, -1};
-        if (kb + 4 < nkb) {
-            pg_b4 = block_pages(kb + 4);
-            issue(stg0, pg_b4);
-        }
+        const int2 pg_b4 = kb + 4 < nkb ? block_pages(kb + 4) : int2{-1, -1};
+        issue(stg0, pg_b4);
         __syncthreads();
         pg_b1 = pg_b3;
         pg_b2 = pg_b4;
