@@ -173,6 +173,8 @@ struct AttnArgs {
     const int32_t *chunks, *rows, *items;
     const int32_t *combine;   // merge entries of key-split prefill tiles
     float *partials;          // [slot][group][hd + 2]
+    // n_prefill: prefill items at the head of `items` (0: decode items only, served by the
+    // decode-only kernel on the bf16 path); n_items: all items of the launch
     int n_prefill, n_items, n_combine, Te, nq, nkv, hd, page;
     int *err;
 };

@@ -614,10 +614,12 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
         AttnArgs ag = aa;
         int n_dec = 0;
         if (gi == 0) {
+            ag.n_prefill = p.n_pre_emb;
             ag.n_items = p.n_pre_emb;
             ag.n_combine = p.n_merge_emb;
         } else {
             ag.items = aa.items + kItemInts * p.n_pre_emb;
+            ag.n_prefill = p.n_prefill - p.n_pre_emb;
             ag.n_items = aa.n_items - p.n_pre_emb;
             ag.combine = aa.combine + kCombineInts * p.n_merge_emb;
             ag.n_combine = merges_gen;
