@@ -57,6 +57,48 @@ __device__ __forceinline__ PoolView pool_view(const AttnArgs &a, int p) {
 // prefill chunks of the generator (prompt chunks) read its cache
 __device__ __forceinline__ int chunk_pool(const int32_t *ch) { return (ch[3] & kChunkGen) ? 1 : 0; }
 
+// Cross-lane partners without LDS permutes (each an exact copy of another lane's value):
+//   quad_xor1 / quad_xor2: lane ^ 1 / lane ^ 2 (DPP quad permutations);
+//   half_mirror: lane 7 - i within each 8 lanes, mirror: lane 15 - i within each 16 lanes (DPP);
+//   with_partner16 / with_partner32: this lane's value and that of the same lane in the paired
+//   16-lane row (lane ^ 16) or wave half (lane ^ 32), via v_permlane16_swap / v_permlane32_swap,
+//   whose pair of results holds both values (in an order that depends on the lane).
+// For a value equal across each quad (or each 8 or 16 lanes), a mirror partner is the xor
+// partner's equal, so reductions over lanes give the same results as with xor shuffles.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float quad_xor1(float v) { return dpp_mov<0xB1>(v); }
+__device__ __forceinline__ float quad_xor2(float v) { return dpp_mov<0x4E>(v); }
+__device__ __forceinline__ float half_mirror(float v) { return dpp_mov<0x141>(v); }
+__device__ __forceinline__ float mirror(float v) { return dpp_mov<0x140>(v); }
+__device__ __forceinline__ float2 with_partner16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return float2{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ float2 with_partner32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return float2{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+// maximum and sum over the 16 quads of the wave of a value equal within each quad
+__device__ __forceinline__ float quads_max(float v) {
+    v = fmaxf(v, half_mirror(v));
+    v = fmaxf(v, mirror(v));
+    float2 p = with_partner16(v);
+    v = fmaxf(p.x, p.y);
+    p = with_partner32(v);
+    return fmaxf(p.x, p.y);
+}
+__device__ __forceinline__ float quads_sum(float v) {
+    v += half_mirror(v);
+    v += mirror(v);
+    float2 p = with_partner16(v);
+    v = p.x + p.y;
+    p = with_partner32(v);
+    return p.x + p.y;
+}
+
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c,
                                            false);
@@ -181,8 +223,8 @@ __device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *sme
                 for (int cc = 0; cc < KL; ++cc)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) d2 = dot2(qh[cc][e], kr[i][cc][e], d2);
-                d2 += __shfl_xor(d2, 1, 64);
-                d2 += __shfl_xor(d2, 2, 64);
+                d2 += quad_xor1(d2);
+                d2 += quad_xor2(d2);
                 s[i][h] = vis ? d2 * scale : -INFINITY;
                 mloc[h] = fmaxf(mloc[h], s[i][h]);
             }
@@ -199,9 +241,7 @@ __device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *sme
         // ---- online softmax over the wave's keys so far
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            float mh = mloc[h];
-#pragma unroll
-            for (int o = 4; o <= 32; o <<= 1) mh = fmaxf(mh, __shfl_xor(mh, o, 64));
+            const float mh = quads_max(mloc[h]);
             const float mn = fmaxf(m[h], mh);
             const float alpha = m[h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[h] - mn);
             m[h] = mn;
@@ -214,9 +254,7 @@ __device__ void decode_item_bf16(const AttnArgs &a, const int32_t *it, char *sme
                 const int key = i * kPage + kin;
                 if (qtr == 0) pk16[((key >> 1) * G + h) * 2 + (key & 1)] = (uint16_t)f2bf_bits(pr);
             }
-#pragma unroll
-            for (int o = 4; o <= 32; o <<= 1) ls += __shfl_xor(ls, o, 64);
-            l[h] = l[h] * alpha + ls;
+            l[h] = l[h] * alpha + quads_sum(ls);
 #pragma unroll
             for (int d = 0; d < VD; ++d) acc[h][d] *= alpha;
         }
