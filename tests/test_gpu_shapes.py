@@ -5,8 +5,9 @@ has its own instantiation of the attention kernels, the rotation epilogue and th
 append row kernel.  One two-step scenario runs on all six pairs: a chunk resuming after 1500
 cached tokens (mean), a one-chunk CLS request, a last-token request over two chunks, a one-chunk
 prompt that gets logits, and decode rows at contexts 0, 17, 1100 and 2100 (several key splits);
-then the second chunk, the prompt's first decode token and the decode rows again.  Logits,
-embeddings, pooling state and every cache write are compared.
+then the second chunk, the prompt's first decode token and the decode rows again; then the
+decode rows alone (a launch without prefill tiles: the decode-only attention kernel on the bf16
+path).  Logits, embeddings, pooling state and every cache write are compared.
 """
 import numpy as np
 import pytest
@@ -41,7 +42,7 @@ def test_every_head_shape_mixed_steps(dtype, head_dim, group):
     pk.fill_random(0, 1500, seed)
     for s, c in dec_ctx.items():
         pk.fill_random(s, c, seed + 1)
-    for s, n in {0: 1600, 1: 77, 2: 80, 3: 41, 4: 2, 5: 19, 6: 1102, 7: 2102}.items():
+    for s, n in {0: 1600, 1: 77, 2: 80, 3: 42, 4: 3, 5: 20, 6: 1103, 7: 2103}.items():
         pk.reserve(s, n)
     acc_w = np.zeros(n_seq)
     acc_w[0] = 1500
@@ -55,4 +56,6 @@ def test_every_head_shape_mixed_steps(dtype, head_dim, group):
     rows2 = [DecodeRow(3, 40)] + [DecodeRow(s, c + 1) for s, c in dec_ctx.items()]
     b2 = Batch([EmbChunk(2, 50, 30, True, "last")], rows2, draw_tokens(seed, 2, 30 + 5, cfg.vocab))
     pair.step(b2)
+    rows3 = [DecodeRow(3, 41)] + [DecodeRow(s, c + 2) for s, c in dec_ctx.items()]
+    pair.step(Batch([], rows3, draw_tokens(seed, 3, 5, cfg.vocab)))
     print(f"{dtype} hd {head_dim} group {group}: {pair.report}", flush=True)
