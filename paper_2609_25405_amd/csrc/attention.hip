@@ -10,19 +10,20 @@
 //   * prefill items (rows of embedding and generation prefill chunks, heaviest first; each
 //     chunk reads the cache of its own model): (128 / group) tokens of one chunk
 //     times the `group` query heads of one KV head; each wave owns 32 query rows of one head
-//     and walks the keys of its request in 32-key blocks, with operands loaded straight from
-//     the cache (L2-resident, shared by the group's waves) one block ahead of the MFMAs, an
-//     online softmax in fp32 (exp2 domain) and causal masking on the diagonal blocks.  Waves
-//     never synchronise, so each stops at its own causal bound.  A tile over a long cached
-//     prefix comes as several items, one per run of keys (the walk is serial, about a
-//     microsecond per 32-key block, so one long tile would otherwise set the launch's length);
-//     those write partials like split decode rows, merged by attn_combine.
-//   * decode items: one (decode row, KV head, key-range split), walked in 128-key chunks.  Each
-//     wave owns two pages of a chunk, scores with v_dot2_f32_bf16 for all `group` query heads
-//     at once, keeps an online softmax, and accumulates P V from registers; the next chunk's K
-//     and V loads (64 KiB per item) are in flight while a chunk is computed.  Rows with
-//     several splits write (max, sum, unnormalised output) partials merged by attn_combine in
-//     split order, so results do not depend on scheduling.
+//     and walks the keys of its request in 32-key blocks that the workgroup stages in LDS
+//     (two buffers, the next blocks' loads in registers, one barrier per block; the block is
+//     shared by the group's waves), with an online softmax in fp32 (exp2 domain) and causal
+//     masking on the diagonal blocks; a wave past its causal bound skips the block's
+//     arithmetic.  A tile over a long cached prefix comes as several items, one per run of
+//     keys (the walk is serial, about a microsecond and a half per 32-key block, so one long
+//     tile would otherwise set the launch's length); those write partials like split decode
+//     rows, merged by attn_combine.
+//   * decode items: one (decode row, KV head, key-range split), walked in 128-key chunks (64
+//     in the decode-only kernel).  Each wave owns two pages of a chunk (one), scores with
+//     v_dot2_f32_bf16 for all `group` query heads at once, keeps an online softmax, and
+//     accumulates P V from registers; the next chunk's K and V loads are in flight while a
+//     chunk is computed.  Rows with several splits write (max, sum, unnormalised output)
+//     partials merged by attn_combine in split order, so results do not depend on scheduling.
 // Page ids read from the block table are range-checked; a bad id sets the sticky device error
 // word and its keys are skipped (never dereferenced).
 #include "common.hpp"
@@ -105,8 +106,8 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
 }
 
 // ------------------------------------------------------------------ decode split, bf16 path
-// A split is walked in chunks of kDecodeChunkPages pages (128 keys); each wave owns two pages of
-// a chunk.  Loads are branch-free (invalid or absent pages read page 0 and are masked) and
+// A split is walked in chunks of CP pages (kDecodeChunkPages = 8 pages, 128 keys, in the combined
+// kernel; 4 in the decode-only kernel); each wave owns CP / 4 pages of a chunk.  Loads are branch-free (invalid or absent pages read page 0 and are masked) and
 // software-pipelined across chunks: the next chunk's K lines go out as soon as this chunk's
 // scores are taken, its V lines as soon as this chunk's P V is done, and page ids two chunks
 // ahead, so the memory pipe stays busy while the wave computes.  Each wave keeps an online
