@@ -570,8 +570,8 @@ hipError_t run_bf16(const GemmArgs &a, hipStream_t s) {
 //    concurrently with another stream (GemmArgs::wide), the same projections take 256x256
 //    tiles: 4x fewer workgroup-microseconds per flop at a longer launch, which the other
 //    stream's launches fill (the two-model 32-layer step, QKV, o and down of the generator's
-//    256 decode rows so tiled: 23.4 -> 22.5 ms and 23.9 -> 23.2 ms on two GPUs; gate/up so
-//    tiled as well measured slower than neither);
+//    256 decode rows so tiled: 23.4 -> 22.5 ms and 23.9 -> 23.2 ms on two GPUs; the
+//    generator's gate/up on such tiles as well measured slower);
 //  - gate/up of 256 < M <= 896, measured on the 7B shape with cold weights: 192x256 when
 //    128x128 tiles need more than the 512 slots of one round and 192x256 tiles fit in one
 //    (M = 640: 172 against 195 us), else the tile that pads M least (M = 384 98 against 130 us,
