@@ -144,3 +144,47 @@ def test_runner_lora_requests():
         lora = W64["adapters"][ad] if ad >= 0 else None
         assert_vectors_close(embs[rid][None], embed_single_pass(cfg, W64, ids, "mean", lora=lora)[None],
                              "bf16", f"embedding {rid}")
+
+
+@pytest.mark.parametrize("dtype,qk_std", [("f32", None), ("bf16", 0.09)])
+def test_lora_two_models_concurrent_groups(dtype, qk_std):
+    """Adapters on the embedding model of a two-model step: the embedding rows (adapted and
+    base chunks) run on one stream with their shrink launches, the generator's decode rows over
+    its own weights and cache on the other, every step checked against the oracle."""
+    cfg = tiny_config(dtype)
+    W_e = make_weights(cfg, 107, model_tag=1, qk_std=qk_std)
+    W_e["adapters"] = [make_lora(cfg, 107, 16, tag=1), make_lora(cfg, 107, 16, tag=2, scale=1.0)]
+    W_g = make_weights(cfg, 107, model_tag=2, qk_std=qk_std)
+    W64 = as_float64(W_e)
+    lens, ads, chunk, max_blocks = [150, 97, 64], [0, 1, -1], 64, 32
+    decode_ctx = (50, 90, 300)
+    pe = PagedKV(cfg, len(lens) * max_blocks + 3, len(lens), max_blocks, 107)
+    for s, n in enumerate(lens):
+        pe.reserve(s, n)
+    pg = PagedKV(cfg, len(decode_ctx) * max_blocks + 3, len(decode_ctx), max_blocks, 108)
+    for i, c in enumerate(decode_ctx):
+        pg.fill_random(i, c, 109)
+        pg.reserve(i, c + 8)
+    pair = Pair(cfg, W_e, pe, cfg, W_g, pg)
+    pair.workspace(max_tokens=chunk * len(lens) + len(decode_ctx), max_chunks=len(lens),
+                   max_decode=len(decode_ctx), max_ctx=max_blocks * 16)
+    ids = {s: draw_tokens(107, s, lens[s], cfg.vocab) for s in range(len(lens))}
+    done = {}
+    for step, off in enumerate(range(0, max(lens), chunk)):
+        chunks, toks, cads = [], [], []
+        for s in range(len(lens)):
+            if off < lens[s]:
+                ln = min(chunk, lens[s] - off)
+                chunks.append(EmbChunk(s, off, ln, off + ln == lens[s], "mean"))
+                toks.append(ids[s][off:off + ln])
+                cads.append(ads[s])
+        rows = [DecodeRow(i, c + step) for i, c in enumerate(decode_ctx)]
+        toks.append(draw_tokens(107, 100 + step, len(rows), cfg.vocab))
+        _, _, out = pair.step(Batch(chunks, rows, np.concatenate(toks).astype(np.int32), chunk_adapter=cads))
+        for i, c in enumerate(chunks):
+            if c.last:
+                done[c.seq] = out[i].cpu().numpy()
+    for s, ad in enumerate(ads):
+        want = embed_single_pass(cfg, W64, ids[s], "mean", lora=W64["adapters"][ad] if ad >= 0 else None)
+        assert_vectors_close(done[s][None], want[None], dtype, f"request {s} vs single pass")
+    print(pair.report, flush=True)
