@@ -26,10 +26,11 @@ def _need_gpu(request):
     print(f"\n[case] {request.node.name}", flush=True)
 
 
-@pytest.mark.parametrize("dtype,qk_std", [("f32", None), ("bf16", 0.09)])
-def test_weighted_and_buffered_heads_over_two_steps(dtype, qk_std):
+@pytest.mark.parametrize("dtype,qk_std,two_models", [("f32", None, False), ("bf16", 0.09, False), ("bf16", 0.09, True)])
+def test_weighted_and_buffered_heads_over_two_steps(dtype, qk_std, two_models):
     """Requests: 0 weighted mean (150 tokens in 100 + 50), 1 buffered (90 in 64 + 26), 2 mean
-    (40, one chunk), 3 weighted mean with all-zero weights (20), plus decode rows."""
+    (40, one chunk), 3 weighted mean with all-zero weights (20), plus decode rows; with two
+    models the decode rows run through a generator of its own weights and cache, concurrently."""
     cfg = tiny_config(dtype)
     W = make_weights(cfg, 91, qk_std=qk_std)
     W64 = as_float64(W)
@@ -37,10 +38,15 @@ def test_weighted_and_buffered_heads_over_two_steps(dtype, qk_std):
     pk = PagedKV(cfg, n_seq * mb + 3, n_seq, mb, 91)
     for s in range(4):
         pk.reserve(s, 200)
+    if two_models:
+        pg = PagedKV(cfg, n_seq * mb + 3, n_seq, mb, 93)
+        W_g = make_weights(cfg, 91, model_tag=2, qk_std=qk_std)
+    else:
+        pg = pk
     for s in (4, 5):
-        pk.fill_random(s, 60 + 10 * s, 92)
-        pk.reserve(s, 64 + 10 * s)
-    pair = Pair(cfg, W, pk)
+        pg.fill_random(s, 60 + 10 * s, 92)
+        pg.reserve(s, 64 + 10 * s)
+    pair = Pair(cfg, W, pk, cfg, W_g, pg) if two_models else Pair(cfg, W, pk)
     pair.workspace(max_tokens=256, max_chunks=4, max_decode=2, max_ctx=256)
     ids = {0: draw_tokens(91, 0, 150, cfg.vocab), 1: draw_tokens(91, 1, 90, cfg.vocab),
            2: draw_tokens(91, 2, 40, cfg.vocab), 3: draw_tokens(91, 3, 20, cfg.vocab)}
