@@ -22,8 +22,9 @@ the kernel with the largest share of the step, timed by event pairs around its l
 the timed steps (no events on any other launch there).  `cpu_baseline` times the float64 CPU oracle on a
 sample of the same step (see cpu_baseline_sample), with its embedding and decode tokens/s and the
 GPU/CPU ratio.  Extra keys: the same two models over an embedding-fraction sweep (`sweep`), the
-one-7B-layer mixed step (`layer7b`), and a plain 1 GiB device copy's rate (`copy_ceiling`, a
-practical HBM ceiling, not a target).
+dominant kernel's launches with the embedding rows alone (`dominant_alone`: no generator launches
+sharing the CUs), the one-7B-layer mixed step (`layer7b`), and a plain 1 GiB device copy's rate
+(`copy_ceiling`, a practical HBM ceiling, not a target).
 """
 from __future__ import annotations
 
@@ -524,6 +525,7 @@ def two_models_bench(args, layers: int = 32) -> dict:
                       "ms_per_step": t, "tokens_per_s": b.n_tokens / (t * 1e-3)})
     res["sweep"] = sweep
     res["sweep_tokens_per_s"] = sum(b.n_tokens for b in steps) / (sum(s["ms_per_step"] for s in sweep) * 1e-3)
+    res["dominant_alone"] = dominant_alone(dm_e, kv_e, batch, paged_e.n_seq, dom, max(5, args.steps // 2))
     if not args.no_cpu_baseline:
         from workload import DeviceKVRecipe
         rec_g = DeviceKVRecipe(paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
@@ -532,6 +534,29 @@ def two_models_bench(args, layers: int = 32) -> dict:
     del st, ws, kv_e, kv_g, dm_e, dm_g, W_e, W_g
     torch.cuda.empty_cache()
     return config, res
+
+
+def dominant_alone(dm_e, kv_e, batch, n_seq_e, dom: str, steps: int) -> dict:
+    """The headline batch's embedding chunks alone through the embedding model (no generator
+    launches beside them): HIP events around each launch of the dominant kernel in `steps`
+    steps, against its roofline.  The same launches as in the headline step, without the CUs
+    they share there."""
+    from paper_2609_25405_amd import runtime as R
+    from workload import Batch
+    name = dom.split("@")[0]
+    b = Batch(batch.chunks, [], batch.token_ids[:batch.n_emb_tokens])
+    ws = R.Workspace(dm_e, dm_e, b.n_tokens, max(1, len(b.chunks)), 1, 4096)
+    st = Stepper(dm_e, dm_e, kv_e, kv_e, b, ws, n_seq_e)
+    ms, (n, tot) = st.time(steps, 2, only=name)
+    flop, byts = launch_work(dm_e.cfg, b, False).get(name, (0.0, 0.0))
+    avg = tot / max(1, n)
+    out = {"kernel": name, "launches": n, "avg_launch_ms": avg, "step_ms": ms,
+           "what": "the headline batch's embedding chunks through the embedding model alone; HIP events "
+                   "around each launch of the kernel"}
+    if flop > 0 and avg > 0:
+        out.update(achieved=flop / (avg * 1e-3) / 1e12, unit="TFLOP/s", frac=flop / (avg * 1e-3) / 1e12 / PEAK_BF16_TFLOPS)
+    del st, ws
+    return out
 
 
 def layer7b_bench(args, with_cpu: bool) -> dict:
