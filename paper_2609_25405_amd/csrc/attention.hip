@@ -775,15 +775,15 @@ __global__ __launch_bounds__(256, BF16 ? 2 : 1) void attn_kernel(AttnArgs a) {
 }
 
 // Decode items only (bf16; a launch whose work list holds no prefill tile, e.g. the generator's
-// rows of a two-model step): chunks of kSharedChunkPages pages, one page per wave.  Without the
+// rows of a two-model step): chunks of kDecodeOnlyChunkPages pages, one page per wave.  Without the
 // prefill path's registers and LDS the workgroup needs 134 VGPRs and 13 KB (7B shape, group 4)
 // instead of 212 and 38 KB, so three fit per CU instead of two (two-model step with decode rows
 // only: 10.30 -> 10.14 ms).
-constexpr int kSharedChunkPages = 4;
+constexpr int kDecodeOnlyChunkPages = 4;
 template <int HD, int G>
 __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) char smem[decode_smem<HD, G, kSharedChunkPages>()];
-    decode_item_bf16<HD, G, kSharedChunkPages>(a, a.items + kItemInts * blockIdx.x, smem);
+    __shared__ __attribute__((aligned(16))) char smem[decode_smem<HD, G, kDecodeOnlyChunkPages>()];
+    decode_item_bf16<HD, G, kDecodeOnlyChunkPages>(a, a.items + kItemInts * blockIdx.x, smem);
 }
 
 // Merge key-range partials in split order: M = max m_s, L = sum l_s 2^(m_s - M),
