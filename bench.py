@@ -525,7 +525,11 @@ def two_models_bench(args, layers: int = 32) -> dict:
                       "ms_per_step": t, "tokens_per_s": b.n_tokens / (t * 1e-3)})
     res["sweep"] = sweep
     res["sweep_tokens_per_s"] = sum(b.n_tokens for b in steps) / (sum(s["ms_per_step"] for s in sweep) * 1e-3)
-    res["dominant_alone"] = dominant_alone(dm_e, kv_e, batch, paged_e.n_seq, dom, max(5, args.steps // 2))
+    try:
+        res["dominant_alone"] = dominant_alone(dm_e, kv_e, batch, paged_e.n_seq, dom, max(5, args.steps // 2))
+    except Exception as e:   # noqa: BLE001  (an extra: reported, not fatal to the headline)
+        log(f"dominant_alone failed: {e!r}")
+        res["dominant_alone"] = {"error": repr(e)}
     if not args.no_cpu_baseline:
         from workload import DeviceKVRecipe
         rec_g = DeviceKVRecipe(paged_g.n_pages, paged_g.n_seq, paged_g.max_blocks, paged_g.block_table, 2)
@@ -659,9 +663,19 @@ def main() -> int:
         config, res = two_models_bench(args)
         out = line(args, config, res, args.steps, args.warmup)
         if not args.no_extras:
-            c7, r7 = layer7b_bench(args, with_cpu=False)
-            out["layer7b"] = dict(config=c7, **r7)
-            out["copy_ceiling"] = copy_ceiling()
+            # extras: a Python-level failure in one of them is reported in its key, not allowed to
+            # take the measured headline line with it
+            try:
+                c7, r7 = layer7b_bench(args, with_cpu=False)
+                out["layer7b"] = dict(config=c7, **r7)
+            except Exception as e:   # noqa: BLE001
+                log(f"layer7b failed: {e!r}")
+                out["layer7b"] = {"error": repr(e)}
+            try:
+                out["copy_ceiling"] = copy_ceiling()
+            except Exception as e:   # noqa: BLE001
+                log(f"copy_ceiling failed: {e!r}")
+                out["copy_ceiling"] = {"error": repr(e)}
     elif args.workload == "7b-layer-mixed":
         config, res = layer7b_bench(args, with_cpu=True)
         out = line(args, config, res, args.steps, args.warmup)
