@@ -465,19 +465,29 @@ __device__ void prefill_item_f32(const AttnArgs &a, const int32_t *it) {
 }
 
 // ------------------------------------------------------------------ prefill, bf16 MFMA path
-// 32-key blocks (two pages) are staged cooperatively into LDS: keys as [key][dim] rows, values
-// as [dim][key] rows (the cache already stores each page dim-major, so this is a plain copy).
-// Global loads of block kb+1 (and the page ids of block kb+2) are issued before block kb is
-// computed and land in the other LDS buffer after it; one barrier per block.
+// 64-key blocks (four pages) reach LDS by direct global->LDS copies (global_load_lds_dwordx4, no
+// register staging): keys as [key][dim] rows of HD*2 bytes, 16-byte chunks XOR-swizzled by row
+// so the 16 lanes reading one chunk of 16 keys hit distinct banks; values page by page as the
+// cache holds them, [page][dim][16 positions], the two 16-byte halves of a dim swapped on every
+// other group of 8 dims.  Two LDS buffers, alternating from the item's first block (a key piece
+// may start on an odd block): the copies of block kb+1 go out after the barrier
+// that opens block kb and land while block kb is computed; one barrier per 64 keys.  A block
+// holding keys past the tile's end or a bad page gets those values (and a bad page's keys)
+// zeroed in LDS before it is read (cache slots past a sequence's length may hold NaN).
 template <int HD>
 struct PrefillStage {
-    static constexpr int KROW = HD * 2 + 16;      // padded key row (bytes)
-    static constexpr int VROW = 32 * 2 + 8;       // padded value row over 32 keys (bytes)
-    static constexpr int KCH = 32 * HD / 8;       // 16-byte chunks of the key block
-    static constexpr int VCH = 2 * HD * 2;        // 16-byte chunks of the value block
-    static constexpr int PER_THREAD = (KCH + VCH) / 256;
-    static constexpr int BYTES = 32 * KROW + HD * VROW;
-    static_assert((KCH + VCH) % 256 == 0, "chunks per thread");
+    static constexpr int KEYS = 64;                     // keys per block
+    static constexpr int KRB = HD * 2;                  // bytes of one key row
+    static constexpr int KCH = KRB / 16;                // 16-byte chunks per key row
+    static constexpr int RP256 = 256 / KRB;             // key rows per 256 bytes
+    static constexpr int KBYTES = KEYS * KRB;           // key block
+    static constexpr int VPAGE = HD * kPage * 2;        // one page's values (one KV head)
+    static constexpr int BYTES = KBYTES + 4 * VPAGE;    // one buffer
+    static constexpr int K_INST = KBYTES / 1024, V_INST = 4 * VPAGE / 1024;   // 1 KiB copies
+    static_assert(K_INST % 4 == 0 && V_INST % 4 == 0, "copies per wave");
+    // physical 16-byte chunk of logical chunk c of key row r / of value chunk c of dim d
+    static __device__ __forceinline__ int kchunk(int r, int c) { return c ^ ((r / RP256) % KCH); }
+    static __device__ __forceinline__ int vchunk(int d, int c) { return c ^ ((d >> 3) & 1); }
 };
 
 template <int HD, int G>
@@ -489,8 +499,8 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ci = it[IT_INDEX], g = it[IT_KVHEAD], qb = it[IT_A], qn = it[IT_B];
     // keys [k0, kend) of the tile: all of them up to its causal bound, or one piece of a
-    // key-split tile (pieces start on 64-key boundaries, so block k0 / 32 is even; only the last
-    // piece reaches the diagonal), whose (max, sum, unnormalised output) go to partial slots
+    // key-split tile (pieces start on 64-key boundaries and only the last piece reaches the
+    // diagonal), whose (max, sum, unnormalised output) go to partial slots
     const int k0 = it[IT_KEY_BEGIN], kend = it[IT_KEY_END], pslot = it[IT_PARTIAL];
     const int32_t *ch = a.chunks + kChunkInts * ci;
     const int seq = ch[0], off = ch[1], tok0 = ch[4];
@@ -504,7 +514,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     const PoolView pv = pool_view(a, chunk_pool(ch));
     const size_t page_bytes = (size_t)a.nkv * kPage * HD * 2;
     const int32_t *bt = pv.bt + (size_t)seq * pv.max_blocks;
-    const int kb0 = k0 / 32, nkb = (kend + 31) / 32;
+    const int kb0 = k0 / St::KEYS, nkb = (kend + St::KEYS - 1) / St::KEYS;
     const int last_block = (kend - 1) / kPage;      // last page index the tile reads
 
     // page ids of the tile's keys, staged in LDS a window at a time (validated there, -1 = bad)
@@ -519,73 +529,61 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         }
         if (bad) flag_error(a.err, ORTHRUS_DEVERR_PAGE);
     };
-    int w0 = 2 * kb0;
-    auto page_of = [&](int blk) -> int2 {  // pages of the block's two halves; -1 = bad
-        const int p0 = min(2 * blk, last_block), p1 = min(2 * blk + 1, last_block);
-        return int2{__builtin_amdgcn_readfirstlane(pg_lds[p0 - w0]), __builtin_amdgcn_readfirstlane(pg_lds[p1 - w0])};
+    int w0 = 4 * kb0;
+    // page id of page p (0..3) of block blk (-1 = bad); pages past the tile's last one repeat it
+    auto page_of = [&](int blk, int p) -> int {
+        return __builtin_amdgcn_readfirstlane(pg_lds[min(4 * blk + p, last_block) - w0]);
     };
-
-    // chunk assignment of this thread: PER_THREAD chunks c = tid + 256 * i over [K | V] (the
-    // first KI of them key chunks); two register stages keep the next two blocks' loads in
-    // flight.  Source and LDS offsets do not depend on the block, only the two page ids do.
-    constexpr int KI = St::KCH / 256;
-    static_assert(St::KCH % 256 == 0, "key chunks per thread");
-    uint32_t src_off[St::PER_THREAD], lds_off[St::PER_THREAD];
-    int lo_key[St::PER_THREAD];       // K: key within the block; V: first key of the 8-key run
-    bool hi_page[St::PER_THREAD];     // chunk reads the block's second page
-#pragma unroll
-    for (int i = 0; i < St::PER_THREAD; ++i) {
-        const int c = tid + 256 * i;
-        if (i < KI) {
-            const int key = c / (HD / 8), part = c % (HD / 8);
-            hi_page[i] = key >= kPage;
-            lo_key[i] = key;
-            src_off[i] = ((g * kPage + (key & 15)) * HD + part * 8) * 2;
-            lds_off[i] = key * St::KROW + part * 16;
-        } else {
-            const int v = c - St::KCH;
-            const int p2 = v / (HD * 2), rem = v % (HD * 2);
-            const int d = rem >> 1, h2 = rem & 1;
-            hi_page[i] = p2 != 0;
-            lo_key[i] = p2 * kPage + h2 * 8;
-            src_off[i] = (g * HD + d) * kPage * 2 + h2 * 16;
-            lds_off[i] = 32 * St::KROW + d * St::VROW + p2 * 32 + h2 * 16;
+    // page ids of block b, switching the LDS window when b leaves it (blocks never straddle a
+    // window: windows start at multiples of four pages); called at the same point by every thread
+    auto block_pages = [&](int b, int (&pg)[4]) {
+        if (4 * b - w0 >= kPrefillPageWindow) {
+            __syncthreads();
+            w0 += kPrefillPageWindow;
+            load_window(w0);
+            __syncthreads();
         }
-    }
-    u32x4 stg0[St::PER_THREAD], stg1[St::PER_THREAD];
-    auto issue = [&](u32x4 (&stg)[St::PER_THREAD], int2 pg) {
-        const char *k0 = pv.k + (size_t)max(pg.x, 0) * page_bytes, *k1 = pv.k + (size_t)max(pg.y, 0) * page_bytes;
-        const char *v0 = pv.v + (size_t)max(pg.x, 0) * page_bytes, *v1 = pv.v + (size_t)max(pg.y, 0) * page_bytes;
 #pragma unroll
-        for (int i = 0; i < St::PER_THREAD; ++i) {
-            const char *base = i < KI ? (hi_page[i] ? k1 : k0) : (hi_page[i] ? v1 : v0);
-            stg[i] = *(const u32x4 *)(base + src_off[i]);
+        for (int p = 0; p < 4; ++p) pg[p] = page_of(b, p);
+    };
+    // this wave's copies of block b (pages pg) into buffer buf: key copies w, w + 4, ..., then
+    // value copies; a bad page reads page 0 (zeroed in LDS afterwards)
+    auto issue = [&](const int (&pg)[4], int buf) {
+        char *kl = smem + buf * St::BYTES, *vl = kl + St::KBYTES;
+#pragma unroll
+        for (int j = wave; j < St::K_INST; j += 4) {
+            const int row = j * (1024 / St::KRB) + lane / St::KCH;
+            const int c = St::kchunk(row, lane % St::KCH);
+            const char *src = pv.k + (size_t)max(pg[row / kPage], 0) * page_bytes +
+                              ((size_t)(g * kPage + row % kPage) * HD + c * 8) * 2;
+            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(kl + j * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int j = wave; j < St::V_INST; j += 4) {
+            constexpr int PER_PAGE = St::VPAGE / 1024;
+            const int p = j / PER_PAGE, d = (j % PER_PAGE) * 32 + lane / 2;
+            const int c = St::vchunk(d, lane % 2);
+            const char *src = pv.v + (size_t)max(pg[p], 0) * page_bytes + ((size_t)(g * HD + d) * kPage + c * 8) * 2;
+            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)(vl + j * 1024), 16, 0, 0);
         }
     };
-    // keys at or past the tile's causal bound, or on a bad page, are stored as zeros (their
-    // slots may hold other data or NaN poison); blocks clear of both are stored as loaded
-    auto stash = [&](const u32x4 (&stg)[St::PER_THREAD], char *buf, int blk, int2 pg) {
-        const bool ok0 = pg.x >= 0, ok1 = pg.y >= 0;
-        if (ok0 && ok1 && (blk + 1) * 32 <= kend) {
-#pragma unroll
-            for (int i = 0; i < St::PER_THREAD; ++i) *(u32x4 *)(buf + lds_off[i]) = stg[i];
-            return;
+    // zero, in buffer buf of block b, the values of keys at or past kend and the keys and values
+    // of bad pages (a uniform condition decides whether any thread needs to)
+    auto needs_fixup = [&](int b, const int (&pg)[4]) {
+        return (b + 1) * St::KEYS > kend || pg[0] < 0 || pg[1] < 0 || pg[2] < 0 || pg[3] < 0;
+    };
+    auto fixup = [&](int b, const int (&pg)[4], int buf) {
+        char *kl = smem + buf * St::BYTES, *vl = kl + St::KBYTES;
+        for (int i = tid; i < 4 * HD; i += 256) {           // value rows: (page, dim)
+            const int p = i / HD, d = i % HD;
+            const int first = b * St::KEYS + p * kPage;     // key of slot 0 of this page
+            const int keep = pg[p] < 0 ? 0 : max(0, min(kPage, kend - first));
+            for (int sl = keep; sl < kPage; ++sl)
+                *(uint16_t *)(vl + p * St::VPAGE + d * 32 + St::vchunk(d, sl / 8) * 16 + (sl % 8) * 2) = 0;
         }
-#pragma unroll
-        for (int i = 0; i < St::PER_THREAD; ++i) {
-            u32x4 v = stg[i];
-            const bool ok = hi_page[i] ? ok1 : ok0;
-            if (i < KI) {
-                if (!ok || blk * 32 + lo_key[i] >= kend) v = u32x4{0u, 0u, 0u, 0u};
-            } else {
-                const int nvalid = ok ? kend - (blk * 32 + lo_key[i]) : 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t m = (2 * e + 1 < nvalid) ? 0xffffffffu : ((2 * e < nvalid) ? 0xffffu : 0u);
-                    v[e] &= m;
-                }
-            }
-            *(u32x4 *)(buf + lds_off[i]) = v;
+        for (int i = tid; i < St::KEYS * St::KCH; i += 256) {   // key chunks of bad pages
+            const int row = i / St::KCH, c = i % St::KCH;
+            if (pg[row / kPage] < 0) *(u32x4 *)(kl + row * St::KRB + St::kchunk(row, c) * 16) = u32x4{0u, 0u, 0u, 0u};
         }
     };
 
@@ -607,114 +605,113 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     const float scale = kLog2e / sqrtf((float)HD);
     const int wave_first = off + qb + sb * 32;    // first query position of this wave
 
-    // page ids of block b, switching the LDS window when b leaves it (blocks never straddle a
-    // window: windows start at even pages); called at the same point by every thread
-    auto block_pages = [&](int b) -> int2 {
-        if (2 * b - w0 >= kPrefillPageWindow) {
-            __syncthreads();
-            w0 += kPrefillPageWindow;
-            load_window(w0);
-            __syncthreads();
-        }
-        return page_of(b);
-    };
     auto compute = [&](int kb) {
-        const char *buf = smem + (kb & 1) * St::BYTES;
-        if (rows > 0 && kb * 32 <= wave_first + rows - 1) {
-            const char *kl = buf, *vl = buf + 32 * St::KROW;
-            f32x16 s;
+        if (rows <= 0 || kb * St::KEYS > wave_first + rows - 1) return;   // past this wave's queries
+        const char *kl = smem + ((kb - kb0) & 1) * St::BYTES, *vl = kl + St::KBYTES;
+        // S^T = K Q^T for the two 32-key halves: two independent MFMA chains; lane's query = col,
+        // register e of half j holds key 32 j + 8 (e / 4) + 4 half + e % 4 of the block
+        f32x16 s[2];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) s[e] = 0.f;
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-                const bf16x8 kf = *(const bf16x8 *)(kl + col * St::KROW + (kk * 16 + half * 8) * 2);
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+            for (int e = 0; e < 16; ++e) s[j][e] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int row = 32 * j + col;
+                const bf16x8 kf = *(const bf16x8 *)(kl + row * St::KRB + St::kchunk(row, 2 * kk + half) * 16);
+                s[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[j], 0, 0, 0);
             }
-            // lane's query = col; register e holds key 8*(e/4) + 4*half + e%4 of the block
-            if ((kb + 1) * 32 > wave_first) {   // block reaches this wave's first query: mask
+        if ((kb + 1) * St::KEYS > wave_first) {   // block reaches this wave's first query: mask
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int kpos = kb * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                    if (kpos > qpos) s[e] = -INFINITY;
+                    const int kpos = kb * St::KEYS + 32 * j + (e >> 2) * 8 + half * 4 + (e & 3);
+                    if (kpos > qpos) s[j][e] = -INFINITY;
                 }
-            }
-            float mloc = s[0];
+        }
+        float mloc = s[0][0];
 #pragma unroll
-            for (int e = 1; e < 16; ++e) mloc = fmaxf(mloc, s[e]);
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale;
-            if (__ballot(mloc > m + 8.f) != 0) {
-                const float mn = fmaxf(m, mloc);
-                const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
-                l *= alpha;
+        for (int e = 1; e < 16; ++e) mloc = fmaxf(mloc, s[0][e]);
 #pragma unroll
-                for (int d = 0; d < DB; ++d)
+        for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, s[1][e]);
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale;
+        if (__ballot(mloc > m + 8.f) != 0) {
+            const float mn = fmaxf(m, mloc);
+            const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+            l *= alpha;
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) acc[d][e] *= alpha;
-                m = mn;
-            }
-            const float neg_m = (m == -INFINITY) ? 0.f : -m;
-            float p[16], psum = 0.f;
+            for (int d = 0; d < DB; ++d)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[d][e] *= alpha;
+            m = mn;
+        }
+        const float neg_m = (m == -INFINITY) ? 0.f : -m;
+        float psum = 0.f;
+        bf16x8 pf[2][2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            float p[16];
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                p[e] = __builtin_amdgcn_exp2f(fmaf(s[e], scale, neg_m));
+                p[e] = __builtin_amdgcn_exp2f(fmaf(s[j][e], scale, neg_m));
                 psum += p[e];
             }
-            psum += __shfl_xor(psum, 32, 64);
-            l += psum;
-            bf16x8 pf[2];
 #pragma unroll
             for (int k2 = 0; k2 < 2; ++k2) {
                 u32x4 w;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) w[q] = pack_bf16x2(p[k2 * 8 + 2 * q], p[k2 * 8 + 2 * q + 1]);
-                pf[k2] = __builtin_bit_cast(bf16x8, w);
+                pf[j][k2] = __builtin_bit_cast(bf16x8, w);
             }
-            // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; lane half `half` holds keys
-            // 16*k2 + 4*half .. +3 and 16*k2 + 8 + 4*half .. +3 of the block
+        }
+        psum += __shfl_xor(psum, 32, 64);
+        l += psum;
+        // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; for half j and k2, lane half `half`
+        // holds keys 4 half .. +3 and 8 + 4 half .. +3 of page 2 j + k2 of the block
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
                 for (int d = 0; d < DB; ++d) {
-                    const char *vrow = vl + (d * 32 + col) * St::VROW + k2 * 32;
-                    const uint64_t lo = *(const uint64_t *)(vrow + half * 8);
-                    const uint64_t hi = *(const uint64_t *)(vrow + 16 + half * 8);
+                    const int dim = d * 32 + col;
+                    const char *vrow = vl + (2 * j + k2) * St::VPAGE + dim * 32;
+                    const uint64_t lo = *(const uint64_t *)(vrow + St::vchunk(dim, 0) * 16 + half * 8);
+                    const uint64_t hi = *(const uint64_t *)(vrow + St::vchunk(dim, 1) * 16 + half * 8);
                     u32x4 vu = {(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
-                    acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pf[k2],
+                    acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pf[j][k2],
                                                                      acc[d], 0, 0, 0);
                 }
-        }
     };
+
     load_window(w0);
     __syncthreads();
-    int2 pg_b0 = page_of(kb0);
-    issue(stg0, pg_b0);
-    stash(stg0, smem, kb0, pg_b0);
-    int2 pg_b1 = kb0 + 1 < nkb ? page_of(kb0 + 1) : int2{-1, -1};
-    int2 pg_b2 = kb0 + 2 < nkb ? page_of(kb0 + 2) : int2{-1, -1};
-    // Every stage is loaded on every path, blocks past the tile's end from page 0 (never
-    // stashed): the load counter then advances alike on all paths, so the waits the compiler
-    // places before each stash cover that stage's loads only and leave the next stage's in
-    // flight (with conditional loads it waited for all of them).
-    issue(stg1, pg_b1);
-    issue(stg0, pg_b2);
-    __syncthreads();
-    // iteration kb: compute block kb, stash block kb + 1 from its stage, reuse that stage for
-    // block kb + 3; stage of block b is stg1 for odd b, stg0 for even b
-    for (int kb = kb0; kb < nkb; kb += 2) {
+    int pg_cur[4];
+    block_pages(kb0, pg_cur);
+    issue(pg_cur, 0);
+    for (int kb = kb0; kb < nkb; ++kb) {
+        // this wave's copies of block kb have landed; the barrier: everyone's have, and everyone
+        // is done with block kb - 1, whose buffer the next copies refill
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        const bool fix = needs_fixup(kb, pg_cur);
+        int pg_nxt[4];
+        if (kb + 1 < nkb) {
+            block_pages(kb + 1, pg_nxt);
+            issue(pg_nxt, (kb + 1 - kb0) & 1);
+        }
+        if (fix) {
+            fixup(kb, pg_cur, (kb - kb0) & 1);
+            __syncthreads();
+        }
         compute(kb);
-        if (kb + 1 < nkb) stash(stg1, smem + St::BYTES, kb + 1, pg_b1);
-        const int2 pg_b3 = kb + 3 < nkb ? block_pages(kb + 3) : int2{-1, -1};
-        issue(stg1, pg_b3);
-        __syncthreads();
-        // a guarded block, not a loop exit: an exit here gave the compiler a path into the next
-        // iteration on which the stage just issued is the newest, and its waits for every stage
-        if (kb + 1 < nkb) compute(kb + 1);
-        if (kb + 2 < nkb) stash(stg0, smem, kb + 2, pg_b2);
-        const int2 pg_b4 = kb + 4 < nkb ? block_pages(kb + 4) : int2{-1, -1};
-        issue(stg0, pg_b4);
-        __syncthreads();
-        pg_b1 = pg_b3;
-        pg_b2 = pg_b4;
+        if (kb + 1 < nkb) {
+#pragma unroll
+            for (int p = 0; p < 4; ++p) pg_cur[p] = pg_nxt[p];
+        }
     }
     if (col >= rows) return;
     if (pslot >= 0) {
