@@ -10,14 +10,13 @@
 //   * prefill items (rows of embedding and generation prefill chunks, heaviest first; each
 //     chunk reads the cache of its own model): (128 / group) tokens of one chunk
 //     times the `group` query heads of one KV head; each wave owns 32 query rows of one head
-//     and walks the keys of its request in 32-key blocks that the workgroup stages in LDS
-//     (two buffers, the next blocks' loads in registers, one barrier per block; the block is
-//     shared by the group's waves), with an online softmax in fp32 (exp2 domain) and causal
-//     masking on the diagonal blocks; a wave past its causal bound skips the block's
-//     arithmetic.  A tile over a long cached prefix comes as several items, one per run of
-//     keys (the walk is serial, about a microsecond and a half per 32-key block, so one long
-//     tile would otherwise set the launch's length); those write partials like split decode
-//     rows, merged by attn_combine.
+//     and walks the keys of its request in 64-key blocks that the workgroup copies straight
+//     into LDS (two buffers, one barrier per block; the block is shared by the group's waves),
+//     with an online softmax in fp32 (exp2 domain) and causal masking on the diagonal blocks; a
+//     wave past its causal bound skips the block's arithmetic.  A tile over a long cached
+//     prefix comes as several items, one per run of keys (the walk is serial, so one long tile
+//     would otherwise set the launch's length); those write partials like split decode rows,
+//     merged by attn_combine.
 //   * decode items: one (decode row, KV head, key-range split), walked in 128-key chunks (64
 //     in the decode-only kernel).  Each wave owns two pages of a chunk (one), scores with
 //     v_dot2_f32_bf16 for all `group` query heads at once, keeps an online softmax, and
