@@ -80,6 +80,9 @@ def test_long_prefix_prefill_key_splits():
     pieces = items[:npre][items[:npre, 7] >= 0]
     # chunk 0's tiles in 3 pieces (6032..6070 keys, 2048-key target), chunk 1's in 2
     assert len(pieces) == 2 * (3 * 3 + 2 * 2), pieces
+    # some pieces start on an odd 64-key block (the kernel's LDS buffers alternate from a
+    # piece's own first block, not from block 0)
+    assert any((int(p[5]) // 64) % 2 == 1 for p in pieces), pieces[:, 5]
     pair.step(b)
     print(pair.report, flush=True)
 
