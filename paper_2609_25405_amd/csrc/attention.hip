@@ -607,18 +607,22 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
     auto compute = [&](int kb) {
         if (rows <= 0 || kb * St::KEYS > wave_first + rows - 1) return;   // past this wave's queries
         const char *kl = smem + ((kb - kb0) & 1) * St::BYTES, *vl = kl + St::KBYTES;
-        // S^T = K Q^T for the two 32-key halves: two independent MFMA chains; lane's query = col,
-        // register e of half j holds key 32 j + 8 (e / 4) + 4 half + e % 4 of the block
+        // S^T = K Q^T for the two 32-key halves: two independent MFMA chains; lane's query = col.
+        // Row r of half j's operand is key 32 j + (r with bits 2 and 3 swapped), so register e
+        // of half j holds key 32 j + 16 (e / 8) + 8 half + 4 (e / 4 % 2) + e % 4: the eight
+        // probabilities a lane packs for one page are then its slots 8 half .. 8 half + 7, one
+        // 16-byte chunk of each value row
         f32x16 s[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) s[j][e] = 0.f;
+        const int kcol = col ^ ((((col >> 2) ^ (col >> 3)) & 1) * 12);
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                const int row = 32 * j + col;
+                const int row = 32 * j + kcol;
                 const bf16x8 kf = *(const bf16x8 *)(kl + row * St::KRB + St::kchunk(row, 2 * kk + half) * 16);
                 s[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[j], 0, 0, 0);
             }
@@ -627,7 +631,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
             for (int j = 0; j < 2; ++j)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int kpos = kb * St::KEYS + 32 * j + (e >> 2) * 8 + half * 4 + (e & 3);
+                    const int kpos = kb * St::KEYS + 32 * j + (e >> 3) * 16 + half * 8 + ((e >> 2) & 1) * 4 + (e & 3);
                     if (kpos > qpos) s[j][e] = -INFINITY;
                 }
         }
@@ -669,7 +673,7 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
         psum += __shfl_xor(psum, 32, 64);
         l += psum;
         // O^T[dim][query] += V^T[dim][keys] P^T[keys][query]; for half j and k2, lane half `half`
-        // holds keys 4 half .. +3 and 8 + 4 half .. +3 of page 2 j + k2 of the block
+        // holds slots 8 half .. 8 half + 7 of page 2 j + k2 of the block
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -677,12 +681,8 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
 #pragma unroll
                 for (int d = 0; d < DB; ++d) {
                     const int dim = d * 32 + col;
-                    const char *vrow = vl + (2 * j + k2) * St::VPAGE + dim * 32;
-                    const uint64_t lo = *(const uint64_t *)(vrow + St::vchunk(dim, 0) * 16 + half * 8);
-                    const uint64_t hi = *(const uint64_t *)(vrow + St::vchunk(dim, 1) * 16 + half * 8);
-                    u32x4 vu = {(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
-                    acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pf[j][k2],
-                                                                     acc[d], 0, 0, 0);
+                    const bf16x8 vf = *(const bf16x8 *)(vl + (2 * j + k2) * St::VPAGE + dim * 32 + St::vchunk(dim, half) * 16);
+                    acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j][k2], acc[d], 0, 0, 0);
                 }
     };
 
