@@ -783,8 +783,8 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnArgs a) {
 }
 
 // Merge key-range partials in split order: M = max m_s, L = sum l_s 2^(m_s - M),
-// o = sum acc_s 2^(m_s - M) / L.  Blocks [0, n_dec_blocks): one (decode row, KV head) each, for
-// its `group` query heads; then kCombineRows rows of one key-split prefill tile per block.  Up to
+// o = sum acc_s 2^(m_s - M) / L.  Blocks [0, n_dec_blocks): one (split decode row, KV head)
+// each, for its `group` query heads (rows with one split wrote their output directly); then kCombineRows rows of one key-split prefill tile per block.  Up to
 // kCombineSplits splits are loaded in one round before any arithmetic (a block is a single
 // memory round trip), longer decode rows loop.
 constexpr int kCombineRows = 4;
@@ -831,7 +831,7 @@ template <typename T, int HD, int G>
 __global__ __launch_bounds__(G * HD) void attn_combine_kernel(AttnArgs a, int n_dec_blocks) {
     const int h = threadIdx.x / HD, d = threadIdx.x % HD;
     if ((int)blockIdx.x < n_dec_blocks) {
-        const int j = blockIdx.x / a.nkv, g = blockIdx.x % a.nkv;
+        const int j = a.split_rows[blockIdx.x / a.nkv], g = blockIdx.x % a.nkv;
         const int32_t *row = a.rows + kRowInts * j;
         const int nsplit = row[3];
         if (nsplit <= 1) return;

@@ -171,6 +171,7 @@ struct AttnArgs {
     const int32_t *block_table[2];
     int n_pages[2], max_blocks[2];
     const int32_t *chunks, *rows, *items;
+    const int32_t *split_rows;  // indices of the decode rows with more than one split
     const int32_t *combine;   // merge entries of key-split prefill tiles
     float *partials;          // [slot][group][hd + 2]
     // n_prefill: prefill items at the head of `items` (0: decode items only, served by the
@@ -179,8 +180,8 @@ struct AttnArgs {
     int *err;
 };
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
-// merges the partials of split decode rows (the first n_decode rows' entries; 0 = none) and of
-// the a.n_combine key-split prefill tiles
+// merges the partials of the n_decode decode rows listed in a.split_rows (0 = none) and of the
+// a.n_combine key-split prefill tiles
 hipError_t launch_attn_combine(int dtype, const AttnArgs &a, int n_decode, hipStream_t s);
 
 struct PoolArgs {

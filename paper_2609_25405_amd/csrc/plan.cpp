@@ -299,7 +299,8 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     p.off_items = p.off_rows + kRowInts * p.D;
     p.off_lm = p.off_items + (int)items.size();
     p.off_combine = p.off_lm + p.n_lm;
-    int end = p.off_combine + (int)combine.size();
+    p.off_split = p.off_combine + (int)combine.size();
+    int end = p.off_split + p.n_split_rows;
     if (p.any_wmean) {
         p.off_wts = end;
         end += p.Te;
@@ -350,6 +351,8 @@ int plan_step(const Model &emb, const Model &gen, const orthrus_batch &b, const 
     std::copy(rows.begin(), rows.end(), p.meta.begin() + p.off_rows);
     std::copy(items.begin(), items.end(), p.meta.begin() + p.off_items);
     std::copy(combine.begin(), combine.end(), p.meta.begin() + p.off_combine);
+    for (int j = 0, k = 0; j < p.D; ++j)
+        if (rows[kRowInts * j + 3] > 1) p.meta[p.off_split + k++] = j;
     return ORTHRUS_OK;
 }
 

@@ -77,11 +77,12 @@ struct StepPlan {
     int n_used = 0;
     int used[ORTHRUS_MAX_STEP_ADAPTERS] = {0, 0, 0, 0};
     int off_radp = -1;
-    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows combine, then
+    // packed metadata, uploaded verbatim: tok[T] pos[T] seq[T] chunks rows items lm_rows combine
+    // split_rows (the n_split_rows decode rows with more than one split, in row order), then
     // (weighted mean) fp32 weights[Te] and (buffered head) hidden-buffer row[Te] (-1: none)
     std::vector<int32_t> meta;
     int off_tok = 0, off_pos = 0, off_seq = 0, off_chunks = 0, off_rows = 0, off_items = 0,
-        off_lm = 0, off_combine = 0, off_wts = -1, off_hid = -1;
+        off_lm = 0, off_combine = 0, off_split = 0, off_wts = -1, off_hid = -1;
 };
 
 int validate_config(const orthrus_config &c);

@@ -291,7 +291,9 @@ size_t orthrus_workspace_bytes(const orthrus_model *emb, const orthrus_model *ge
                         kRowInts * (size_t)max_decode + kItemInts * (pre_items + dec_items + pieces) +
                         kCombineInts * (pieces / 2) +
                         (size_t)max_chunks + max_decode +  // rows that get logits
-                        2 * (size_t)max_tokens;            // token weights, hidden-buffer rows
+                        max_decode +                       // decode rows with several splits
+                        3 * (size_t)max_tokens;            // token weights, hidden-buffer rows,
+                                                           // adapter positions
     return make_layout(m, max_tokens, meta, dec_items + pieces * qrows).total;
 }
 
@@ -555,6 +557,7 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
     aa.rows = meta + p.off_rows;
     aa.items = meta + p.off_items;
     aa.combine = meta + p.off_combine;
+    aa.split_rows = meta + p.off_split;
     aa.n_combine = p.n_split_prefill;
     aa.partials = (float *)(ws + L.partials);
     aa.n_prefill = p.n_prefill;
@@ -623,7 +626,7 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
             ag.n_items = aa.n_items - p.n_pre_emb;
             ag.combine = aa.combine + kCombineInts * p.n_merge_emb;
             ag.n_combine = merges_gen;
-            n_dec = p.n_split_rows > 0 ? p.D : 0;
+            n_dec = p.n_split_rows;
         }
         return combine ? launch_attn_combine(dt, ag, n_dec, groups[gi].st) : launch_attention(dt, ag, groups[gi].st);
     };
@@ -731,7 +734,7 @@ int step_impl(const orthrus_model *emb, const orthrus_model *gen, const orthrus_
         } else {
             RUN("attention", launch_attention(dt, aa, s));
             if (p.n_split_rows > 0 || p.n_split_prefill > 0)
-                RUN("attn_combine", launch_attn_combine(dt, aa, p.n_split_rows > 0 ? p.D : 0, s));
+                RUN("attn_combine", launch_attn_combine(dt, aa, p.n_split_rows, s));
         }
         int splits = add_splits(qd);
         for (int gi = 0; gi < n_groups; ++gi) {
