@@ -118,6 +118,31 @@ def test_gqa_long_context_splits(dtype):
     print(pair.report, flush=True)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_split_and_single_decode_rows_together(dtype):
+    """Decode rows with one key split (written by the attention launch itself) next to rows
+    with two and three splits (merged by the launch over the split rows only), beside a chunk."""
+    cfg = _gqa_config(dtype)
+    W = make_weights(cfg, 8, qk_std=0.06 if dtype == "bf16" else 0.15)
+    n_seq, max_blocks = 5, 136
+    pk = PagedKV(cfg, n_seq * max_blocks + 3, n_seq, max_blocks, 8)
+    ctx = [50, 1100, 300, 2100]
+    for i, c in enumerate(ctx):
+        pk.fill_random(1 + i, c, 8)
+        pk.reserve(1 + i, c + 1)
+    pk.reserve(0, 96)
+    pair = Pair(cfg, W, pk)
+    pair.workspace(max_tokens=128, max_chunks=1, max_decode=4, max_ctx=2176)
+    rows = [DecodeRow(1 + i, c) for i, c in enumerate(ctx)]
+    b = Batch([EmbChunk(0, 0, 96, True, "mean")], rows, draw_tokens(8, 1, 100, cfg.vocab))
+    npre, _, items = R.plan(pair.dm_e, pair.dm_e, b, pair.dkv_e, pair.dkv_e)
+    dec = items[npre:]
+    splits = [int(dec[dec[:, 1] == j, 4].max()) for j in range(len(rows))]
+    assert splits == ([1, 2, 1, 3] if dtype == "bf16" else [1, 5, 2, 9]), splits
+    pair.step(b)
+    print(pair.report, flush=True)
+
+
 def test_two_models_two_pools():
     """Separate embedding and generation models (same shape) with separate caches."""
     cfg = tiny_config("bf16")
