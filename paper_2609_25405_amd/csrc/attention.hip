@@ -681,7 +681,8 @@ __device__ void prefill_item_mfma(const AttnArgs &a, const int32_t *it, char *sm
 #pragma unroll
                 for (int d = 0; d < DB; ++d) {
                     const int dim = d * 32 + col;
-                    const bf16x8 vf = *(const bf16x8 *)(vl + (2 * j + k2) * St::VPAGE + dim * 32 + St::vchunk(dim, half) * 16);
+                    const bf16x8 vf =
+                        *(const bf16x8 *)(vl + (2 * j + k2) * St::VPAGE + dim * 32 + St::vchunk(dim, half) * 16);
                     acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j][k2], acc[d], 0, 0, 0);
                 }
     };
@@ -784,9 +785,10 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnArgs a) {
 
 // Merge key-range partials in split order: M = max m_s, L = sum l_s 2^(m_s - M),
 // o = sum acc_s 2^(m_s - M) / L.  Blocks [0, n_dec_blocks): one (split decode row, KV head)
-// each, for its `group` query heads (rows with one split wrote their output directly); then kCombineRows rows of one key-split prefill tile per block.  Up to
-// kCombineSplits splits are loaded in one round before any arithmetic (a block is a single
-// memory round trip), longer decode rows loop.
+// each, for its `group` query heads (rows with one split wrote their output directly); then
+// kCombineRows rows of one key-split prefill tile per block.  Up to kCombineSplits splits are
+// loaded in one round before any arithmetic (a block is a single memory round trip), longer
+// decode rows loop.
 constexpr int kCombineRows = 4;
 constexpr int kCombineSplits = 8;
 static_assert(kMaxPrefillSplits <= kCombineSplits, "prefill pieces load in one round");
